@@ -1,0 +1,132 @@
+/*
+ * libsfda -- Semidirect Fourier Delta Attention (SFDA) forward and decode on AMD MI355X (gfx950).
+ *
+ * Plain C ABI: device pointers, sizes and a HIP stream passed as an opaque pointer.  No C++,
+ * HIP or framework types cross this boundary.
+ *
+ * The operation (Sec. 3, Eq. (sfda) and the readout that follows it), per batch b and head h,
+ * over complex coordinates, with x^* the conjugate transpose:
+ *
+ *   Lambda_t = diag(alpha_t * exp(i theta_t))             alpha_t, theta_t real, m channels
+ *   S_t      = (I - beta_t k_t k_t^*) Lambda_t S_{t-1} + beta_t k_t v_t^*      S_t in C^{m x n}
+ *   o_t      = S_t^* q_t                                  (state after token t's update)
+ *
+ * so that (k v^*)_{ij} = k_i conj(v_j) and o_{t,j} = sum_i conj(S_t[i][j]) q_t[i].
+ *
+ * Memory layouts (row-major, contiguous; complex = interleaved (re, im) scalar pairs):
+ *   q, k          [B, H, T, m] complex     v, o   [B, H, T, n] complex
+ *   alpha, theta  [B, H, T, m] real        beta   [B, H, T]    real
+ *   S0, S_T, S    [B, H, m, n] complex, always float32
+ * Element type of q, k, v, alpha, theta, beta is `in_dtype`; of o it is `out_dtype`.
+ * For the decode step drop the T axis: q, k [B, H, m], v, o [B, H, n], alpha, theta [B, H, m],
+ * beta [B, H].
+ *
+ * Ownership: the caller allocates and frees every buffer and owns the stream; the library
+ * allocates no device memory and keeps no state between calls (calls are reentrant; calls
+ * that write the same buffers on different streams race, as any two kernels would).
+ *
+ * Errors: all argument checks run on the host before anything is enqueued; on any error
+ * nothing is launched and a status code is returned.  A launch failure returns
+ * SFDA_ERR_HIP.  Faults inside a kernel surface at the caller's next synchronisation.
+ * Nothing aborts, throws or prints.
+ *
+ * Determinism: no atomics; for identical inputs, sizes and dtypes results are bitwise
+ * identical from run to run.
+ */
+#ifndef SFDA_H
+#define SFDA_H
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SFDA_ABI_VERSION 1
+
+typedef enum { SFDA_F32 = 0, SFDA_BF16 = 1 } sfda_dtype_t;
+
+typedef enum {
+    SFDA_OK = 0,
+    SFDA_ERR_NULL = 1,   /* a required pointer is NULL                                   */
+    SFDA_ERR_SHAPE = 2,  /* a size is out of range (see each entry point)                 */
+    SFDA_ERR_CHUNK = 3,  /* chunk length C not supported                                  */
+    SFDA_ERR_DTYPE = 4,  /* unknown dtype                                                 */
+    SFDA_ERR_ALIGN = 5,  /* a pointer is not 16-byte aligned                              */
+    SFDA_ERR_ALIAS = 6,  /* an output overlaps an input or another output                 */
+    SFDA_ERR_HIP = 7     /* the HIP runtime reported an error when launching              */
+} sfda_status_t;
+
+/* A hipStream_t passed as an opaque pointer; NULL means the default (null) stream. */
+typedef void* sfda_stream_t;
+
+/*
+ * sfda_chunk_fwd -- the whole forward pass over T tokens, evaluated chunk by chunk through
+ * the constructive chunk-WY factorisation P = Gamma - Y M W^* (Thm 4.2, Cor. 4.3) with the
+ * exact affine chunk transfer (Thm 4.4), the intra-chunk prefix outputs (Thm 4.5) and a
+ * sequential boundary-state scan across chunks (Thm 6.1, eq. (apply-transfer)).  The result
+ * equals the token-by-token recurrence above up to floating-point rounding.
+ *
+ *   q, k, v, alpha, theta, beta : inputs (device, in_dtype), layouts above.
+ *   S0   : initial state [B,H,m,n] complex float32, or NULL for the zero state.
+ *   o    : output [B,H,T,n] complex (device, out_dtype); every element is written.
+ *   S_T  : state after token T [B,H,m,n] complex float32, or NULL if not wanted.
+ *          S_T == S0 (same pointer) is allowed and updates the state in place; any other
+ *          overlap between S_T and another buffer is SFDA_ERR_ALIAS.
+ *   B, H >= 0 (B*H == 0 is a no-op); T >= 0 (T == 0 writes S_T = S0, or zeros);
+ *   1 <= m <= 64; n >= 1; C in {16, 32, 64} (SFDA_ERR_CHUNK otherwise).  The last chunk may
+ *   be ragged (T mod C != 0).
+ *   Numerical range: the chunk factorisation divides by the in-chunk cumulative decay, so
+ *   prod over any C consecutive tokens of alpha_t[i] must stay above about 1e-30 for every
+ *   channel i (e.g. alpha >= 0.35 for C = 64, alpha >= 0.014 for C = 16); alpha must be > 0.
+ *   Accumulation and state are float32 for both dtypes; with in_dtype == SFDA_BF16 the
+ *   matrix products take bfloat16 operands.
+ */
+sfda_status_t sfda_chunk_fwd(const void* q, const void* k, const void* v,
+                             const void* alpha, const void* theta, const void* beta,
+                             const float* S0, void* o, float* S_T,
+                             int B, int H, int T, int m, int n, int C,
+                             sfda_dtype_t in_dtype, sfda_dtype_t out_dtype,
+                             sfda_stream_t stream);
+
+/*
+ * sfda_chunk_fwd_sliced -- sfda_chunk_fwd with an explicit number of value columns per
+ * workgroup, `slice` (a multiple of 8 in [8, 64]; SFDA_ERR_SHAPE otherwise).  The n value
+ * columns are independent in the recurrence (column j of S only mixes with column j of
+ * v^*), so the library splits them into ceil(n / slice) workgroups per (b, h); a smaller
+ * slice gives more workgroups at the cost of repeating the chunk factors per slice.
+ * sfda_chunk_fwd uses slice = min(64, n rounded up to a multiple of 8).  Results are the
+ * same up to rounding for every slice.
+ */
+sfda_status_t sfda_chunk_fwd_sliced(const void* q, const void* k, const void* v,
+                                    const void* alpha, const void* theta, const void* beta,
+                                    const float* S0, void* o, float* S_T,
+                                    int B, int H, int T, int m, int n, int C, int slice,
+                                    sfda_dtype_t in_dtype, sfda_dtype_t out_dtype,
+                                    sfda_stream_t stream);
+
+/*
+ * sfda_step -- one recurrent decode token per (b, h) (Sec. 3, Eq. (sfda) and the readout),
+ * updating the state in place:
+ *   S <- (I - beta k k^*) Lambda S + beta k v^*,   o = S^* q   (post-update S).
+ *
+ *   q, k, v, alpha, theta, beta : one token per head (device, in_dtype), layouts above.
+ *   S : [B,H,m,n] complex float32, read and overwritten.
+ *   o : [B,H,n] complex (device, out_dtype).  o must not overlap S or any input.
+ *   B, H >= 0; 1 <= m <= 64; n >= 1.
+ */
+sfda_status_t sfda_step(const void* q, const void* k, const void* v,
+                        const void* alpha, const void* theta, const void* beta,
+                        float* S, void* o, int B, int H, int m, int n,
+                        sfda_dtype_t in_dtype, sfda_dtype_t out_dtype,
+                        sfda_stream_t stream);
+
+/* Static, human-readable text for a status code. */
+const char* sfda_status_string(sfda_status_t s);
+
+/* SFDA_ABI_VERSION of the built library. */
+int sfda_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SFDA_H */

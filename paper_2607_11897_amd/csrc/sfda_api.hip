@@ -1,0 +1,156 @@
+// C-ABI entry points of libsfda: argument validation, then one kernel launch.
+#include <stdint.h>
+
+#include "../../include/sfda.h"
+#include "sfda_launch.h"
+
+namespace {
+
+struct Range {
+    uintptr_t lo, hi;   // [lo, hi)
+};
+
+Range range_of(const void* p, long bytes) {
+    const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+    return Range{a, a + static_cast<uintptr_t>(bytes > 0 ? bytes : 0)};
+}
+
+bool overlap(Range a, Range b) {
+    return a.lo < a.hi && b.lo < b.hi && a.lo < b.hi && b.lo < a.hi;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+long esize(sfda_dtype_t d) { return d == SFDA_BF16 ? 2 : 4; }
+
+bool dtype_ok(sfda_dtype_t d) { return d == SFDA_F32 || d == SFDA_BF16; }
+
+}  // namespace
+
+extern "C" {
+
+const char* sfda_status_string(sfda_status_t s)
+{
+    switch (s) {
+        case SFDA_OK: return "ok";
+        case SFDA_ERR_NULL: return "a required pointer is NULL";
+        case SFDA_ERR_SHAPE: return "a size is out of range";
+        case SFDA_ERR_CHUNK: return "unsupported chunk length (C must be 16, 32 or 64)";
+        case SFDA_ERR_DTYPE: return "unsupported dtype";
+        case SFDA_ERR_ALIGN: return "a pointer is not 16-byte aligned";
+        case SFDA_ERR_ALIAS: return "an output buffer overlaps another buffer";
+        case SFDA_ERR_HIP: return "the HIP runtime reported an error";
+    }
+    return "unknown status";
+}
+
+int sfda_abi_version(void) { return SFDA_ABI_VERSION; }
+
+static sfda_status_t chunk_fwd_impl(const void* q, const void* k, const void* v,
+                                    const void* alpha, const void* theta, const void* beta,
+                                    const float* S0, void* o, float* S_T, int B, int H, int T,
+                                    int m, int n, int C, sfda_dtype_t in_dtype,
+                                    sfda_dtype_t out_dtype, sfda_stream_t stream, int slice)
+{
+    if (!dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return SFDA_ERR_DTYPE;
+    if (B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1) return SFDA_ERR_SHAPE;
+    if (C != 16 && C != 32 && C != 64) return SFDA_ERR_CHUNK;
+    if (slice < 8 || slice > 64 || (slice & 7) != 0) return SFDA_ERR_SHAPE;
+    const long BH = static_cast<long>(B) * H;
+    if (BH * ((n + slice - 1) / slice) > 0x7FFFFFFFL) return SFDA_ERR_SHAPE;
+    if (BH == 0) return SFDA_OK;
+    const bool need_inputs = T > 0;
+    if (need_inputs && (!q || !k || !v || !alpha || !theta || !beta || !o)) return SFDA_ERR_NULL;
+    const void* ptrs[] = {q, k, v, alpha, theta, beta, S0, o, S_T};
+    for (const void* p : ptrs)
+        if (p && !aligned16(p)) return SFDA_ERR_ALIGN;
+
+    const long ei = esize(in_dtype), eo = esize(out_dtype);
+    const long BHT = BH * T;
+    const Range rq = range_of(q, BHT * m * 2 * ei), rk = range_of(k, BHT * m * 2 * ei);
+    const Range rv = range_of(v, BHT * n * 2 * ei);
+    const Range ra = range_of(alpha, BHT * m * ei), rt = range_of(theta, BHT * m * ei);
+    const Range rb = range_of(beta, BHT * ei);
+    const Range ro = range_of(o, BHT * n * 2 * eo);
+    const Range rs0 = range_of(S0, BH * m * n * 2 * 4);
+    const Range rst = range_of(S_T, BH * m * n * 2 * 4);
+    const Range ins[] = {rq, rk, rv, ra, rt, rb};
+    if (need_inputs) {
+        for (const Range& r : ins)
+            if (overlap(ro, r)) return SFDA_ERR_ALIAS;
+        if (overlap(ro, rs0) || overlap(ro, rst)) return SFDA_ERR_ALIAS;
+    }
+    if (S_T) {
+        if (need_inputs)
+            for (const Range& r : ins)
+                if (overlap(rst, r)) return SFDA_ERR_ALIAS;
+        if (S0 && static_cast<const void*>(S0) != static_cast<const void*>(S_T) && overlap(rs0, rst))
+            return SFDA_ERR_ALIAS;
+    }
+
+    sfda::ChunkLaunch L;
+    L.q = q; L.k = k; L.v = v; L.alpha = alpha; L.theta = theta; L.beta = beta;
+    L.S0 = S0; L.o = o; L.S_T = S_T;
+    L.B = B; L.H = H; L.T = T; L.m = m; L.n = n; L.C = C; L.slice = slice;
+    L.in_bf16 = in_dtype == SFDA_BF16;
+    L.out_bf16 = out_dtype == SFDA_BF16;
+    const hipError_t e = sfda::launch_chunk(L, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? SFDA_OK : SFDA_ERR_HIP;
+}
+
+sfda_status_t sfda_chunk_fwd(const void* q, const void* k, const void* v, const void* alpha,
+                             const void* theta, const void* beta, const float* S0, void* o,
+                             float* S_T, int B, int H, int T, int m, int n, int C,
+                             sfda_dtype_t in_dtype, sfda_dtype_t out_dtype, sfda_stream_t stream)
+{
+    const int slice = n <= 64 ? ((n + 7) / 8) * 8 : 64;
+    return chunk_fwd_impl(q, k, v, alpha, theta, beta, S0, o, S_T, B, H, T, m, n, C, in_dtype,
+                          out_dtype, stream, slice);
+}
+
+sfda_status_t sfda_chunk_fwd_sliced(const void* q, const void* k, const void* v,
+                                    const void* alpha, const void* theta, const void* beta,
+                                    const float* S0, void* o, float* S_T, int B, int H, int T,
+                                    int m, int n, int C, int slice, sfda_dtype_t in_dtype,
+                                    sfda_dtype_t out_dtype, sfda_stream_t stream)
+{
+    return chunk_fwd_impl(q, k, v, alpha, theta, beta, S0, o, S_T, B, H, T, m, n, C, in_dtype,
+                          out_dtype, stream, slice);
+}
+
+sfda_status_t sfda_step(const void* q, const void* k, const void* v, const void* alpha,
+                        const void* theta, const void* beta, float* S, void* o, int B, int H,
+                        int m, int n, sfda_dtype_t in_dtype, sfda_dtype_t out_dtype,
+                        sfda_stream_t stream)
+{
+    if (!dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return SFDA_ERR_DTYPE;
+    if (B < 0 || H < 0 || m < 1 || m > 64 || n < 1) return SFDA_ERR_SHAPE;
+    const long BH = static_cast<long>(B) * H;
+    int np = 1;
+    while (np < n && np < 64) np <<= 1;
+    if (BH * ((n + np - 1) / np) > 0x7FFFFFFFL) return SFDA_ERR_SHAPE;
+    if (BH == 0) return SFDA_OK;
+    if (!q || !k || !v || !alpha || !theta || !beta || !S || !o) return SFDA_ERR_NULL;
+    const void* ptrs[] = {q, k, v, alpha, theta, beta, S, o};
+    for (const void* p : ptrs)
+        if (!aligned16(p)) return SFDA_ERR_ALIGN;
+    const long ei = esize(in_dtype), eo = esize(out_dtype);
+    const Range ins[] = {range_of(q, BH * m * 2 * ei), range_of(k, BH * m * 2 * ei),
+                         range_of(v, BH * n * 2 * ei), range_of(alpha, BH * m * ei),
+                         range_of(theta, BH * m * ei), range_of(beta, BH * ei)};
+    const Range rs = range_of(S, BH * m * n * 2 * 4);
+    const Range ro = range_of(o, BH * n * 2 * eo);
+    if (overlap(ro, rs)) return SFDA_ERR_ALIAS;
+    for (const Range& r : ins)
+        if (overlap(ro, r) || overlap(rs, r)) return SFDA_ERR_ALIAS;
+
+    sfda::StepLaunch L;
+    L.q = q; L.k = k; L.v = v; L.alpha = alpha; L.theta = theta; L.beta = beta;
+    L.S = S; L.o = o; L.B = B; L.H = H; L.m = m; L.n = n;
+    L.in_bf16 = in_dtype == SFDA_BF16;
+    L.out_bf16 = out_dtype == SFDA_BF16;
+    const hipError_t e = sfda::launch_step(L, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? SFDA_OK : SFDA_ERR_HIP;
+}
+
+}  // extern "C"

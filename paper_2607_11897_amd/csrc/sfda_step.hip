@@ -1,0 +1,164 @@
+// Recurrent decode step of SFDA (Sec. 3, Eq. (sfda) and the readout o = S^* q), one token
+// per (batch, head), state updated in place.
+//
+// Per head, with S' = Lambda S (row i scaled by lambda_i = alpha_i e^{i theta_i}):
+//   a = k^* S'            (1 x n)      b = q^* S'            (1 x n)
+//   delta = beta (conj(v) - a)          so S = S' + k delta  (= (I - beta k k^*) S' + beta k v^*)
+//   o = S^* q = conj(b + (q^* k) delta)
+// which reads S once and writes it once -- the step is bound by HBM bandwidth.
+//
+// Launch: one 256-thread workgroup per (head, slice of NP value columns); NP is a power of
+// two <= 64.  Thread (rg, j) owns column j and rows rg, rg + G, rg + 2G, ... (G = 256 / NP),
+// so each wave reads and writes whole contiguous row segments.  Column sums over rows are
+// reduced in a fixed order through LDS (deterministic; no atomics).
+#include "sfda_device.h"
+#include "sfda_launch.h"
+
+namespace sfda {
+
+template <typename TIN, typename TOUT, int NP>
+__global__ __launch_bounds__(256) void step_kernel(
+    const TIN* __restrict__ q, const TIN* __restrict__ k, const TIN* __restrict__ v,
+    const TIN* __restrict__ alpha, const TIN* __restrict__ theta, const TIN* __restrict__ beta,
+    float* __restrict__ S, TOUT* __restrict__ o, int m, int n, int n_slices)
+{
+    constexpr int G = 256 / NP;                 // row groups
+    constexpr int RPT = (64 + G - 1) / G;       // rows per thread (m <= 64)
+    const long bh = blockIdx.x / n_slices;
+    const int sl = blockIdx.x - static_cast<int>(bh) * n_slices;
+    const int tid = threadIdx.x;
+    const int jl = tid % NP;
+    const int rg = tid / NP;
+    const int j = sl * NP + jl;
+    const bool colok = j < n;
+
+    __shared__ float2 lam_s[64], k_s[64], q_s[64];
+    __shared__ float2 red_a[G][NP], red_b[G][NP];
+    __shared__ float2 delta_s[NP];
+    __shared__ float2 qk_s;
+
+    // state loads first, so their latency overlaps the small per-head set-up below
+    float* Sh = S + bh * m * n * 2;
+    float2 s[RPT];
+#pragma unroll
+    for (int r = 0; r < RPT; ++r) {
+        const int i = rg + G * r;
+        s[r] = (i < m && colok) ? *reinterpret_cast<const float2*>(Sh + 2 * (static_cast<long>(i) * n + j))
+                                : make_float2(0.f, 0.f);
+    }
+
+    if (tid < 64) {
+        float2 qk = make_float2(0.f, 0.f);
+        if (tid < m) {
+            const long e = bh * m + tid;
+            const float a = Elem<TIN>::load(alpha, e);
+            float sn, cs;
+            sincosf(Elem<TIN>::load(theta, e), &sn, &cs);
+            lam_s[tid] = make_float2(a * cs, a * sn);
+            const float2 kk = Elem<TIN>::load2(k, e);
+            const float2 qq = Elem<TIN>::load2(q, e);
+            k_s[tid] = kk;
+            q_s[tid] = qq;
+            qk = make_float2(qq.x * kk.x + qq.y * kk.y, qq.x * kk.y - qq.y * kk.x);  // conj(q) k
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+            qk.x += __shfl_xor(qk.x, off);
+            qk.y += __shfl_xor(qk.y, off);
+        }
+        if (tid == 0) qk_s = qk;
+    }
+    __syncthreads();
+
+    // S' = Lambda S and the column partial sums a = k^* S', b = q^* S'
+    float2 pa = make_float2(0.f, 0.f), pb = make_float2(0.f, 0.f);
+#pragma unroll
+    for (int r = 0; r < RPT; ++r) {
+        const int i = rg + G * r;
+        if (i < m) {
+            const float2 l = lam_s[i];
+            const float2 x = s[r];
+            const float2 y = make_float2(l.x * x.x - l.y * x.y, l.x * x.y + l.y * x.x);
+            s[r] = y;
+            const float2 kk = k_s[i];
+            const float2 qq = q_s[i];
+            pa.x += kk.x * y.x + kk.y * y.y;
+            pa.y += kk.x * y.y - kk.y * y.x;
+            pb.x += qq.x * y.x + qq.y * y.y;
+            pb.y += qq.x * y.y - qq.y * y.x;
+        }
+    }
+    red_a[rg][jl] = pa;
+    red_b[rg][jl] = pb;
+    __syncthreads();
+
+    if (rg == 0) {
+        float2 a = make_float2(0.f, 0.f), b = make_float2(0.f, 0.f);
+#pragma unroll
+        for (int gi = 0; gi < G; ++gi) {
+            a.x += red_a[gi][jl].x; a.y += red_a[gi][jl].y;
+            b.x += red_b[gi][jl].x; b.y += red_b[gi][jl].y;
+        }
+        float2 d = make_float2(0.f, 0.f);
+        if (colok) {
+            const float bt = Elem<TIN>::load(beta, bh);
+            const float2 vv = Elem<TIN>::load2(v, bh * n + j);
+            d = make_float2(bt * (vv.x - a.x), bt * (-vv.y - a.y));
+            const float2 qk = qk_s;
+            const float2 ob = make_float2(b.x + qk.x * d.x - qk.y * d.y, b.y + qk.x * d.y + qk.y * d.x);
+            Elem<TOUT>::store2(o, bh * n + j, ob.x, -ob.y);
+        }
+        delta_s[jl] = d;
+    }
+    __syncthreads();
+
+    const float2 d = delta_s[jl];
+#pragma unroll
+    for (int r = 0; r < RPT; ++r) {
+        const int i = rg + G * r;
+        if (i < m && colok) {
+            const float2 kk = k_s[i];
+            const float2 x = s[r];
+            *reinterpret_cast<float2*>(Sh + 2 * (static_cast<long>(i) * n + j)) =
+                make_float2(x.x + kk.x * d.x - kk.y * d.y, x.y + kk.x * d.y + kk.y * d.x);
+        }
+    }
+}
+
+template <typename TIN, typename TOUT>
+static hipError_t launch_step_t(const StepLaunch& L, hipStream_t st)
+{
+    int np = 1;
+    while (np < L.n && np < 64) np <<= 1;
+    const int n_slices = (L.n + np - 1) / np;
+    const dim3 grid(static_cast<unsigned>(static_cast<long>(L.B) * L.H * n_slices));
+    const TIN* q = static_cast<const TIN*>(L.q);
+    const TIN* k = static_cast<const TIN*>(L.k);
+    const TIN* v = static_cast<const TIN*>(L.v);
+    const TIN* a = static_cast<const TIN*>(L.alpha);
+    const TIN* th = static_cast<const TIN*>(L.theta);
+    const TIN* b = static_cast<const TIN*>(L.beta);
+    TOUT* o = static_cast<TOUT*>(L.o);
+#define SFDA_STEP_CASE(NP_)                                                              \
+    case NP_:                                                                            \
+        hipLaunchKernelGGL((step_kernel<TIN, TOUT, NP_>), grid, dim3(256), 0, st, q, k, v, a, \
+                           th, b, L.S, o, L.m, L.n, n_slices);                           \
+        break;
+    switch (np) {
+        SFDA_STEP_CASE(1) SFDA_STEP_CASE(2) SFDA_STEP_CASE(4) SFDA_STEP_CASE(8)
+        SFDA_STEP_CASE(16) SFDA_STEP_CASE(32) SFDA_STEP_CASE(64)
+        default: return hipErrorInvalidValue;
+    }
+#undef SFDA_STEP_CASE
+    return hipGetLastError();
+}
+
+hipError_t launch_step(const StepLaunch& L, hipStream_t st)
+{
+    if (L.in_bf16) {
+        return L.out_bf16 ? launch_step_t<uint16_t, uint16_t>(L, st) : launch_step_t<uint16_t, float>(L, st);
+    }
+    return L.out_bf16 ? launch_step_t<float, uint16_t>(L, st) : launch_step_t<float, float>(L, st);
+}
+
+}  // namespace sfda

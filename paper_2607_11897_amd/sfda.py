@@ -1,0 +1,132 @@
+"""Thin Python binding of libsfda (ctypes).  Argument marshalling only: every step of the
+computation runs in the HIP kernels behind the C ABI declared in include/sfda.h.
+
+Tensors are torch tensors on the GPU, contiguous, with complex values stored as a trailing
+axis of 2 (re, im) -- float32 (``torch.view_as_real`` of complex64 gives this layout) or
+bfloat16.  torch is used for device memory and streams only.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsfda.so")
+
+SFDA_F32, SFDA_BF16 = 0, 1
+STATUS = {0: "SFDA_OK", 1: "SFDA_ERR_NULL", 2: "SFDA_ERR_SHAPE", 3: "SFDA_ERR_CHUNK",
+          4: "SFDA_ERR_DTYPE", 5: "SFDA_ERR_ALIGN", 6: "SFDA_ERR_ALIAS", 7: "SFDA_ERR_HIP"}
+EXPORTS = ("sfda_chunk_fwd", "sfda_chunk_fwd_sliced", "sfda_step", "sfda_status_string",
+           "sfda_abi_version")
+
+_lib = None
+
+
+class SfdaError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        msg = load_library().sfda_status_string(status).decode()
+        super().__init__(f"{where}: {STATUS.get(status, status)} ({msg})")
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libsfda.so; raises if it has not been built (there is no fallback path)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"libsfda.so not found at {path}: build it with "
+                           "`python -m paper_2607_11897_amd.build` (no CPU fallback exists)")
+    lib = ctypes.CDLL(path)
+    vp, i = ctypes.c_void_p, ctypes.c_int
+    lib.sfda_chunk_fwd.argtypes = [vp] * 9 + [i] * 6 + [i, i, vp]
+    lib.sfda_chunk_fwd.restype = i
+    lib.sfda_chunk_fwd_sliced.argtypes = [vp] * 9 + [i] * 7 + [i, i, vp]
+    lib.sfda_chunk_fwd_sliced.restype = i
+    lib.sfda_step.argtypes = [vp] * 8 + [i] * 4 + [i, i, vp]
+    lib.sfda_step.restype = i
+    lib.sfda_status_string.argtypes = [i]
+    lib.sfda_status_string.restype = ctypes.c_char_p
+    lib.sfda_abi_version.restype = i
+    _lib = lib
+    return lib
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return SFDA_F32
+    if t.dtype == torch.bfloat16:
+        return SFDA_BF16
+    raise TypeError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def chunk_fwd(q, k, v, alpha, theta, beta, S0=None, C: int = 64, *, o=None, S_T=None,
+              out_dtype=None, want_state: bool = True, slice: Optional[int] = None,
+              stream=None) -> Tuple:
+    """SFDA chunkwise forward.  q, k: [B,H,T,m,2]; v: [B,H,T,n,2]; alpha, theta: [B,H,T,m];
+    beta: [B,H,T] (all float32 or all bfloat16); S0: [B,H,m,n,2] float32 or None.
+    Returns (o [B,H,T,n,2] in out_dtype, S_T [B,H,m,n,2] float32 or None)."""
+    import torch
+    lib = load_library()
+    B, H, T, m, _ = q.shape
+    n = v.shape[3]
+    in_code = _dtype_code(q)
+    for t in (k, v, alpha, theta, beta):
+        if t.dtype != q.dtype:
+            raise TypeError("q, k, v, alpha, theta, beta must share one dtype")
+    out_dtype = q.dtype if out_dtype is None else out_dtype
+    if o is None:
+        o = torch.empty((B, H, T, n, 2), dtype=out_dtype, device=q.device)
+    if S_T is None and want_state:
+        S_T = torch.empty((B, H, m, n, 2), dtype=torch.float32, device=q.device)
+    if S0 is not None and S0.dtype != torch.float32:
+        raise TypeError("S0 must be float32")
+    args = [_ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(theta), _ptr(beta), _ptr(S0),
+            _ptr(o), _ptr(S_T), B, H, T, m, n, C]
+    if slice is None:
+        st = lib.sfda_chunk_fwd(*args, in_code, _dtype_code(o), _stream(stream))
+    else:
+        st = lib.sfda_chunk_fwd_sliced(*args, slice, in_code, _dtype_code(o), _stream(stream))
+    if st != 0:
+        raise SfdaError(st, "sfda_chunk_fwd")
+    return o, S_T
+
+
+def step(q, k, v, alpha, theta, beta, S, *, o=None, out_dtype=None, stream=None):
+    """One decode token per head.  q, k: [B,H,m,2]; v: [B,H,n,2]; alpha, theta: [B,H,m];
+    beta: [B,H]; S: [B,H,m,n,2] float32, updated in place.  Returns o [B,H,n,2]."""
+    import torch
+    lib = load_library()
+    B, H, m, _ = q.shape
+    n = v.shape[2]
+    in_code = _dtype_code(q)
+    for t in (k, v, alpha, theta, beta):
+        if t.dtype != q.dtype:
+            raise TypeError("q, k, v, alpha, theta, beta must share one dtype")
+    if S.dtype != torch.float32:
+        raise TypeError("S must be float32")
+    out_dtype = q.dtype if out_dtype is None else out_dtype
+    if o is None:
+        o = torch.empty((B, H, n, 2), dtype=out_dtype, device=q.device)
+    st = lib.sfda_step(_ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(theta), _ptr(beta),
+                       _ptr(S), _ptr(o), B, H, m, n, in_code, _dtype_code(o), _stream(stream))
+    if st != 0:
+        raise SfdaError(st, "sfda_step")
+    return o

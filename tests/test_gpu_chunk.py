@@ -1,0 +1,224 @@
+"""GPU parity of sfda_chunk_fwd against the complex128 oracle (token-by-token recurrence).
+
+Bars: max-norm relative error <= 1e-4 for float32 inputs, <= 2e-2 for bfloat16 inputs with
+float32 accumulation and state; checked on o and on S_T.  Full-size workloads run in the
+same launch configuration as bench.py and are checked on a sampled set of heads (heads are
+independent, so a sampled head's oracle result is exact for that head).
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import pytest
+
+from gpu_util import I, ensure_built, rel_err, run_chunk, run_oracle, upload, to_complex
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def lib():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return ensure_built()
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+
+
+def check(x, C, tol, out_dtype=None, slice=None, label=""):
+    say(label, x.shape, "C", C, x.dtype, "slice", slice)
+    o, S = run_chunk(x, C, out_dtype=out_dtype, slice=slice)
+    o_ref, S_ref = run_oracle(x)
+    eo, es = rel_err(o, o_ref), rel_err(S, S_ref)
+    say(label, "err(o)", eo, "err(S_T)", es)
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(S))
+    assert eo <= tol and es <= tol, (label, eo, es)
+    return eo, es
+
+
+def small(T=100, B=1, H=2, m=64, n=64, dtype="f32", laws=I.LAWS_MAIN, seed=7):
+    w = I.Workload("case", B, H, T, m, n, 16, dtype, laws, seed, 1e-4)
+    return I.make_chunk_inputs(w)
+
+
+# --------------------------------------------------------------------------- workloads
+
+@pytest.mark.parametrize("name", ["tiny_f32", "tiny_f32_n16"])
+def test_tiny(name):
+    w = I.WORKLOADS[name]
+    check(I.make_chunk_inputs(w), w.C, w.tol, label=name)
+
+
+@pytest.mark.parametrize("C", [16, 32, 64])
+def test_chunk_sizes_ragged(C):
+    check(small(T=3 * C + 5), C, 1e-4, label=f"C{C}")
+
+
+@pytest.mark.parametrize("m,n", [(5, 3), (16, 8), (33, 24), (64, 80), (48, 130)])
+def test_odd_shapes(m, n):
+    check(small(T=40, m=m, n=n, B=2, H=1), 16, 1e-4, label=f"m{m}n{n}")
+
+
+@pytest.mark.parametrize("slice", [8, 16, 32, 64])
+def test_slices_agree(slice):
+    check(small(T=130, n=64), 64, 1e-4, slice=slice, label=f"slice{slice}")
+
+
+def test_bf16_small():
+    check(small(T=300, dtype="bf16"), 64, 2e-2, label="bf16")
+
+
+def test_f32_in_bf16_out():
+    x = small(T=70)
+    say("f32 in, bf16 out")
+    o, S = run_chunk(x, 64, out_dtype="bf16")
+    o_ref, S_ref = run_oracle(x)
+    assert rel_err(o, o_ref) <= 1e-2 and rel_err(S, S_ref) <= 1e-4
+
+
+def test_decay_near_documented_limit():
+    """alpha = 0.4 everywhere at C = 64: in-chunk decay product 0.4^64 ~ 3e-26."""
+    laws = I.Laws(alpha=("uniform", 0.4, 0.41), theta=("uniform", -math.pi, math.pi),
+                  beta=("uniform", 0.0, 1.0), s0_scale=0.1)
+    check(small(T=200, laws=laws), 64, 1e-4, label="alpha0.4")
+    laws16 = I.Laws(alpha=("uniform", 0.02, 0.03), theta=("uniform", -math.pi, math.pi),
+                    beta=("uniform", 0.0, 1.0), s0_scale=0.1)
+    check(small(T=50, laws=laws16), 16, 1e-4, label="alpha0.02_C16")
+
+
+def test_fwd_f32_b4h8_t2k_full():
+    w = I.WORKLOADS["fwd_f32_b4h8_t2k"]
+    check(I.make_chunk_inputs(w), w.C, w.tol, label=w.name)
+
+
+def test_fwd_bf16_b8h16_t4k_full_sampled_heads():
+    """The benchmarked workload, run at full size; six heads are checked against the oracle."""
+    w = I.WORKLOADS["fwd_bf16_b8h16_t4k"]
+    say(w.name, "generating")
+    x = I.make_chunk_inputs(w)
+    say(w.name, "running")
+    o, S = run_chunk(x, w.C)
+    heads = [(0, 0), (1, 5), (3, 15), (4, 7), (6, 2), (7, 15)]
+    for (b, h) in heads:
+        xo = x.head(b, h)
+        o_ref, S_ref = run_oracle(xo)
+        eo, es = rel_err(o[b, h], o_ref[0, 0]), rel_err(S[b, h], S_ref[0, 0])
+        say(w.name, (b, h), "err(o)", eo, "err(S_T)", es)
+        assert eo <= w.tol and es <= w.tol
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(S))
+
+
+def test_long_f32_h16_t64k_sampled_heads():
+    """Long context: error of o over prefix windows and of S_T, for two heads."""
+    w = I.WORKLOADS["long_f32_h16_t64k"]
+    say(w.name, "generating")
+    x = I.make_chunk_inputs(w)
+    say(w.name, "running")
+    o, S = run_chunk(x, w.C)
+    for h in (0, 9):
+        xo = x.head(0, h)
+        o_ref, S_ref = run_oracle(xo)
+        errs = {}
+        for lg in range(10, 17):
+            Tp = 2 ** lg
+            errs[Tp] = rel_err(o[0, h, :Tp], o_ref[0, 0, :Tp])
+        es = rel_err(S[0, h], S_ref[0, 0])
+        say(w.name, "head", h, "err(o) by prefix", errs, "err(S_T)", es)
+        assert max(errs.values()) <= w.tol and es <= w.tol
+
+
+# --------------------------------------------------------------------------- edge cases
+
+def test_T0_copies_state_and_in_place():
+    import torch
+    from paper_2607_11897_amd import sfda
+    x = small(T=0)
+    d = upload(x)
+    say("T=0")
+    o, S = sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], d["S0"], C=64)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_complex(S), x.S0)
+    o, S = sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], None, C=64)
+    torch.cuda.synchronize()
+    assert np.all(to_complex(S) == 0)
+
+
+def test_state_in_place_and_resume():
+    """S_T == S0 in place; running T1 then T2 tokens from S_T(T1) equals one run over T1+T2
+    (the affine chunk parenthesisation, Cor. A.3), within the fp32 bar."""
+    import torch
+    from paper_2607_11897_amd import sfda
+    x = small(T=150)
+    d = upload(x)
+    say("resume")
+    o_all, S_all = sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], d["S0"], C=64)
+    S = d["S0"].clone()
+    outs = []
+    for (a, b) in ((0, 37), (37, 101), (101, 150)):
+        sl = lambda t: t[:, :, a:b].contiguous()
+        o, _ = sfda.chunk_fwd(sl(d["q"]), sl(d["k"]), sl(d["v"]), sl(d["alpha"]), sl(d["theta"]),
+                              sl(d["beta"]), S, C=64, S_T=S)
+        outs.append(o)
+    torch.cuda.synchronize()
+    o_ref, S_ref = run_oracle(x)
+    assert rel_err(to_complex(torch.cat(outs, dim=2)), o_ref) <= 1e-4
+    assert rel_err(to_complex(S), S_ref) <= 1e-4
+    assert rel_err(to_complex(S), to_complex(S_all)) <= 1e-5
+
+
+def test_one_token_matches_step():
+    import torch
+    from paper_2607_11897_amd import sfda
+    x = small(T=1, B=2, H=3)
+    d = upload(x)
+    say("T=1 vs step")
+    o, S = sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], d["S0"], C=16)
+    S2 = d["S0"].clone()
+    o2 = sfda.step(d["q"][:, :, 0].contiguous(), d["k"][:, :, 0].contiguous(), d["v"][:, :, 0].contiguous(),
+                   d["alpha"][:, :, 0].contiguous(), d["theta"][:, :, 0].contiguous(),
+                   d["beta"][:, :, 0].contiguous(), S2)
+    torch.cuda.synchronize()
+    assert rel_err(to_complex(o)[:, :, 0], to_complex(o2)) <= 1e-5
+    assert rel_err(to_complex(S), to_complex(S2)) <= 1e-5
+
+
+def test_deterministic_bitwise():
+    x = small(T=200, dtype="bf16")
+    say("determinism")
+    o1, S1 = run_chunk(x, 64)
+    o2, S2 = run_chunk(x, 64)
+    assert np.array_equal(o1, o2) and np.array_equal(S1, S2)
+
+
+def test_guard_bands_untouched():
+    """Canary words around o and S_T stay intact (no out-of-range writes)."""
+    import torch
+    from paper_2607_11897_amd import sfda
+    x = small(T=77, m=40, n=24, B=2, H=2)
+    d = upload(x)
+    B, H, T, m, n = x.shape
+    pad = 256
+    canary = -12345.0
+    ob = torch.full((2 * pad + B * H * T * n * 2,), canary, device="cuda")
+    sb = torch.full((2 * pad + B * H * m * n * 2,), canary, device="cuda")
+    o = ob[pad:pad + B * H * T * n * 2].view(B, H, T, n, 2)
+    S = sb[pad:pad + B * H * m * n * 2].view(B, H, m, n, 2)
+    say("guard bands")
+    sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], d["S0"], C=32, o=o, S_T=S)
+    torch.cuda.synchronize()
+    for buf in (ob, sb):
+        assert torch.all(buf[:pad] == canary) and torch.all(buf[-pad:] == canary)
+    o_ref, S_ref = run_oracle(x)
+    assert rel_err(to_complex(o), o_ref) <= 1e-4 and rel_err(to_complex(S), S_ref) <= 1e-4
+
+
+def test_zero_heads_is_noop():
+    import torch
+    from paper_2607_11897_amd import sfda
+    e = torch.empty((0, 3, 10, 64, 2), device="cuda")
+    say("B=0")
+    o, S = sfda.chunk_fwd(e, e, e, e[..., 0], e[..., 0], e[..., 0, 0], None, C=64)
+    assert o.numel() == 0 and S.numel() == 0
