@@ -1,0 +1,264 @@
+"""Benchmark of the SFDA hot path on one MI355X.
+
+A step is one sfda_chunk_fwd call over the bf16 workload B=8, H=16, T=4096, m=64 complex
+key channels (d_k=128), n=64 complex value columns (d_v=128), C=64: chunk factors, Gram
+matrices, triangular solve, intra-chunk readout, state update and the chunk-to-chunk state
+scan, all in one launch.  Inputs are resident in HBM before timing starts.  Throughput is
+B*T tokens (every token through all H heads) per second.
+
+Also reported on the same JSON line:
+  roofline      the chunk kernel against HBM bandwidth (algorithmic bytes / launch time),
+                with achieved MFMA rates (useful causal flops and dense-tile flops) beside it
+  decode        the sfda_step kernel on the state [512, 32, 64, 64] complex fp32 (HBM-bound)
+  cpu_baseline  the CPU oracle (complex128 recurrence) on a bounded sample of the workload
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--only chunk|decode]
+       [--no-cpu-baseline] [--mode copy]   (copy: a plain device copy, for counter scaling)
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "SFDA fwd tokens/s (H=16,d_k=128,d_v=128,T=4096,C=64) + % MFMA/HBM peak"
+HBM_PEAK_GBS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2516.6
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = ["paper_2607_11897_amd/csrc/sfda_chunk.hip", "paper_2607_11897_amd/csrc/sfda_step.hip",
+                  "paper_2607_11897_amd/csrc/sfda_device.h"]
+
+
+def kernel_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def chunk_bytes_per_token_head(m, n, T, in_bytes, out_bytes):
+    """Algorithmic HBM bytes per token and head: q, k (m complex), v (n complex), alpha,
+    theta (m real), beta, o (n complex) once each, plus S0 and S_T (m x n complex fp32)
+    amortised over the T tokens of a head."""
+    return (2 * m * 2 + n * 2 + 2 * m + 1) * in_bytes + n * 2 * out_bytes + 2 * m * n * 8 / T
+
+
+def chunk_flops_per_chunk_head(C, m, n):
+    """Real flops per chunk and head (a complex multiply-add is 8 real flops).
+    useful: Gram L' and A (causal halves, C^2 m / 2 each), Wt and U (C^2 m / 2, C^2 n / 2),
+    A Delta (C^2 n / 2), Wt S, conj(Q)G S and the state update (C m n each), and the
+    triangular solve (C^3 / 6).  dense_tile: the same eight products counted as full
+    tiles, without the solve."""
+    useful = 8 * (C * C * (3 * m + 2 * n) / 2 + 3 * C * m * n + C ** 3 / 6)
+    tile = 8 * (C * C * (3 * m + 2 * n) + 3 * C * m * n)
+    return useful, tile
+
+
+def decode_bytes_per_head(m, n, in_bytes=4, out_bytes=4):
+    """State read and written once (m x n complex fp32 each way) plus one token's q, k, v,
+    alpha, theta, beta and o."""
+    return 2 * m * n * 8 + (2 * m * 2 + n * 2 + 2 * m + 1) * in_bytes + n * 2 * out_bytes
+
+
+def load_traffic(kernel: str, workload: str):
+    """HBM traffic measured by counters for a kernel, if a committed counter summary exists
+    for the current kernel source."""
+    path = os.path.join(PROFILES, f"{kernel}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("kernel_hash") != kernel_hash():
+        return None
+    return d.get("bytes_per_launch")
+
+
+def timed(fn, steps, warmup, stream):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        fn()
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps   # ms per call
+
+
+def bench_chunk(args, stream):
+    import numpy as np
+    import torch
+    from paper_2607_11897_amd import inputs as I
+    from paper_2607_11897_amd import sfda
+    w = I.WORKLOADS["fwd_bf16_b8h16_t4k"]
+    print(f"# generating inputs for {w.name}", file=sys.stderr, flush=True)
+    x = I.make_chunk_inputs(w)
+    st = x.storage()
+    dev = torch.device("cuda:0")
+
+    def up(a, dt):
+        if dt == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+
+    d = {k: up(st[k], w.dtype) for k in ("q", "k", "v", "alpha", "theta", "beta")}
+    S0 = up(st["S0"], "f32")
+    B, H, T, m, n = x.shape
+    o = torch.empty((B, H, T, n, 2), dtype=torch.bfloat16, device=dev)
+    S_T = torch.empty((B, H, m, n, 2), dtype=torch.float32, device=dev)
+
+    def run():
+        sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], S0, C=w.C,
+                       o=o, S_T=S_T, stream=stream)
+
+    print(f"# timing sfda_chunk_fwd: warmup {args.warmup}, steps {args.steps}", file=sys.stderr, flush=True)
+    ms = timed(run, args.steps, args.warmup, stream)
+    units = B * H * T
+    bytes_alg = chunk_bytes_per_token_head(m, n, T, 2, 2) * units
+    useful, tile = chunk_flops_per_chunk_head(w.C, m, n)
+    nchunk = B * H * (T // w.C)
+    sec = ms / 1e3
+    achieved = bytes_alg / sec / 1e9
+    traffic = load_traffic("chunk_fwd", w.name)
+    return dict(
+        w=w, ms=ms, tokens_per_s=B * T / sec, x=x,
+        roofline={"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+                  "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                  "traffic": traffic,
+                  "kernel": "sfda::chunk_kernel<bf16, C=64>",
+                  "bytes_per_launch": int(bytes_alg),
+                  "bytes_per_token_head": chunk_bytes_per_token_head(m, n, T, 2, 2),
+                  "mfma": {"peak_tflops": BF16_MFMA_PEAK_TFLOPS,
+                           "useful_tflops": round(useful * nchunk / sec / 1e12, 2),
+                           "useful_frac": round(useful * nchunk / sec / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
+                           "tile_tflops": round(tile * nchunk / sec / 1e12, 2),
+                           "tile_frac": round(tile * nchunk / sec / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
+                           "flops_per_chunk_head": {"useful": useful, "tile": tile}}},
+    )
+
+
+def bench_decode(args, stream):
+    import torch
+    from paper_2607_11897_amd import inputs as I
+    from paper_2607_11897_amd import sfda
+    D = I.DECODE
+    B, H, m, n = D["B"], D["H"], D["m"], D["n"]
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(D["seed"])
+    S = torch.randn(B, H, m, n, 2, generator=gen, device="cuda") * 0.0707
+    q, k, v, a, th, bt = I.fill_decode_bulk_torch(gen, B, H, m, n, "cuda")
+    o = torch.empty((B, H, n, 2), device="cuda")
+
+    def run():
+        sfda.step(q, k, v, a, th, bt, S, o=o, stream=stream)
+
+    steps = max(20, args.steps)
+    print(f"# timing sfda_step: steps {steps}", file=sys.stderr, flush=True)
+    ms = timed(run, steps, max(3, args.warmup), stream)
+    bytes_step = decode_bytes_per_head(m, n) * B * H
+    gbs = bytes_step / (ms / 1e3) / 1e9
+    return {"workload": D["name"], "us_per_step": round(ms * 1e3, 2),
+            "tokens_per_s": round(B / (ms / 1e3), 1),
+            "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                         "traffic": load_traffic("step", D["name"]),
+                         "kernel": "sfda::step_kernel<f32, 64>",
+                         "bytes_per_launch": int(bytes_step)}}
+
+
+def cpu_baseline(x, budget_s=12.0):
+    """The oracle on whole batch elements of the workload (all H heads, all T tokens), one
+    after another until about budget_s seconds of CPU time have been spent."""
+    import oracle
+    B, H, T, m, n = x.shape
+    threads = oracle.max_threads()
+    done = 0
+    t0 = time.perf_counter()
+    while done < B:
+        xb = x.__class__(x.q[done:done + 1], x.k[done:done + 1], x.v[done:done + 1],
+                         x.alpha[done:done + 1], x.theta[done:done + 1], x.beta[done:done + 1],
+                         None if x.S0 is None else x.S0[done:done + 1], x.dtype)
+        oracle.recurrence(xb.q, xb.k, xb.v, xb.alpha, xb.theta, xb.beta, xb.S0)
+        done += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    el = time.perf_counter() - t0
+    return {"value": round(done * T / el, 1), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{done} of {B} batch elements x {H} heads x {T} tokens "
+                      f"(complex128 recurrence), {el:.1f} s"}
+
+
+def copy_calibration(args):
+    """A plain device-to-device copy of 1 GiB, repeated, for scaling HBM counters."""
+    import torch
+    nbytes = 1 << 30
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    ms = timed(lambda: dst.copy_(src), max(5, args.steps), 2, torch.cuda.current_stream())
+    print(json.dumps({"mode": "copy", "bytes_read": nbytes, "bytes_written": nbytes,
+                      "ms_per_copy": ms, "GBps": 2 * nbytes / (ms / 1e3) / 1e9}), flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--only", choices=["chunk", "decode"], default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--mode", choices=["bench", "copy"], default="bench")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported. The (batch, head) "
+              "units are independent, so several GPUs would each run their own share.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    from paper_2607_11897_amd import build, sfda
+    if not os.path.exists(sfda.LIB_PATH):
+        build.build(verbose=False)
+    sfda.load_library()
+    if args.mode == "copy":
+        copy_calibration(args)
+        return
+    stream = torch.cuda.current_stream()
+    out = {}
+    if args.only in (None, "decode"):
+        out["decode"] = bench_decode(args, stream)
+    if args.only == "decode":
+        print(json.dumps(out), flush=True)
+        return
+    r = bench_chunk(args, stream)
+    w = r["w"]
+    line = {
+        "metric": METRIC, "value": round(r["tokens_per_s"], 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(r["ms"], 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "T": w.T, "d_k": 2 * w.m, "d_v": 2 * w.n,
+                   "m_complex": w.m, "n_complex": w.n, "C": w.C, "state": "fp32", "accum": "fp32"},
+        "roofline": r["roofline"],
+    }
+    if "decode" in out:
+        line["decode"] = out["decode"]
+    if not args.no_cpu_baseline:
+        print("# timing the CPU oracle", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(r["x"])
+    line["kernel_hash"] = kernel_hash()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
