@@ -110,8 +110,10 @@ __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
             for (int r = 0; r < 4; ++r) {
                 const int i = kb * 16 + 4 * g + r;
                 float x = 0.f;
-                if (args.S0 != nullptr && cb < ncb && j < n && i < m)
-                    x = args.S0[2 * (base_mn + static_cast<long>(i) * n + j) + qp];
+                if (args.S0 != nullptr) {   // uniform branch; the load itself is unconditional
+                    const bool ok = cb < ncb && j < n && i < m;
+                    x = masked(ok, args.S0[2 * (base_mn + static_cast<long>(min(i, m - 1)) * n + min(j, n - 1)) + qp]);
+                }
                 Sacc[w][kb][r] = x;
             }
         }
@@ -133,9 +135,9 @@ __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int t = t0 + kb * 16 + 4 * g + r;
-                    vf[w][kb][r] = (cb < ncb && j < n && t < T)
-                                       ? Elem<TIN>::load2(gv, base_tn + static_cast<long>(t) * n + j)
-                                       : make_float2(0.f, 0.f);
+                    const bool ok = cb < ncb && j < n && t < T;
+                    const float2 x = Elem<TIN>::load2(gv, base_tn + static_cast<long>(min(t, T - 1)) * n + min(j, n - 1));
+                    vf[w][kb][r] = masked(ok, x);
                 }
         }
         {
@@ -146,20 +148,23 @@ __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
 #pragma unroll
             for (int u = 0; u < SEG; ++u) {
                 const int t = t0 + seg * SEG + u;
-                float a = 1.f, th = 0.f;
-                if (t < T && i < m) {
-                    const long e = base_tm + static_cast<long>(t) * m + i;
-                    a = Elem<TIN>::load(ga, e);
-                    th = Elem<TIN>::load(gth, e);
-                }
-                sa += logf(a);
+                const bool ok = t < T && i < m;
+                const long e = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
+                const float a_ld = pin(Elem<TIN>::load(ga, e));
+                const float a = ok ? a_ld : 1.f;
+                const float th = masked(ok, Elem<TIN>::load(gth, e));
+                sa += __logf(a);
                 sp += th;
                 la[u] = sa;
                 ph[u] = sp;
             }
             sm.sega[seg][i] = sa;
             sm.segp[seg][i] = sp;
-            if (tid < C) sm.beta[tid] = (t0 + tid < T) ? Elem<TIN>::load(gb, bh * static_cast<long>(T) + t0 + tid) : 0.f;
+            {
+                const int tb = t0 + (tid & (C - 1));
+                const float bv = Elem<TIN>::load(gb, bh * static_cast<long>(T) + min(tb, T - 1));
+                if (tid < C) sm.beta[tid] = masked(tb < T, bv);
+            }
             __syncthreads();
             float oa = 0.f, op = 0.f;
             for (int s2 = 0; s2 < seg; ++s2) {
@@ -172,18 +177,17 @@ __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
                 const int t = t0 + tl;
                 const float A = la[u] + oa;
                 const float Ph = ph[u] + op;
-                const float e = expf(A);
-                const float ei = expf(-A);
+                const float e = __expf(A);
+                const float ei = __expf(-A);
                 float sn, cs;
-                sincosf(Ph, &sn, &cs);
+                __sincosf(Ph, &sn, &cs);
                 const float gr = e * cs, gi = e * sn;        // g_t
                 const float hr = ei * cs, hi = -ei * sn;     // 1 / g_t
-                float2 qq = make_float2(0.f, 0.f), kk = make_float2(0.f, 0.f);
-                if (t < T && i < m) {
-                    const long e2 = base_tm + static_cast<long>(t) * m + i;
-                    qq = Elem<TIN>::load2(gq, e2);
-                    kk = Elem<TIN>::load2(gk, e2);
-                }
+                const bool ok = t < T && i < m;
+                const long e2 = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
+                float2 qq = Elem<TIN>::load2(gq, e2), kk = Elem<TIN>::load2(gk, e2);
+                qq = masked(ok, qq);
+                kk = masked(ok, kk);
                 sm.qg[tl * LDX + i] = make_float2(qq.x * gr + qq.y * gi, qq.x * gi - qq.y * gr);
                 sm.kg[tl * LDX + i] = make_float2(kk.x * gr + kk.y * gi, kk.x * gi - kk.y * gr);
                 sm.ki[tl * LDX + i] = make_float2(kk.x * hr - kk.y * hi, kk.x * hi + kk.y * hr);
@@ -451,9 +455,10 @@ __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
                         const int jt = jb * 16 + 4 * g + r;
-                        float2 x = make_float2(0.f, 0.f);
-                        if (jt < row) x = sm.g2[jt * LDG + row];
-                        else if (jt == row) x = sm.g2[row * LDG + row];
+                        const float2 lo = sm.g2[jt * LDG + row];      // A[row][jt] stored transposed
+                        const float2 dg = sm.g2[row * LDG + row];     // A diagonal
+                        const float2 lo_p = pin(lo), dg_p = pin(dg);
+                        const float2 x = masked(jt <= row, jt < row ? lo_p : dg_p);
                         a.v[2 * r] = x.x;
                         a.v[2 * r + 1] = x.y;
                     }
@@ -535,9 +540,7 @@ static hipError_t launch_chunk_t(const ChunkLaunch& L, hipStream_t st)
 
 hipError_t launch_chunk(const ChunkLaunch& L, hipStream_t st)
 {
-    if (L.in_bf16)
-        return L.out_bf16 ? launch_chunk_t<PREC_BF16, uint16_t, uint16_t>(L, st)
-                          : launch_chunk_t<PREC_BF16, uint16_t, float>(L, st);
+    if (L.in_bf16) return launch_chunk_bf16(L, st);
     return L.out_bf16 ? launch_chunk_t<PREC_F32, float, uint16_t>(L, st)
                       : launch_chunk_t<PREC_F32, float, float>(L, st);
 }

@@ -74,6 +74,25 @@ template <> struct Elem<uint16_t> {
     }
 };
 
+// ----------------------------------------------------------------- branch-free masking
+
+// Keeps a loaded value opaque to the optimiser, so a load that is later masked with a
+// select stays unconditional (otherwise it is sunk into a branch and issued -- and waited
+// on -- by itself).
+__device__ __forceinline__ float pin(float x) { asm volatile("" : "+v"(x)); return x; }
+__device__ __forceinline__ float2 pin(float2 x) {
+    asm volatile("" : "+v"(x.x), "+v"(x.y));
+    return x;
+}
+__device__ __forceinline__ float masked(bool ok, float x) {
+    x = pin(x);
+    return ok ? x : 0.f;
+}
+__device__ __forceinline__ float2 masked(bool ok, float2 x) {
+    x = pin(x);
+    return ok ? x : make_float2(0.f, 0.f);
+}
+
 // ----------------------------------------------------------------- lane exchange
 
 // Value of lane l ^ 1 (DPP quad permutation [1, 0, 3, 2]).

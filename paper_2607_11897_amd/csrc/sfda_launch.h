@@ -26,5 +26,6 @@ struct ChunkLaunch {
 
 hipError_t launch_step(const StepLaunch& L, hipStream_t st);
 hipError_t launch_chunk(const ChunkLaunch& L, hipStream_t st);
+hipError_t launch_chunk_bf16(const ChunkLaunch& L, hipStream_t st);   // bf16 inputs
 
 }  // namespace sfda
