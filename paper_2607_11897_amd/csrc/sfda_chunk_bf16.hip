@@ -33,6 +33,8 @@
 //
 // Complex products use the real-block form of sfda_device.h on v_mfma_f32_16x16x32_bf16
 // with fp32 accumulation; the diagonal inverses are computed in fp32.
+#include <utility>
+
 #include "sfda_device.h"
 #include "sfda_launch.h"
 
@@ -51,9 +53,11 @@ __device__ __forceinline__ u32 pack_bf16(float lo, float hi) {
     bf16x2 v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};
     return __builtin_bit_cast(u32, v);
 }
+template <typename TOUT> __device__ __forceinline__ TOUT to_out(float x);
+template <> __device__ __forceinline__ float to_out<float>(float x) { return x; }
+template <> __device__ __forceinline__ uint16_t to_out<uint16_t>(float x) { return f32_to_bf16_bits(x); }
 __device__ __forceinline__ float bf_lo(u32 w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(u32 w) { return __uint_as_float(w & 0xFFFF0000u); }
-__device__ __forceinline__ u32 pin_u(u32 x) { asm volatile("" : "+v"(x)); return x; }
 
 __device__ __forceinline__ f32x4 mfma(u32x4 a, u32x4 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(a), as_bf(b), c, 0, 0, 0);
@@ -104,6 +108,35 @@ __device__ __forceinline__ int blk_frag(int row, int chunk) {
     return row * 64 + (((chunk ^ (row >> 2)) & 3) << 4);
 }
 
+// One step of the 16 x 16 unit-lower-triangular inverse (see produce2_blocks): lane (g, jj)
+// holds rows 4g .. 4g+3 of column jj of N in nv and rows 4g .. 4g+3 of X = -(D_beta L') in
+// the accumulator tiles xd (real column c of half h).  Step S2 adds X(r, S2) N(S2, jj) to
+// every row r > S2.
+template <int S2>
+__device__ __forceinline__ void inverse_step(float2 (&nv)[4], const f32x4 (&xd)[2], int g, int jj)
+{
+    const int src = ((S2 >> 2) * 16 + jj) * 4;            // lane holding N(S2, jj)
+    const float2 own = nv[S2 & 3];
+    const float pr = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(own.x)));
+    const float pi = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(own.y)));
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        // X(4g + r, S2): Re at lane 2 (S2 & 7), Im at lane 2 (S2 & 7) + 1 of this 16-lane row
+        const int xv = __float_as_int(xd[S2 >> 3][r]);
+        const float xr = __int_as_float(__builtin_amdgcn_update_dpp(0, xv, 0x150 + 2 * (S2 & 7), 0xF, 0xF, false));
+        const float xi = __int_as_float(__builtin_amdgcn_update_dpp(0, xv, 0x151 + 2 * (S2 & 7), 0xF, 0xF, false));
+        const bool below = 4 * g + r > S2;
+        nv[r].x += below ? xr * pr - xi * pi : 0.f;
+        nv[r].y += below ? xr * pi + xi * pr : 0.f;
+    }
+}
+template <int... S>
+__device__ __forceinline__ void inverse_steps(float2 (&nv)[4], const f32x4 (&xd)[2], int g, int jj,
+                                              std::integer_sequence<int, S...>)
+{
+    (inverse_step<S>(nv, xd, g, jj), ...);
+}
+
 template <int C>
 struct Smem {
     static constexpr int NRB = C / 16;
@@ -120,7 +153,7 @@ struct Smem {
         float2 gc[MP];           // g_C
     };
     Set set[2];
-    float scr[4][16 * 16 * 2];   // per producer wave: diagonal block of L' (fp32)
+    u32x4 ostage[4][128];        // per consumer wave: one 16-row output tile (<= 2 KiB)
 };
 
 struct Args {
@@ -131,11 +164,12 @@ struct Args {
     int T, m, n, n_slices, slice;
 };
 
-template <typename TOUT, int C>
+// CBW: 8-column blocks of S per consumer wave (2 for 64-column slices, 1 for <= 32).
+template <typename TOUT, int C, int CBW>
 __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
 {
     constexpr int NRB = C / 16;
-    constexpr int SEGT = C / 4;          // tokens per producer lane
+    constexpr int TPL = C / 16;          // tokens per producer lane (16 segments of TPL)
     __shared__ Smem<C> sm;
     char* const smb = reinterpret_cast<char*>(&sm);
 
@@ -148,7 +182,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar)
     const int c = lane & 15;
     const int g = lane >> 4;
     const int qp = lane & 1;
@@ -165,35 +199,36 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
     auto set_off = [&](int s) -> char* { return reinterpret_cast<char*>(&sm.set[s]); };
 
     // ---------------------------------------------------------------- consumer state
-    f32x4 Sacc[2][4];        // columns cb = wave + 4 w, rows kb*16 + 4g + r
-    u32x4 db[2][NRB];        // Delta as B fragments
-    u32 vv[2][NRB][2];       // prefetched v: this lane's part of 4 tokens, two bf16 per word
+    f32x4 Sacc[CBW][4];      // columns cb = CBW wave + w, rows kb*16 + 4g + r
+    u32x4 db[CBW][NRB];      // Delta as B fragments
+    u32 vv[CBW][NRB][2];     // prefetched v: this lane's part of 4 tokens, two bf16 per word
     // ---------------------------------------------------------------- producer state
-    u32 pa[SEGT / 2], pt[SEGT / 2];   // alpha, theta bits, two tokens per word
-    u32 pq[SEGT], pk[SEGT];           // q, k (one complex bf16 per word)
+    // producer lane = 4 channels x TPL tokens; prefetched raw (consumed a phase later)
+    uint2 pa[TPL], pt[TPL];           // alpha, theta bits of 4 channels
+    u32x4 pq[TPL], pk[TPL];           // q, k of 4 channels (complex bf16)
     u32 pbeta = 0;
 
-    const int cbw0 = wave, cbw1 = wave + 4;   // consumer column blocks
-    auto cb_active = [&](int w) { return (w == 0 ? cbw0 : cbw1) < ncb; };
+    // consumer column block w is cb = CBW wave + w (contiguous); blocks past the slice compute
+    // on zeros
 
     auto load_v = [&](int ch) {
         const int t0 = ch * C;
 #pragma unroll
-        for (int w = 0; w < 2; ++w) {
-            const int cb = w == 0 ? cbw0 : cbw1;
+        for (int w = 0; w < CBW; ++w) {
+            const int cb = CBW * wave + w;
             const int j = n0 + cb * 8 + (c >> 1);
 #pragma unroll
             for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
                 for (int r2 = 0; r2 < 2; ++r2) {
+                    // raw (clamped-index) loads; out-of-range entries are masked where they are
+                    // used, one chunk later, so nothing waits on these loads here
                     u32 word = 0;
 #pragma unroll
                     for (int h = 0; h < 2; ++h) {
                         const int t = t0 + rb * 16 + 4 * g + 2 * r2 + h;
-                        const bool ok = cb < ncb && j < n && t < T;
                         const long e = 2 * (base_tn + static_cast<long>(min(t, T - 1)) * n + min(j, n - 1)) + qp;
-                        const u32 x = pin_u(args.v[e]);
-                        word |= (ok ? x : 0u) << (16 * h);
+                        word |= static_cast<u32>(args.v[e]) << (16 * h);
                     }
                     vv[w][rb][r2] = word;
                 }
@@ -201,26 +236,39 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
     };
 
     const int pw = wave - 4;                   // producer wave index
-    const int pch = (pw & 3) * 16 + c;         // producer channel
-    const int psg = g;                         // producer token segment
+    const int pseg = lane >> 2;                // token segment (tokens pseg*TPL .. +TPL-1)
+    const int pc0 = (pw & 3) * 16 + (lane & 3) * 4;   // first of this lane's 4 channels
 
     auto load_p = [&](int ch) {
         const int t0 = ch * C;
-        const int i = min(pch, m - 1);
+        if ((m & 3) == 0) {     // 4-channel vector loads (8 bytes of alpha/theta, 16 of q/k)
+            const int cc = min(pc0, m - 4);
 #pragma unroll
-        for (int u = 0; u < SEGT; ++u) {
-            const int t = min(t0 + psg * SEGT + u, T - 1);
-            const long e = base_tm + static_cast<long>(t) * m + i;
-            const u32 av = args.alpha[e], tv = args.theta[e];
-            if (u & 1) {
-                pa[u >> 1] |= av << 16;
-                pt[u >> 1] |= tv << 16;
-            } else {
-                pa[u >> 1] = av;
-                pt[u >> 1] = tv;
+            for (int u = 0; u < TPL; ++u) {
+                const int t = min(t0 + pseg * TPL + u, T - 1);
+                const long e = base_tm + static_cast<long>(t) * m + cc;
+                pa[u] = *reinterpret_cast<const uint2*>(args.alpha + e);
+                pt[u] = *reinterpret_cast<const uint2*>(args.theta + e);
+                pq[u] = *reinterpret_cast<const u32x4*>(args.q + 2 * e);
+                pk[u] = *reinterpret_cast<const u32x4*>(args.k + 2 * e);
             }
-            pq[u] = *reinterpret_cast<const u32*>(args.q + 2 * e);
-            pk[u] = *reinterpret_cast<const u32*>(args.k + 2 * e);
+        } else {                // any m: element loads (clamped)
+#pragma unroll
+            for (int u = 0; u < TPL; ++u) {
+                const int t = min(t0 + pseg * TPL + u, T - 1);
+                const long r0 = base_tm + static_cast<long>(t) * m;
+                u32 a4[4], t4[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const long e = r0 + min(pc0 + k, m - 1);
+                    a4[k] = args.alpha[e];
+                    t4[k] = args.theta[e];
+                    pq[u][k] = *reinterpret_cast<const u32*>(args.q + 2 * e);
+                    pk[u][k] = *reinterpret_cast<const u32*>(args.k + 2 * e);
+                }
+                pa[u] = make_uint2(a4[0] | (a4[1] << 16), a4[2] | (a4[3] << 16));
+                pt[u] = make_uint2(t4[0] | (t4[1] << 16), t4[2] | (t4[3] << 16));
+            }
         }
         pbeta = args.beta[base_t + min(t0 + (lane & (C - 1)), T - 1)];
     };
@@ -230,174 +278,200 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         char* S = set_off(ch & 1);
         auto& st = sm.set[ch & 1];
         const int t0 = ch * C;
-        const bool chan_ok = pch < m;
-        auto alpha_at = [&](int u) {
-            const bool ok = chan_ok && (t0 + psg * SEGT + u) < T;
-            const u32 w = pa[u >> 1];
-            return ok ? ((u & 1) ? bf_hi(w) : bf_lo(w)) : 1.f;
+        auto half = [](uint2 w, int k) {       // k-th bf16 of 4 packed in two words
+            const u32 x = (k < 2) ? w.x : w.y;
+            return (k & 1) ? bf_hi(x) : bf_lo(x);
         };
-        auto theta_at = [&](int u) {
-            const bool ok = chan_ok && (t0 + psg * SEGT + u) < T;
-            const u32 w = pt[u >> 1];
-            return ok ? ((u & 1) ? bf_hi(w) : bf_lo(w)) : 0.f;
-        };
-        float sa = 0.f, sp = 0.f;      // segment totals (first pass)
+        // running sums of log alpha and theta over this lane's TPL tokens, per channel
+        float la[TPL][4], lp[TPL][4];
+        float sa[4], sp[4];
 #pragma unroll
-        for (int u = 0; u < SEGT; ++u) {
-            sa += __logf(alpha_at(u));
-            sp += theta_at(u);
+        for (int k = 0; k < 4; ++k) {
+            const bool chan_ok = pc0 + k < m;
+            float ra = 0.f, rp = 0.f;
+#pragma unroll
+            for (int u = 0; u < TPL; ++u) {
+                const bool ok = chan_ok && (t0 + pseg * TPL + u) < T;
+                ra += __logf(ok ? half(pa[u], k) : 1.f);
+                rp += ok ? half(pt[u], k) : 0.f;
+                la[u][k] = ra;
+                lp[u][k] = rp;
+            }
+            sa[k] = ra;
+            sp[k] = rp;
         }
-        // exclusive prefix over the four token segments of this channel (lane groups)
-        float pre_a = 0.f, pre_p = 0.f;
+        // exclusive prefix over the 16 token segments (lanes 4 apart): inclusive scan by
+        // doubling, then remove this segment's own total
+        float ia[4], ip[4];
 #pragma unroll
-        for (int d = 1; d < 4; ++d) {
-            const int src = ((psg - d) & 3) * 16 + c;
-            const float ya = __shfl(sa, src);
-            const float yp = __shfl(sp, src);
-            if (psg >= d) { pre_a += ya; pre_p += yp; }
+        for (int k = 0; k < 4; ++k) { ia[k] = sa[k]; ip[k] = sp[k]; }
+#pragma unroll
+        for (int d = 1; d < 16; d <<= 1) {
+            const int src = max(lane - 4 * d, 0);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const float ya = __shfl(ia[k], src);
+                const float yp = __shfl(ip[k], src);
+                if (pseg >= d) { ia[k] += ya; ip[k] += yp; }
+            }
         }
-        float A = pre_a, Ph = pre_p;   // running sums (second pass, same order as the first)
 #pragma unroll
-        for (int u = 0; u < SEGT; ++u) {
-            const int tl = psg * SEGT + u;
-            const bool ok = chan_ok && (t0 + tl) < T;
-            A += __logf(alpha_at(u));
-            Ph += theta_at(u);
-            const float e = __expf(A), ei = __expf(-A);
-            float sn, cs;
-            __sincosf(Ph, &sn, &cs);
-            const float gr = e * cs, gi = e * sn;
-            const float hr = ei * cs, hi = -ei * sn;
-            const u32 qw = ok ? pq[u] : 0u, kw = ok ? pk[u] : 0u;
-            const float qr = bf_lo(qw), qi = bf_hi(qw), kr = bf_lo(kw), ki = bf_hi(kw);
-            *reinterpret_cast<u32*>(S + offsetof(typename Smem<C>::Set, qg) + rm_off(tl, pch)) =
-                pack_bf16(qr * gr + qi * gi, qr * gi - qi * gr);
-            *reinterpret_cast<u32*>(S + offsetof(typename Smem<C>::Set, kg) + rm_off(tl, pch)) =
-                pack_bf16(kr * gr + ki * gi, kr * gi - ki * gr);
-            *reinterpret_cast<u32*>(S + offsetof(typename Smem<C>::Set, ki) + rm_off(tl, pch)) =
-                pack_bf16(kr * hr - ki * hi, kr * hi + ki * hr);
-            if (tl == C - 1) st.gc[pch] = make_float2(gr, gi);
+        for (int u = 0; u < TPL; ++u) {
+            const int tl = pseg * TPL + u;
+            const bool row_ok = (t0 + tl) < T;
+            u32x4 wq, wk, wi;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const bool ok = row_ok && (pc0 + k < m);
+                const float A = (ia[k] - sa[k]) + la[u][k];
+                const float Ph = (ip[k] - sp[k]) + lp[u][k];
+                const float e = __expf(A), ei = __expf(-A);
+                float sn, cs;
+                __sincosf(Ph, &sn, &cs);
+                const float gr = e * cs, gi = e * sn;
+                const float hr = ei * cs, hi = -ei * sn;
+                const u32 qw = ok ? pq[u][k] : 0u, kw = ok ? pk[u][k] : 0u;
+                const float qr = bf_lo(qw), qi = bf_hi(qw), kr = bf_lo(kw), ki = bf_hi(kw);
+                wq[k] = pack_bf16(qr * gr + qi * gi, qr * gi - qi * gr);
+                wk[k] = pack_bf16(kr * gr + ki * gi, kr * gi - ki * gr);
+                wi[k] = pack_bf16(kr * hr - ki * hi, kr * hi + ki * hr);
+                if (tl == C - 1) st.gc[pc0 + k] = make_float2(gr, gi);
+            }
+            *reinterpret_cast<u32x4*>(S + offsetof(typename Smem<C>::Set, qg) + rm_off(tl, pc0)) = wq;
+            *reinterpret_cast<u32x4*>(S + offsetof(typename Smem<C>::Set, kg) + rm_off(tl, pc0)) = wk;
+            *reinterpret_cast<u32x4*>(S + offsetof(typename Smem<C>::Set, ki) + rm_off(tl, pc0)) = wi;
         }
         if (pw == 0 && lane < C) st.beta[lane] = (t0 + lane < T) ? bf16_bits_to_f32(static_cast<uint16_t>(pbeta)) : 0.f;
     };
 
     auto produce2_blocks = [&](int ch) {   // Gram blocks and diagonal inverses of chunk ch
-        if (pw >= NRB) return;
         char* S = set_off(ch & 1);
         auto& st = sm.set[ch & 1];
-        const int rb = pw;
-        u32x4 akg[4], aqg[4];
+        f32x4 xd[2];   // -(D_beta L') on the diagonal block (rows 4g + r, real column c of half h)
+        // Gram work is split into units (rb, jb), jb <= rb: the 16 x 16 blocks of L' and A at
+        // token block rb, key block jb.  Each producer wave first takes its own diagonal unit
+        // (rb = jb = wave), whose L' block it inverts below, then an even share of the rest.
+        int units[3][2];
+        int nu = 0;
+        if (NRB == 4) {
+            const int tab[4][3][2] = {{{0, 0}, {3, 0}, {3, 1}}, {{1, 1}, {1, 0}, {3, 2}},
+                                      {{2, 2}, {2, 0}, {-1, -1}}, {{3, 3}, {2, 1}, {-1, -1}}};
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-            akg[kb] = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, kg) + rm_frag(rb * 16 + c, kb * 4 + g));
-            aqg[kb] = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, qg) + rm_frag(rb * 16 + c, kb * 4 + g));
+            for (int k = 0; k < 3; ++k) { units[k][0] = tab[pw][k][0]; units[k][1] = tab[pw][k][1]; }
+            nu = pw < 2 ? 3 : 2;
+        } else if (NRB == 2) {
+            const int tab[4][2] = {{0, 0}, {1, 1}, {1, 0}, {-1, -1}};
+            units[0][0] = tab[pw][0]; units[0][1] = tab[pw][1];
+            nu = pw < 3 ? 1 : 0;
+        } else {
+            units[0][0] = 0; units[0][1] = 0;
+            nu = pw == 0 ? 1 : 0;
         }
-        float* scr = sm.scr[pw];
-        for (int jb = 0; jb <= rb; ++jb) {
+        for (int u = 0; u < nu; ++u) {
+            const int rb = units[u][0], jb = units[u][1];
+            f32x4 accL[2] = {zero4(), zero4()}, accA[2] = {zero4(), zero4()};
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) {
+                const u32x4 akg = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, kg) + rm_frag(rb * 16 + c, kb * 4 + g));
+                const u32x4 aqg = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, qg) + rm_frag(rb * 16 + c, kb * 4 + g));
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int j = jb * 16 + h * 8 + (c >> 1);
+                    const u32x4 y = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, ki) + rm_frag(j, kb * 4 + g));
+                    const u32x4 bk = ybig(y, qmask);
+                    accL[h] = mfma(akg, bk, accL[h]);
+                    accA[h] = mfma(aqg, bk, accA[h]);
+                }
+            }
+            char* aqb = S + offsetof(typename Smem<C>::Set, aq) + (rb * (rb + 1) / 2 + jb) * 1024;
+            char* lbb = S + offsetof(typename Smem<C>::Set, lb) + (rb > 0 ? (rb * (rb - 1) / 2 + jb) * 1024 : 0);
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int jl = h * 8 + (c >> 1);          // column inside block jb
-                const int j = jb * 16 + jl;
-                f32x4 accL = zero4(), accA = zero4();
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb) {
-                    const u32x4 y = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, ki) + rm_frag(j, kb * 4 + g));
-                    const u32x4 bk = ybig(y, qmask);
-                    accL = mfma(akg[kb], bk, accL);
-                    accA = mfma(aqg[kb], bk, accA);
-                }
-                char* aqb = S + offsetof(typename Smem<C>::Set, aq) + (rb * (rb + 1) / 2 + jb) * 1024;
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int tl = 4 * g + r;
-                    const float va = (jb < rb || jl <= tl) ? accA[r] : 0.f;
+                    const float va = (jb < rb || jl <= tl) ? accA[h][r] : 0.f;
                     *reinterpret_cast<__bf16*>(aqb + blk_off(tl, jl) + 2 * qp) = static_cast<__bf16>(va);
-                    if (jb < rb) {
-                        const float bt = st.beta[rb * 16 + tl];
-                        char* lbb = S + offsetof(typename Smem<C>::Set, lb) + (rb * (rb - 1) / 2 + jb) * 1024;
-                        *reinterpret_cast<__bf16*>(lbb + blk_off(tl, jl) + 2 * qp) = static_cast<__bf16>(-bt * accL[r]);
-                    } else {
-                        scr[(tl * 16 + jl) * 2 + qp] = accL[r];
-                    }
+                    const float xb = -st.beta[rb * 16 + tl] * accL[h][r];   // -(D_beta L')
+                    if (jb < rb)
+                        *reinterpret_cast<__bf16*>(lbb + blk_off(tl, jl) + 2 * qp) = static_cast<__bf16>(xb);
+                    else
+                        xd[h][r] = xb;                     // diagonal block, kept for the inverse
                 }
             }
         }
-        // this wave's writes of its diagonal block must land before its lanes read them
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        // N_pp = (I + D_beta L'_pp)^{-1}; lane jj owns column jj (right-looking updates)
+        if (pw >= NRB) return;
+        const int rb = pw;
+        // N_pp = (I + D_beta L'_pp)^{-1} by right-looking substitution on all 64 lanes: lane
+        // (g, jj) owns rows 4g .. 4g+3 of column jj -- the accumulator layout of xd -- so the
+        // entries X(r, s) = -(D_beta L')_rs it needs sit in its own 16-lane row and arrive by
+        // DPP row broadcast; only the finished pivot value N(s, jj) crosses rows (bpermute).
         const int jj = lane & 15;
-        float2 nv[16];
+        float2 nv[4];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) nv[r] = make_float2(r == jj ? 1.f : 0.f, 0.f);
-#pragma unroll
-        for (int s = 0; s < 15; ++s) {
-#pragma unroll
-            for (int r = s + 1; r < 16; ++r) {
-                const float2 l = *reinterpret_cast<const float2*>(&scr[(r * 16 + s) * 2]);
-                const float bt = st.beta[rb * 16 + r];
-                const float cr = -bt * l.x, ci = -bt * l.y;
-                nv[r].x += cr * nv[s].x - ci * nv[s].y;
-                nv[r].y += cr * nv[s].y + ci * nv[s].x;
-            }
-        }
-        if (lane < 16) {
+        for (int r = 0; r < 4; ++r) nv[r] = make_float2(4 * g + r == jj ? 1.f : 0.f, 0.f);
+        inverse_steps(nv, xd, g, jj, std::make_integer_sequence<int, 15>{});
+        {
             char* ndb = S + offsetof(typename Smem<C>::Set, nd) + rb * 1024;
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-                *reinterpret_cast<u32*>(ndb + blk_off(r, jj)) = pack_bf16(nv[r].x, nv[r].y);
+            for (int r = 0; r < 4; ++r)
+                *reinterpret_cast<u32*>(ndb + blk_off(4 * g + r, jj)) = pack_bf16(nv[r].x, nv[r].y);
         }
     };
 
     auto produce2 = [&](int ch) {
-        produce2_blocks(ch);
-        // inputs of the next chunk are fetched after this phase's register peak; their
-        // latency overlaps the wait at the barrier
+        // inputs of the next chunk are fetched first, so their latency overlaps this phase
         if (ch + 1 < nchunks) load_p(ch + 1);
+        produce2_blocks(ch);
     };
 
     // ---------------------------------------------------------------- consumer phases
     auto consume1 = [&](int ch) {          // Delta of chunk ch
         const char* S = set_off(ch & 1);
         const auto& st = sm.set[ch & 1];
-        u32x4 sb[2][4];          // S as B fragments
+        u32x4 sb[CBW][4];          // S as B fragments
 #pragma unroll
-        for (int w = 0; w < 2; ++w)
+        for (int w = 0; w < CBW; ++w)
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) sb[w][kb] = bfrag(Sacc[w][kb], nsign);
         // block by block: R_p = beta (conj(V) - Kg S)_p, then
         // Delta_p = N_pp (R_p + sum_{q<p} (-(D_beta L'))_pq Delta_q)
 #pragma unroll
         for (int p = 0; p < NRB; ++p) {
-            f32x4 acc[2] = {zero4(), zero4()};
+            f32x4 acc[CBW];
+#pragma unroll
+            for (int w = 0; w < CBW; ++w) acc[w] = zero4();
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) {
                 const u32x4 a = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, kg) + rm_frag(p * 16 + c, kb * 4 + g));
-                if (cb_active(0)) acc[0] = mfma(a, sb[0][kb], acc[0]);
-                if (cb_active(1)) acc[1] = mfma(a, sb[1][kb], acc[1]);
+#pragma unroll
+                for (int w = 0; w < CBW; ++w) acc[w] = mfma(a, sb[w][kb], acc[w]);
             }
             const float4 bt = *reinterpret_cast<const float4*>(&st.beta[p * 16 + 4 * g]);
             const float btr[4] = {bt.x, bt.y, bt.z, bt.w};
 #pragma unroll
-            for (int w = 0; w < 2; ++w)
+            for (int w = 0; w < CBW; ++w) {
+                const int cb = CBW * wave + w;
+                const bool col_ok = cb < ncb && n0 + cb * 8 + (c >> 1) < n;
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const u32 word = vv[w][p][r >> 1];
-                    const float vx = flip((r & 1) ? bf_hi(word) : bf_lo(word), csign);
+                    const bool ok = col_ok && (ch * C + p * 16 + 4 * g + r) < T;
+                    const float vx = ok ? flip((r & 1) ? bf_hi(word) : bf_lo(word), csign) : 0.f;
                     acc[w][r] = btr[r] * (vx - acc[w][r]);
                 }
+            }
 #pragma unroll
             for (int q2 = 0; q2 < p; ++q2) {
                 const u32x4 a = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, lb) + (p * (p - 1) / 2 + q2) * 1024 + blk_frag(c, g));
-                if (cb_active(0)) acc[0] = mfma(a, db[0][q2], acc[0]);
-                if (cb_active(1)) acc[1] = mfma(a, db[1][q2], acc[1]);
+#pragma unroll
+                for (int w = 0; w < CBW; ++w) acc[w] = mfma(a, db[w][q2], acc[w]);
             }
             const u32x4 a = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, nd) + p * 1024 + blk_frag(c, g));
 #pragma unroll
-            for (int w = 0; w < 2; ++w) {
-                f32x4 d = zero4();
-                if (cb_active(w)) d = mfma(a, bfrag(acc[w], nsign), d);
+            for (int w = 0; w < CBW; ++w) {
+                const f32x4 d = mfma(a, bfrag(acc[w], nsign), zero4());
                 db[w][p] = bfrag(d, nsign);
             }
         }
@@ -408,37 +482,66 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         const char* S = set_off(ch & 1);
         const auto& st = sm.set[ch & 1];
         const int t0 = ch * C;
-        u32x4 sb[2][4];          // S (still the chunk-start state) as B fragments
+        u32x4 sb[CBW][4];          // S (still the chunk-start state) as B fragments
 #pragma unroll
-        for (int w = 0; w < 2; ++w)
+        for (int w = 0; w < CBW; ++w)
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) sb[w][kb] = bfrag(Sacc[w][kb], nsign);
 #pragma unroll
         for (int rb = 0; rb < NRB; ++rb) {
-            f32x4 acc[2] = {zero4(), zero4()};
+            f32x4 acc[CBW];
+#pragma unroll
+            for (int w = 0; w < CBW; ++w) acc[w] = zero4();
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) {
                 const u32x4 a = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, qg) + rm_frag(rb * 16 + c, kb * 4 + g));
-                if (cb_active(0)) acc[0] = mfma(a, sb[0][kb], acc[0]);
-                if (cb_active(1)) acc[1] = mfma(a, sb[1][kb], acc[1]);
+#pragma unroll
+                for (int w = 0; w < CBW; ++w) acc[w] = mfma(a, sb[w][kb], acc[w]);
             }
 #pragma unroll
             for (int jb = 0; jb <= rb; ++jb) {
                 const u32x4 a = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, aq) + (rb * (rb + 1) / 2 + jb) * 1024 + blk_frag(c, g));
-                if (cb_active(0)) acc[0] = mfma(a, db[0][jb], acc[0]);
-                if (cb_active(1)) acc[1] = mfma(a, db[1][jb], acc[1]);
+#pragma unroll
+                for (int w = 0; w < CBW; ++w) acc[w] = mfma(a, db[w][jb], acc[w]);
             }
+            // o = conj(O^*).  Whole tiles go through this wave's LDS stage so that every lane
+            // writes 16 contiguous bytes; a ragged tile is written element by element.
+            const bool full = (t0 + rb * 16 + 16 <= T) && (n0 + CBW * 8 * (wave + 1) <= n) && (n & 3) == 0;
+            if (full) {
+                constexpr int PITCH = CBW * 16 * static_cast<int>(sizeof(TOUT));   // bytes per row
+                char* stg = reinterpret_cast<char*>(sm.ostage[wave]);
 #pragma unroll
-            for (int w = 0; w < 2; ++w) {
-                const int cb = w == 0 ? cbw0 : cbw1;
-                const int j = n0 + cb * 8 + (c >> 1);
-                if (cb < ncb && j < n) {
+                for (int w = 0; w < CBW; ++w)
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int t = t0 + rb * 16 + 4 * g + r;
-                        if (t < T)
-                            Elem<TOUT>::store(go, 2 * (base_tn + static_cast<long>(t) * n + j) + qp,
-                                              flip(acc[w][r], csign));
+                    for (int r = 0; r < 4; ++r)
+                        *reinterpret_cast<TOUT*>(stg + (4 * g + r) * PITCH + ((w * 8 + (c >> 1)) * 2 + qp) * sizeof(TOUT)) =
+                            to_out<TOUT>(flip(acc[w][r], csign));
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+                constexpr int CPR = PITCH / 16;                  // 16-byte pieces per row
+                char* obase = reinterpret_cast<char*>(go + 2 * (base_tn + static_cast<long>(t0 + rb * 16) * n + n0 + CBW * 8 * wave));
+#pragma unroll
+                for (int idx0 = 0; idx0 < 16 * CPR; idx0 += 64) {
+                    const int idx = idx0 + lane;
+                    if (16 * CPR % 64 == 0 || idx < 16 * CPR) {
+                        const int row = idx / CPR, piece = idx % CPR;
+                        *reinterpret_cast<u32x4*>(obase + static_cast<long>(row) * n * 2 * sizeof(TOUT) + piece * 16) =
+                            *reinterpret_cast<const u32x4*>(stg + row * PITCH + piece * 16);
+                    }
+                }
+                __builtin_amdgcn_wave_barrier();   // stage reads finish before the next tile's writes
+            } else {
+#pragma unroll
+                for (int w = 0; w < CBW; ++w) {
+                    const int cb = CBW * wave + w;
+                    const int j = n0 + cb * 8 + (c >> 1);
+                    if (cb < ncb && j < n) {
+                        TOUT* const orow = go + 2 * (base_tn + static_cast<long>(t0 + rb * 16 + 4 * g) * n + j) + qp;
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            if (t0 + rb * 16 + 4 * g + r < T)
+                                Elem<TOUT>::store(orow, 2L * r * n, flip(acc[w][r], csign));
                     }
                 }
             }
@@ -453,14 +556,14 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
                     a[r] = *reinterpret_cast<const u32*>(S + offsetof(typename Smem<C>::Set, ki) + rm_off(tb * 16 + 4 * g + r, irow));
-                if (cb_active(0)) Sacc[0][kb] = mfma(a, db[0][tb], Sacc[0][kb]);
-                if (cb_active(1)) Sacc[1][kb] = mfma(a, db[1][tb], Sacc[1][kb]);
+#pragma unroll
+                for (int w = 0; w < CBW; ++w) Sacc[w][kb] = mfma(a, db[w][tb], Sacc[w][kb]);
             }
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const float2 gg = st.gc[kb * 16 + 4 * g + r];
 #pragma unroll
-                for (int w = 0; w < 2; ++w) {
+                for (int w = 0; w < CBW; ++w) {
                     const float own = Sacc[w][kb][r];
                     const float oth = partner(own);
                     Sacc[w][kb][r] = gg.x * own + flip(gg.y, nsign) * oth;
@@ -476,8 +579,8 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
     // same sequence of workgroup barriers: two per chunk plus the producers' lead-in chunk.
     if (consumer) {
 #pragma unroll
-        for (int w = 0; w < 2; ++w) {
-            const int cb = w == 0 ? cbw0 : cbw1;
+        for (int w = 0; w < CBW; ++w) {
+            const int cb = CBW * wave + w;
             const int j = n0 + cb * 8 + (c >> 1);
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb)
@@ -485,9 +588,11 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 for (int r = 0; r < 4; ++r) {
                     const int i = kb * 16 + 4 * g + r;
                     float x = 0.f;
-                    if (args.S0 != nullptr)
-                        x = masked(cb < ncb && j < n && i < m,
-                                   args.S0[2 * (base_mn + static_cast<long>(min(i, m - 1)) * n + min(j, n - 1)) + qp]);
+                    if (args.S0 != nullptr) {   // uniform test; the load itself is unconditional
+                        // (clamped index, masked by a multiply so that no load waits alone)
+                        const float keep = (cb < ncb && j < n && i < m) ? 1.f : 0.f;
+                        x = keep * args.S0[2 * (base_mn + static_cast<long>(min(i, m - 1)) * n + min(j, n - 1)) + qp];
+                    }
                     Sacc[w][kb][r] = x;
                 }
         }
@@ -500,8 +605,8 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         }
         if (args.S_T != nullptr) {
 #pragma unroll
-            for (int w = 0; w < 2; ++w) {
-                const int cb = w == 0 ? cbw0 : cbw1;
+            for (int w = 0; w < CBW; ++w) {
+                const int cb = CBW * wave + w;
                 const int j = n0 + cb * 8 + (c >> 1);
                 if (cb >= ncb || j >= n) continue;
 #pragma unroll
@@ -538,12 +643,16 @@ static hipError_t launch_t(const ChunkLaunch& L, hipStream_t st)
     a.T = L.T; a.m = L.m; a.n = L.n; a.slice = L.slice;
     a.n_slices = (L.n + L.slice - 1) / L.slice;
     const dim3 grid(static_cast<unsigned>(static_cast<long>(L.B) * L.H * a.n_slices));
+#define SFDA_PIPE_LAUNCH(C_, W_) \
+    hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, C_, W_>), grid, dim3(NTH), 0, st, a)
+    const bool wide = L.slice > 32;
     switch (L.C) {
-        case 16: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 16>), grid, dim3(NTH), 0, st, a); break;
-        case 32: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 32>), grid, dim3(NTH), 0, st, a); break;
-        case 64: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 64>), grid, dim3(NTH), 0, st, a); break;
+        case 16: if (wide) SFDA_PIPE_LAUNCH(16, 2); else SFDA_PIPE_LAUNCH(16, 1); break;
+        case 32: if (wide) SFDA_PIPE_LAUNCH(32, 2); else SFDA_PIPE_LAUNCH(32, 1); break;
+        case 64: if (wide) SFDA_PIPE_LAUNCH(64, 2); else SFDA_PIPE_LAUNCH(64, 1); break;
         default: return hipErrorInvalidValue;
     }
+#undef SFDA_PIPE_LAUNCH
     return hipGetLastError();
 }
 
