@@ -282,7 +282,9 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             const u32 x = (k < 2) ? w.x : w.y;
             return (k & 1) ? bf_hi(x) : bf_lo(x);
         };
-        // running sums of log alpha and theta over this lane's TPL tokens, per channel
+        // running sums over this lane's TPL tokens, per channel, of log2(alpha) and of theta
+        // in revolutions (theta / 2 pi): the hardware exp2 / sin / cos then need no scaling
+        constexpr float INV_2PI = 0.15915494309189535f;
         float la[TPL][4], lp[TPL][4];
         float sa[4], sp[4];
 #pragma unroll
@@ -292,8 +294,8 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
 #pragma unroll
             for (int u = 0; u < TPL; ++u) {
                 const bool ok = chan_ok && (t0 + pseg * TPL + u) < T;
-                ra += __logf(ok ? half(pa[u], k) : 1.f);
-                rp += ok ? half(pt[u], k) : 0.f;
+                ra += __builtin_amdgcn_logf(ok ? half(pa[u], k) : 1.f);
+                rp += ok ? half(pt[u], k) * INV_2PI : 0.f;
                 la[u][k] = ra;
                 lp[u][k] = rp;
             }
@@ -323,11 +325,10 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const bool ok = row_ok && (pc0 + k < m);
-                const float A = (ia[k] - sa[k]) + la[u][k];
-                const float Ph = (ip[k] - sp[k]) + lp[u][k];
-                const float e = __expf(A), ei = __expf(-A);
-                float sn, cs;
-                __sincosf(Ph, &sn, &cs);
+                const float A = (ia[k] - sa[k]) + la[u][k];     // log2 of the decay product
+                const float Ph = (ip[k] - sp[k]) + lp[u][k];    // phase in revolutions
+                const float e = __builtin_amdgcn_exp2f(A), ei = __builtin_amdgcn_exp2f(-A);
+                const float sn = __builtin_amdgcn_sinf(Ph), cs = __builtin_amdgcn_cosf(Ph);
                 const float gr = e * cs, gi = e * sn;
                 const float hr = ei * cs, hi = -ei * sn;
                 const u32 qw = ok ? pq[u][k] : 0u, kw = ok ? pk[u][k] : 0u;
@@ -344,46 +345,50 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         if (pw == 0 && lane < C) st.beta[lane] = (t0 + lane < T) ? bf16_bits_to_f32(static_cast<uint16_t>(pbeta)) : 0.f;
     };
 
-    auto produce2_blocks = [&](int ch) {   // Gram blocks and diagonal inverses of chunk ch
-        char* S = set_off(ch & 1);
-        auto& st = sm.set[ch & 1];
-        f32x4 xd[2];   // -(D_beta L') on the diagonal block (rows 4g + r, real column c of half h)
-        // Gram work is split into units (rb, jb), jb <= rb: the 16 x 16 blocks of L' and A at
-        // token block rb, key block jb.  Each producer wave first takes its own diagonal unit
-        // (rb = jb = wave), whose L' block it inverts below, then an even share of the rest.
-        int units[3][2];
-        int nu = 0;
+    // Gram work is split into units (rb, jb), jb <= rb: the 16 x 16 blocks at token block rb,
+    // key block jb.  unit_list gives a wave its units: first its own diagonal unit (rb = jb =
+    // wave, whose L' block the producer inverts), then an even share of the rest.
+    auto unit_list = [&](int wv, int (&units)[3][2]) -> int {
         if (NRB == 4) {
             const int tab[4][3][2] = {{{0, 0}, {3, 0}, {3, 1}}, {{1, 1}, {1, 0}, {3, 2}},
                                       {{2, 2}, {2, 0}, {-1, -1}}, {{3, 3}, {2, 1}, {-1, -1}}};
 #pragma unroll
-            for (int k = 0; k < 3; ++k) { units[k][0] = tab[pw][k][0]; units[k][1] = tab[pw][k][1]; }
-            nu = pw < 2 ? 3 : 2;
+            for (int k = 0; k < 3; ++k) { units[k][0] = tab[wv][k][0]; units[k][1] = tab[wv][k][1]; }
+            return wv < 2 ? 3 : 2;
         } else if (NRB == 2) {
             const int tab[4][2] = {{0, 0}, {1, 1}, {1, 0}, {-1, -1}};
-            units[0][0] = tab[pw][0]; units[0][1] = tab[pw][1];
-            nu = pw < 3 ? 1 : 0;
-        } else {
-            units[0][0] = 0; units[0][1] = 0;
-            nu = pw == 0 ? 1 : 0;
+            units[0][0] = tab[wv][0]; units[0][1] = tab[wv][1];
+            return wv < 3 ? 1 : 0;
         }
+        units[0][0] = 0; units[0][1] = 0;
+        return wv == 0 ? 1 : 0;
+    };
+    // one Gram unit: acc[h] (real column block h of key block jb) = X rows rb * (K/G)^T
+    auto gram_unit = [&](const char* S, int xoff, int rb, int jb, f32x4 (&acc)[2]) {
+        acc[0] = zero4();
+        acc[1] = zero4();
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+            const u32x4 ax = *reinterpret_cast<const u32x4*>(S + xoff + rm_frag(rb * 16 + c, kb * 4 + g));
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int j = jb * 16 + h * 8 + (c >> 1);
+                const u32x4 y = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, ki) + rm_frag(j, kb * 4 + g));
+                acc[h] = mfma(ax, ybig(y, qmask), acc[h]);
+            }
+        }
+    };
+
+    auto produce2_blocks = [&](int ch) {   // L' blocks and diagonal inverses of chunk ch
+        char* S = set_off(ch & 1);
+        auto& st = sm.set[ch & 1];
+        f32x4 xd[2];   // -(D_beta L') on the diagonal block (rows 4g + r, real column c of half h)
+        int units[3][2];
+        const int nu = unit_list(pw, units);
         for (int u = 0; u < nu; ++u) {
             const int rb = units[u][0], jb = units[u][1];
-            f32x4 accL[2] = {zero4(), zero4()}, accA[2] = {zero4(), zero4()};
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb) {
-                const u32x4 akg = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, kg) + rm_frag(rb * 16 + c, kb * 4 + g));
-                const u32x4 aqg = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, qg) + rm_frag(rb * 16 + c, kb * 4 + g));
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const int j = jb * 16 + h * 8 + (c >> 1);
-                    const u32x4 y = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, ki) + rm_frag(j, kb * 4 + g));
-                    const u32x4 bk = ybig(y, qmask);
-                    accL[h] = mfma(akg, bk, accL[h]);
-                    accA[h] = mfma(aqg, bk, accA[h]);
-                }
-            }
-            char* aqb = S + offsetof(typename Smem<C>::Set, aq) + (rb * (rb + 1) / 2 + jb) * 1024;
+            f32x4 accL[2];
+            gram_unit(S, offsetof(typename Smem<C>::Set, kg), rb, jb, accL);
             char* lbb = S + offsetof(typename Smem<C>::Set, lb) + (rb > 0 ? (rb * (rb - 1) / 2 + jb) * 1024 : 0);
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
@@ -391,8 +396,6 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int tl = 4 * g + r;
-                    const float va = (jb < rb || jl <= tl) ? accA[h][r] : 0.f;
-                    *reinterpret_cast<__bf16*>(aqb + blk_off(tl, jl) + 2 * qp) = static_cast<__bf16>(va);
                     const float xb = -st.beta[rb * 16 + tl] * accL[h][r];   // -(D_beta L')
                     if (jb < rb)
                         *reinterpret_cast<__bf16*>(lbb + blk_off(tl, jl) + 2 * qp) = static_cast<__bf16>(xb);
@@ -435,19 +438,23 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         for (int w = 0; w < CBW; ++w)
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) sb[w][kb] = bfrag(Sacc[w][kb], nsign);
-        // block by block: R_p = beta (conj(V) - Kg S)_p, then
-        // Delta_p = N_pp (R_p + sum_{q<p} (-(D_beta L'))_pq Delta_q)
+        // all blocks of Kg S first (NRB * CBW independent accumulator chains)
+        f32x4 R[NRB][CBW];
 #pragma unroll
-        for (int p = 0; p < NRB; ++p) {
-            f32x4 acc[CBW];
+        for (int p = 0; p < NRB; ++p)
 #pragma unroll
-            for (int w = 0; w < CBW; ++w) acc[w] = zero4();
+            for (int w = 0; w < CBW; ++w) R[p][w] = zero4();
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb) {
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int p = 0; p < NRB; ++p) {
                 const u32x4 a = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, kg) + rm_frag(p * 16 + c, kb * 4 + g));
 #pragma unroll
-                for (int w = 0; w < CBW; ++w) acc[w] = mfma(a, sb[w][kb], acc[w]);
+                for (int w = 0; w < CBW; ++w) R[p][w] = mfma(a, sb[w][kb], R[p][w]);
             }
+        // R = beta (conj(V) - Kg S)
+#pragma unroll
+        for (int p = 0; p < NRB; ++p) {
             const float4 bt = *reinterpret_cast<const float4*>(&st.beta[p * 16 + 4 * g]);
             const float btr[4] = {bt.x, bt.y, bt.z, bt.w};
 #pragma unroll
@@ -459,19 +466,23 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     const u32 word = vv[w][p][r >> 1];
                     const bool ok = col_ok && (ch * C + p * 16 + 4 * g + r) < T;
                     const float vx = ok ? flip((r & 1) ? bf_hi(word) : bf_lo(word), csign) : 0.f;
-                    acc[w][r] = btr[r] * (vx - acc[w][r]);
+                    R[p][w][r] = btr[r] * (vx - R[p][w][r]);
                 }
             }
+        }
+        // blocked forward substitution: Delta_p = N_pp (R_p + sum_{q<p} (-(D_beta L'))_pq Delta_q)
+#pragma unroll
+        for (int p = 0; p < NRB; ++p) {
 #pragma unroll
             for (int q2 = 0; q2 < p; ++q2) {
                 const u32x4 a = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, lb) + (p * (p - 1) / 2 + q2) * 1024 + blk_frag(c, g));
 #pragma unroll
-                for (int w = 0; w < CBW; ++w) acc[w] = mfma(a, db[w][q2], acc[w]);
+                for (int w = 0; w < CBW; ++w) R[p][w] = mfma(a, db[w][q2], R[p][w]);
             }
             const u32x4 a = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, nd) + p * 1024 + blk_frag(c, g));
 #pragma unroll
             for (int w = 0; w < CBW; ++w) {
-                const f32x4 d = mfma(a, bfrag(acc[w], nsign), zero4());
+                const f32x4 d = mfma(a, bfrag(R[p][w], nsign), zero4());
                 db[w][p] = bfrag(d, nsign);
             }
         }
@@ -487,25 +498,58 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         for (int w = 0; w < CBW; ++w)
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) sb[w][kb] = bfrag(Sacc[w][kb], nsign);
+        // O^* = conj(Q)G S + tril(A) Delta for all blocks, then the state update -- all
+        // independent accumulator chains, issued before any output is stored
+        f32x4 O[NRB][CBW];
 #pragma unroll
-        for (int rb = 0; rb < NRB; ++rb) {
-            f32x4 acc[CBW];
+        for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-            for (int w = 0; w < CBW; ++w) acc[w] = zero4();
+            for (int w = 0; w < CBW; ++w) O[rb][w] = zero4();
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb) {
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int rb = 0; rb < NRB; ++rb) {
                 const u32x4 a = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, qg) + rm_frag(rb * 16 + c, kb * 4 + g));
 #pragma unroll
-                for (int w = 0; w < CBW; ++w) acc[w] = mfma(a, sb[w][kb], acc[w]);
+                for (int w = 0; w < CBW; ++w) O[rb][w] = mfma(a, sb[w][kb], O[rb][w]);
             }
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
             for (int jb = 0; jb <= rb; ++jb) {
                 const u32x4 a = *reinterpret_cast<const u32x4*>(S + offsetof(typename Smem<C>::Set, aq) + (rb * (rb + 1) / 2 + jb) * 1024 + blk_frag(c, g));
 #pragma unroll
-                for (int w = 0; w < CBW; ++w) acc[w] = mfma(a, db[w][jb], acc[w]);
+                for (int w = 0; w < CBW; ++w) O[rb][w] = mfma(a, db[w][jb], O[rb][w]);
             }
-            // o = conj(O^*).  Whole tiles go through this wave's LDS stage so that every lane
-            // writes 16 contiguous bytes; a ragged tile is written element by element.
+        // S <- diag(g_C) (S + (K/G)^T Delta)
+#pragma unroll
+        for (int tb = 0; tb < NRB; ++tb)
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) {
+                const int irow = kb * 16 + c;
+                u32x4 a;
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    a[r] = *reinterpret_cast<const u32*>(S + offsetof(typename Smem<C>::Set, ki) + rm_off(tb * 16 + 4 * g + r, irow));
+#pragma unroll
+                for (int w = 0; w < CBW; ++w) Sacc[w][kb] = mfma(a, db[w][tb], Sacc[w][kb]);
+            }
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float2 gg = st.gc[kb * 16 + 4 * g + r];
+#pragma unroll
+                for (int w = 0; w < CBW; ++w) {
+                    const float own = Sacc[w][kb][r];
+                    const float oth = partner(own);
+                    Sacc[w][kb][r] = gg.x * own + flip(gg.y, nsign) * oth;
+                }
+            }
+        // o = conj(O^*).  Whole tiles go through this wave's LDS stage so that every lane
+        // writes 16 contiguous bytes; a ragged tile is written element by element.
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb) {
             const bool full = (t0 + rb * 16 + 16 <= T) && (n0 + CBW * 8 * (wave + 1) <= n) && (n & 3) == 0;
             if (full) {
                 constexpr int PITCH = CBW * 16 * static_cast<int>(sizeof(TOUT));   // bytes per row
@@ -515,7 +559,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
 #pragma unroll
                     for (int r = 0; r < 4; ++r)
                         *reinterpret_cast<TOUT*>(stg + (4 * g + r) * PITCH + ((w * 8 + (c >> 1)) * 2 + qp) * sizeof(TOUT)) =
-                            to_out<TOUT>(flip(acc[w][r], csign));
+                            to_out<TOUT>(flip(O[rb][w][r], csign));
                 __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
                 __builtin_amdgcn_wave_barrier();
                 __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -541,36 +585,34 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
 #pragma unroll
                         for (int r = 0; r < 4; ++r)
                             if (t0 + rb * 16 + 4 * g + r < T)
-                                Elem<TOUT>::store(orow, 2L * r * n, flip(acc[w][r], csign));
+                                Elem<TOUT>::store(orow, 2L * r * n, flip(O[rb][w][r], csign));
                     }
                 }
             }
         }
-        // S <- diag(g_C) (S + (K/G)^T Delta)
+        if (ch + 1 < nchunks) load_v(ch + 1);
+    };
+
+    auto consume_gram = [&](int ch) {      // A blocks of chunk ch (consumer waves, set ch & 1)
+        char* S = set_off(ch & 1);
+        int units[3][2];
+        const int nu = unit_list(wave, units);
+        for (int u = 0; u < nu; ++u) {
+            const int rb = units[u][0], jb = units[u][1];
+            f32x4 accA[2];
+            gram_unit(S, offsetof(typename Smem<C>::Set, qg), rb, jb, accA);
+            char* aqb = S + offsetof(typename Smem<C>::Set, aq) + (rb * (rb + 1) / 2 + jb) * 1024;
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-            const int irow = kb * 16 + c;
+            for (int h = 0; h < 2; ++h) {
+                const int jl = h * 8 + (c >> 1);
 #pragma unroll
-            for (int tb = 0; tb < NRB; ++tb) {
-                u32x4 a;
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    a[r] = *reinterpret_cast<const u32*>(S + offsetof(typename Smem<C>::Set, ki) + rm_off(tb * 16 + 4 * g + r, irow));
-#pragma unroll
-                for (int w = 0; w < CBW; ++w) Sacc[w][kb] = mfma(a, db[w][tb], Sacc[w][kb]);
-            }
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float2 gg = st.gc[kb * 16 + 4 * g + r];
-#pragma unroll
-                for (int w = 0; w < CBW; ++w) {
-                    const float own = Sacc[w][kb][r];
-                    const float oth = partner(own);
-                    Sacc[w][kb][r] = gg.x * own + flip(gg.y, nsign) * oth;
+                for (int r = 0; r < 4; ++r) {
+                    const int tl = 4 * g + r;
+                    const float va = (jb < rb || jl <= tl) ? accA[h][r] : 0.f;
+                    *reinterpret_cast<__bf16*>(aqb + blk_off(tl, jl) + 2 * qp) = static_cast<__bf16>(va);
                 }
             }
         }
-        if (ch + 1 < nchunks) load_v(ch + 1);
     };
 
     // ---------------------------------------------------------------- roles
@@ -601,6 +643,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             if (ch >= 0) consume1(ch);
             __syncthreads();
             if (ch >= 0) consume2(ch);
+            if (ch + 1 < nchunks) consume_gram(ch + 1);   // operands written in phase 1
             __syncthreads();
         }
         if (args.S_T != nullptr) {
