@@ -78,7 +78,9 @@ typedef void* sfda_stream_t;
  *   prod over any C consecutive tokens of alpha_t[i] must stay above about 1e-30 for every
  *   channel i (e.g. alpha >= 0.35 for C = 64, alpha >= 0.014 for C = 16); alpha must be > 0.
  *   Accumulation and state are float32 for both dtypes; with in_dtype == SFDA_BF16 the
- *   matrix products take bfloat16 operands.
+ *   matrix products take bfloat16 operands, and each head's share of q, k, v and o must
+ *   stay below 2 GiB (T * max(m, n) * 2 * sizeof(out element) < 2^31; SFDA_ERR_SHAPE
+ *   otherwise).
  */
 sfda_status_t sfda_chunk_fwd(const void* q, const void* k, const void* v,
                              const void* alpha, const void* theta, const void* beta,

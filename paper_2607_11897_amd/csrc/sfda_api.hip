@@ -58,6 +58,10 @@ static sfda_status_t chunk_fwd_impl(const void* q, const void* k, const void* v,
     if (slice < 8 || slice > 64 || (slice & 7) != 0) return SFDA_ERR_SHAPE;
     const long BH = static_cast<long>(B) * H;
     if (BH * ((n + slice - 1) / slice) > 0x7FFFFFFFL) return SFDA_ERR_SHAPE;
+    // bf16 inputs: each head's slice of q, k, v and o is addressed with 32-bit byte offsets
+    if (in_dtype == SFDA_BF16 &&
+        static_cast<long>(T) * (m > n ? m : n) * 2 * esize(out_dtype) >= 0x80000000L)
+        return SFDA_ERR_SHAPE;
     if (BH == 0) return SFDA_OK;
     const bool need_inputs = T > 0;
     if (need_inputs && (!q || !k || !v || !alpha || !theta || !beta || !o)) return SFDA_ERR_NULL;
