@@ -19,13 +19,14 @@
 //
 // Pipeline (512 threads = 8 waves, two per SIMD):
 //   waves 0-3 (consumers) own 16 value columns each and hold their columns of S in MFMA
-//     accumulators for the whole scan; for chunk c they compute Delta, O and S_out, then
-//     the A Gram blocks of chunk c + 1;
+//     accumulators for the whole scan; for chunk c they compute Delta and the A Gram
+//     blocks (phase 1), then O and S_out and the off-diagonal L' blocks of chunk c + 1
+//     (phase 2);
 //   waves 4-7 (producers) prepare chunk c + 1: phase 1 turns q, k, alpha, theta, beta
 //     (prefetched a chunk ahead) into g -- running products of alpha and running sums of
-//     theta, scanned across the lanes of a row -- and writes conj(Q)G, conj(K)G, K/G (bf16)
-//     to LDS; phase 2 forms the Gram blocks of L' on MFMA and inverts the diagonal blocks of
-//     I + D_beta L'.
+//     theta -- and writes conj(Q)G, conj(K)G, K/G (bf16) to LDS; phase 2 forms the
+//     diagonal blocks of L' on MFMA, inverts the diagonal blocks of I + D_beta L' (one per
+//     wave) and starts the scan of the chunk after.
 //   Operands live in two LDS sets (chunk c and chunk c + 1); two barriers per chunk.
 //
 // Complex products.  A complex 16 x 16 result block is held as two MFMA accumulator tiles,
@@ -64,9 +65,11 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
 
 __device__ __forceinline__ bf16x8 as_bf(u32x4 x) { return __builtin_bit_cast(bf16x8, x); }
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+// two floats -> (lo, hi) bf16 pair, round to nearest even (one v_cvt_pk_bf16_f32)
 __device__ __forceinline__ u32 pack_bf16(float lo, float hi) {
-    bf16x2 v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};
-    return __builtin_bit_cast(u32, v);
+    const f32x2 v = {lo, hi};
+    return __builtin_bit_cast(u32, __builtin_convertvector(v, bf16x2));
 }
 __device__ __forceinline__ float bf_lo(u32 w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(u32 w) { return __uint_as_float(w & 0xFFFF0000u); }
@@ -82,18 +85,6 @@ struct BPair { u32x4 re, im; };    // right operand for the real / imaginary out
 
 __device__ __forceinline__ void czero(CAcc& z) { z.re = zero4(); z.im = zero4(); }
 
-// from a split accumulator pair holding Y[4g + r][c]
-__device__ __forceinline__ BPair bsplit(const f32x4& yr, const f32x4& yi) {
-    BPair b;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        b.re[r] = pack_bf16(yr[r], -yi[r]);
-        b.im[r] = pack_bf16(yi[r], yr[r]);
-    }
-    return b;
-}
-__device__ __forceinline__ BPair bsplit(const CAcc& y) { return bsplit(y.re, y.im); }
-
 // from interleaved complex bf16 words w[r] = (Re, Im) of Y[4g + r][c]
 __device__ __forceinline__ BPair bwords(u32x4 w) {
     BPair b;
@@ -103,6 +94,14 @@ __device__ __forceinline__ BPair bwords(u32x4 w) {
         b.im[r] = __builtin_amdgcn_alignbit(w[r], w[r], 16);
     }
     return b;
+}
+
+// from a split accumulator pair holding Y[4g + r][c] (rounded to bf16 once)
+__device__ __forceinline__ BPair bsplit(const CAcc& y) {
+    u32x4 w;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) w[r] = pack_bf16(y.re[r], y.im[r]);
+    return bwords(w);
 }
 
 // z += X Y over one K-block of 16 complex indices
@@ -153,13 +152,11 @@ template <int K>
 __device__ __forceinline__ float row_lane(float x) {
     return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x150 + K, 0xF, 0xF, false));
 }
-// value of lane (this - D) of the same row; lanes with no such source get `fill`
-template <int D>
-__device__ __forceinline__ float row_shr(float x, float fill) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(fill), __float_as_int(x),
-                                                      0x110 + D, 0xF, 0xF, false));
+// quad permutation (DPP quad_perm selector P)
+template <int P>
+__device__ __forceinline__ float quad_lane(float x) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), P, 0xF, 0xF, false));
 }
-
 // ------------------------------------------------------------------ LDS addressing (bytes)
 
 // C x 64 complex bf16, row-major, rows padded to 272 bytes (68 words: consecutive rows start
@@ -255,6 +252,7 @@ struct Smem {
         float2 gc[MP];           // g_C
     };
     Set set[2];
+    float2 tot[4][MP];           // per producer wave: product of alpha, sum of theta / 2 pi
 };
 
 struct Args {
@@ -265,9 +263,10 @@ struct Args {
     int T, m, n, n_slices, slice;
 };
 
-// Gram units: the 16 x 16 blocks (rb, jb), jb <= rb, of a C x C Gram matrix, split over four
-// waves.  A wave's first unit is its own diagonal block (rb = jb = wave) when it has one.
-__device__ __forceinline__ int unit_list(int nrb, int wv, int (&units)[3][2])
+// Gram units: 16 x 16 blocks (rb, jb) of a C x C Gram matrix, split over the four consumer
+// waves.  a_units: all blocks jb <= rb (the A Gram); l_units: the blocks jb < rb (the
+// off-diagonal part of L'; its diagonal blocks go to the producer that inverts them).
+__device__ __forceinline__ int a_units(int nrb, int wv, int (&units)[3][2])
 {
     units[1][0] = units[1][1] = units[2][0] = units[2][1] = 0;
     if (nrb == 4) {
@@ -284,6 +283,18 @@ __device__ __forceinline__ int unit_list(int nrb, int wv, int (&units)[3][2])
     }
     units[0][0] = 0; units[0][1] = 0;
     return wv == 0 ? 1 : 0;
+}
+__device__ __forceinline__ int l_units(int nrb, int wv, int (&units)[2][2])
+{
+    units[0][0] = 1; units[0][1] = 0; units[1][0] = 1; units[1][1] = 0;
+    if (nrb == 4) {
+        const int tab[4][2][2] = {{{3, 0}, {1, 0}}, {{3, 1}, {2, 0}}, {{3, 2}, {1, 0}}, {{2, 1}, {1, 0}}};
+#pragma unroll
+        for (int k = 0; k < 2; ++k) { units[k][0] = tab[wv][k][0]; units[k][1] = tab[wv][k][1]; }
+        return wv < 2 ? 2 : 1;
+    }
+    if (nrb == 2) return wv == 0 ? 1 : 0;
+    return 0;
 }
 
 template <typename TOUT, int C>
@@ -461,7 +472,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         auto consume_gram = [&](int ch) {      // A blocks of chunk ch (set ch & 1)
             char* S = set_ptr(ch & 1);
             int units[3][2];
-            const int nu = unit_list(NRB, wave, units);
+            const int nu = a_units(NRB, wave, units);
             CAcc z[3];
 #pragma unroll
             for (int u = 0; u < 3; ++u)
@@ -477,6 +488,29 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     *reinterpret_cast<u32*>(aqb + blk_off(4 * g + r, c)) =
                         keep ? pack_bf16(z[u].re[r], z[u].im[r]) : 0u;
                 }
+            }
+        };
+
+        auto consume_lgram = [&](int ch) {     // off-diagonal blocks of -(D_beta L'), chunk ch
+            char* S = set_ptr(ch & 1);
+            const Set& st = sm.set[ch & 1];
+            int units[2][2];
+            const int nu = l_units(NRB, wave, units);
+            CAcc z[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+                if (u < nu) gram(S, OFF_KG, units[u][0], units[u][1], z[u]);
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                if (u >= nu) continue;
+                const int rb = units[u][0], jb = units[u][1];
+                const float4 bt = *reinterpret_cast<const float4*>(&st.beta[rb * 16 + 4 * g]);
+                const float btr[4] = {bt.x, bt.y, bt.z, bt.w};
+                char* lbb = S + OFF_LB + (rb * (rb - 1) / 2 + jb) * 1024;
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    *reinterpret_cast<u32*>(lbb + blk_off(4 * g + r, c)) =
+                        pack_bf16(-btr[r] * z[u].re[r], -btr[r] * z[u].im[r]);
             }
         };
 
@@ -498,11 +532,13 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 }
             if (nchunks > 0) load_v(0);
         }
+        __syncthreads();          // matches the producers' lead-in barrier
         for (int ch = -1; ch < nchunks; ++ch) {
             if (active && ch >= 0) consume1(ch);
+            if (ch >= 0) consume_gram(ch);
             __syncthreads();
             if (active && ch >= 0) consume2(ch);
-            if (ch + 1 < nchunks) consume_gram(ch + 1);   // operands written in phase 1
+            if (ch + 1 < nchunks) consume_lgram(ch + 1);  // operands written in phase 1
             __syncthreads();
         }
         if (active && args.S_T != nullptr) {
@@ -519,17 +555,20 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         }
     } else {
         // ============================================================ producer waves
-        // lane = (channel group cg: 4 channels, token segment seg: TPL consecutive tokens)
+        // Wave pw owns tokens pw * C/4 .. pw * C/4 + C/4 - 1 of the chunk for all channels, so
+        // one load instruction covers whole rows of q, k, alpha, theta (whole cache lines).
+        // Lane = (channel group cg: channels 4cg .. 4cg+3; token segment tsg: TPL tokens).
+        constexpr int TPW = C / 4;                     // tokens per producer wave
         const int pw = wave - 4;
-        const int seg = lane & 15;
-        const int cg = lane >> 4;
-        const int pc0 = pw * 16 + cg * 4;              // first of this lane's 4 channels
-        const int tseg = seg * TPL;
+        const int tsg = lane & 3;
+        const int cg = lane >> 2;
+        const int pc0 = cg * 4;                        // first of this lane's 4 channels
+        const int tl0 = pw * TPW + tsg * TPL;          // first token (in the chunk) of the lane
         const bool wide = (m & 3) == 0;               // 4-channel vector loads
         u32 poff2[TPL], poff4[TPL];                   // byte offsets (bf16 / complex bf16)
 #pragma unroll
         for (int u = 0; u < TPL; ++u) {
-            const u32 e = static_cast<u32>((tseg + u) * m + pc0);
+            const u32 e = static_cast<u32>((tl0 + u) * m + pc0);
             poff2[u] = pc0 < m ? e * 2u : OOB;
             poff4[u] = pc0 < m ? e * 4u : OOB;
         }
@@ -560,7 +599,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     u32 a4[4], t4[4];
 #pragma unroll
                     for (int k = 0; k < 4; ++k) {
-                        const u32 e = static_cast<u32>((tseg + u) * m + pc0 + k);
+                        const u32 e = static_cast<u32>((tl0 + u) * m + pc0 + k);
                         const bool ok = pc0 + k < m;
                         a4[k] = ld16(ra, ok ? e * 2u : OOB);
                         t4[k] = ld16(rt, ok ? e * 2u : OOB);
@@ -575,17 +614,19 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             pbeta = ld16(rb, static_cast<u32>(lane & (C - 1)) * 2u);
         };
 
-        // phase 1: g and the operands conj(Q)G, conj(K)G, K/G of chunk ch into set ch & 1.
-        // Positions past T or past m read as zero; alpha = 0 there is taken as 1 (a valid
-        // decay is positive), so g stays finite and g_C of a ragged chunk is g at its last
-        // token.
-        auto produce1 = [&](int ch) {
-            char* S = set_ptr(ch & 1);
-            Set& st = sm.set[ch & 1];
-            constexpr float INV_2PI = 0.15915494309189535f;
-            // running product of alpha and running sum of theta (in revolutions, the unit of
-            // the hardware sin / cos) over this lane's TPL tokens, per channel
-            float lm[TPL][4], lph[TPL][4], em[4], eph[4];
+        // Cumulative decay g_t = prod_{s <= t} alpha_s e^{i theta_s} per channel: the running
+        // product of alpha and the running sum of theta (in revolutions, the unit of the
+        // hardware sin / cos) are scanned in three levels -- over the lane's TPL tokens, over
+        // the four token segments of the wave (quad DPP), and over the waves (their totals,
+        // through LDS).  Positions past T or past m read as zero; alpha = 0 there is taken as
+        // 1 (a valid decay is positive), so g stays finite and g_C of a ragged chunk is g at
+        // its last token.
+        constexpr float INV_2PI = 0.15915494309189535f;
+        float lm[TPL][4], lph[TPL][4];    // inclusive over the lane's tokens
+        float qm[4], qph[4];              // exclusive over the wave's earlier segments
+        auto pretot = [&]() {             // first two levels, wave totals to LDS
+            const bool s0 = tsg == 0, s01 = tsg < 2;
+            float tm[4], tp[4];
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 float rm = 1.f, rp = 0.f;
@@ -601,18 +642,42 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     lm[u][k] = rm;
                     lph[u][k] = rp;
                 }
-                // exclusive scan over the 16 segments of the row
-                float xm = rm, xp = rp;
-                xm *= row_shr<1>(xm, 1.f); xp += row_shr<1>(xp, 0.f);
-                xm *= row_shr<2>(xm, 1.f); xp += row_shr<2>(xp, 0.f);
-                xm *= row_shr<4>(xm, 1.f); xp += row_shr<4>(xp, 0.f);
-                xm *= row_shr<8>(xm, 1.f); xp += row_shr<8>(xp, 0.f);
-                em[k] = row_shr<1>(xm, 1.f);
-                eph[k] = row_shr<1>(xp, 0.f);
+                // inclusive scan over the quad: shift by 1, then by 2
+                float ym = quad_lane<0x90>(rm), yp = quad_lane<0x90>(rp);     // [0, 0, 1, 2]
+                rm *= s0 ? 1.f : ym;
+                rp += s0 ? 0.f : yp;
+                ym = quad_lane<0x40>(rm); yp = quad_lane<0x40>(rp);           // [0, 0, 0, 1]
+                rm *= s01 ? 1.f : ym;
+                rp += s01 ? 0.f : yp;
+                ym = quad_lane<0x90>(rm); yp = quad_lane<0x90>(rp);
+                qm[k] = s0 ? 1.f : ym;
+                qph[k] = s0 ? 0.f : yp;
+                tm[k] = quad_lane<0xFF>(rm);                                   // [3, 3, 3, 3]
+                tp[k] = quad_lane<0xFF>(rp);
+            }
+            if (s0) {
+                float4* tw = reinterpret_cast<float4*>(&sm.tot[pw][pc0]);
+                tw[0] = make_float4(tm[0], tp[0], tm[1], tp[1]);
+                tw[1] = make_float4(tm[2], tp[2], tm[3], tp[3]);
+            }
+        };
+
+        // phase 1: g and the operands conj(Q)G, conj(K)G, K/G of chunk ch into set ch & 1
+        auto produce1 = [&](int ch) {
+            char* S = set_ptr(ch & 1);
+            Set& st = sm.set[ch & 1];
+            float em[4], eph[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) { em[k] = qm[k]; eph[k] = qph[k]; }
+            for (int w2 = 0; w2 < pw; ++w2) {          // totals of the earlier waves
+                const float4* tw = reinterpret_cast<const float4*>(&sm.tot[w2][pc0]);
+                const float4 t01 = tw[0], t23 = tw[1];
+                em[0] *= t01.x; eph[0] += t01.y; em[1] *= t01.z; eph[1] += t01.w;
+                em[2] *= t23.x; eph[2] += t23.y; em[3] *= t23.z; eph[3] += t23.w;
             }
 #pragma unroll
             for (int u = 0; u < TPL; ++u) {
-                const int tl = tseg + u;
+                const int tl = tl0 + u;
                 u32x4 wq, wk, wi;
                 float2 gl[4];
 #pragma unroll
@@ -633,7 +698,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 *reinterpret_cast<u32x4*>(S + OFF_QG + rm_off(tl, pc0)) = wq;
                 *reinterpret_cast<u32x4*>(S + OFF_KG + rm_off(tl, pc0)) = wk;
                 *reinterpret_cast<u32x4*>(S + OFF_KI + rm_off(tl, pc0)) = wi;
-                if (u == TPL - 1 && seg == 15) {
+                if (u == TPL - 1 && pw == 3 && tsg == 3) {     // token C - 1
                     float4* gp = reinterpret_cast<float4*>(&st.gc[pc0]);
                     gp[0] = make_float4(gl[0].x, gl[0].y, gl[1].x, gl[1].y);
                     gp[1] = make_float4(gl[2].x, gl[2].y, gl[3].x, gl[3].y);
@@ -642,41 +707,21 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             if (pw == 0 && lane < C) st.beta[lane] = bf16_bits_to_f32(static_cast<uint16_t>(pbeta));
         };
 
-        // phase 2: L' Gram blocks and the diagonal inverses of chunk ch
-        auto produce2 = [&](int ch) {
-            // inputs of the next chunk are fetched first, so their latency overlaps this phase
-            if (ch + 1 < nchunks) load_p(ch + 1);
+        // phase 2: diagonal blocks of L' and their inverses, chunk ch
+        auto invert_diag = [&](int ch) {
             char* S = set_ptr(ch & 1);
             const Set& st = sm.set[ch & 1];
-            int units[3][2];
-            const int nu = unit_list(NRB, pw, units);
-            CAcc z[3];
+            CAcc z;
+            gram(S, OFF_KG, pw, pw, z);
+            f32x4 xr, xi;          // X = -(D_beta L') on the diagonal block, zero on and above
+            const float4 bt = *reinterpret_cast<const float4*>(&st.beta[pw * 16 + 4 * g]);
+            const float btr[4] = {bt.x, bt.y, bt.z, bt.w};
 #pragma unroll
-            for (int u = 0; u < 3; ++u)
-                if (u < nu) gram(S, OFF_KG, units[u][0], units[u][1], z[u]);
-            f32x4 xr = zero4(), xi = zero4();     // X = -(D_beta L') on the diagonal block
-#pragma unroll
-            for (int u = 0; u < 3; ++u) {
-                if (u >= nu) continue;
-                const int rb = units[u][0], jb = units[u][1];
-                const float4 bt = *reinterpret_cast<const float4*>(&st.beta[rb * 16 + 4 * g]);
-                const float btr[4] = {bt.x, bt.y, bt.z, bt.w};
-                if (jb < rb) {
-                    char* lbb = S + OFF_LB + (rb * (rb - 1) / 2 + jb) * 1024;
-#pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        *reinterpret_cast<u32*>(lbb + blk_off(4 * g + r, c)) =
-                            pack_bf16(-btr[r] * z[u].re[r], -btr[r] * z[u].im[r]);
-                } else {
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const bool low = c < 4 * g + r;
-                        xr[r] = low ? -btr[r] * z[u].re[r] : 0.f;
-                        xi[r] = low ? -btr[r] * z[u].im[r] : 0.f;
-                    }
-                }
+            for (int r = 0; r < 4; ++r) {
+                const bool low = c < 4 * g + r;
+                xr[r] = low ? -btr[r] * z.re[r] : 0.f;
+                xi[r] = low ? -btr[r] * z.im[r] : 0.f;
             }
-            if (pw >= NRB) return;
             const int jj = c;
             float nr[4], ni[4];
 #pragma unroll
@@ -691,7 +736,19 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 *reinterpret_cast<u32*>(ndb + blk_off(4 * g + r, jj)) = pack_bf16(nr[r], ni[r]);
         };
 
-        if (nchunks > 0) load_p(0);
+        // phase 2: diagonal blocks of L' and their inverses, chunk ch; then the first two
+        // scan levels of chunk ch + 1, whose inputs are fetched at the start of the phase
+        auto produce2 = [&](int ch) {
+            if (ch + 1 < nchunks) load_p(ch + 1);
+            if (pw < NRB) invert_diag(ch);
+            if (ch + 1 < nchunks) pretot();
+        };
+
+        if (nchunks > 0) {
+            load_p(0);
+            pretot();
+        }
+        __syncthreads();          // wave totals of chunk 0
         for (int ch = -1; ch < nchunks; ++ch) {
             if (ch + 1 < nchunks) produce1(ch + 1);
             __syncthreads();
