@@ -177,61 +177,26 @@ __device__ __forceinline__ int blk_frag(int row, int chunk) {
 // ------------------------------------------------------------------ 16 x 16 inverse
 
 // N = (I - X)^{-1} for X strictly lower triangular (X = -(D_beta L') on a diagonal block),
-// i.e. N = I + X N, by forward substitution in 4 x 4 blocks.  Lane (g, jj) holds rows
-// 4g .. 4g+3 of column jj of N in (nr, ni) and rows 4g .. 4g+3 of X, real column jj, in
-// (xr, xi) -- the split accumulator layout, with X already zero on and above the diagonal.
-// X(4g + r, s) for a fixed pivot s is lane s of the lane's own row (DPP row broadcast);
-// only the finished rows of a block cross lane rows (one bpermute round per block).
-template <int G, int S>
-__device__ __forceinline__ void inv_local(float (&nr)[4], float (&ni)[4], const f32x4& xr,
-                                          const f32x4& xi, bool mine)
+// i.e. N = I + X N, by forward substitution over the pivots s = 0 .. 14.  Lane (i, cg) --
+// i = lane % 16, cg = lane / 16 -- holds row i of X (zero on and above the diagonal, so
+// rows i <= s take no update) and row i, columns 4cg .. 4cg+3 of N; the pivot row
+// N(s, 4cg .. 4cg+3) is lane s of the lane's own 16-lane row (DPP row broadcast).
+template <int S>
+__device__ __forceinline__ void inv_step(float (&nr)[4], float (&ni)[4], const float2 (&xrow)[16])
 {
-    const float pr = mine ? nr[S] : 0.f, pi = mine ? ni[S] : 0.f;
+    const float xr = xrow[S].x, xi = xrow[S].y;
 #pragma unroll
-    for (int r = S + 1; r < 4; ++r) {
-        const float a = row_lane<4 * G + S>(xr[r]), b = row_lane<4 * G + S>(xi[r]);
-        nr[r] += a * pr - b * pi;
-        ni[r] += a * pi + b * pr;
+    for (int k = 0; k < 4; ++k) {
+        const float pr = row_lane<S>(nr[k]), pi = row_lane<S>(ni[k]);
+        nr[k] += xr * pr - xi * pi;
+        ni[k] += xr * pi + xi * pr;
     }
 }
-template <int G, int S>
-__device__ __forceinline__ void inv_cross(float (&nr)[4], float (&ni)[4], const f32x4& xr,
-                                          const f32x4& xi, float pr, float pi)
+template <int... S>
+__device__ __forceinline__ void inv_steps(float (&nr)[4], float (&ni)[4], const float2 (&xrow)[16],
+                                          std::integer_sequence<int, S...>)
 {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const float a = row_lane<4 * G + S>(xr[r]), b = row_lane<4 * G + S>(xi[r]);
-        nr[r] += a * pr - b * pi;
-        ni[r] += a * pi + b * pr;
-    }
-}
-template <int G>
-__device__ __forceinline__ void inv_block(float (&nr)[4], float (&ni)[4], const f32x4& xr,
-                                          const f32x4& xi, int g, int jj)
-{
-    const bool mine = g == G;
-    inv_local<G, 0>(nr, ni, xr, xi, mine);
-    inv_local<G, 1>(nr, ni, xr, xi, mine);
-    inv_local<G, 2>(nr, ni, xr, xi, mine);
-    if constexpr (G < 3) {
-        const int src = (G * 16 + jj) * 4;
-        float br[4], bi[4];
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            br[s] = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(nr[s])));
-            bi[s] = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(ni[s])));
-        }
-        const bool below = g > G;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            br[s] = below ? br[s] : 0.f;
-            bi[s] = below ? bi[s] : 0.f;
-        }
-        inv_cross<G, 0>(nr, ni, xr, xi, br[0], bi[0]);
-        inv_cross<G, 1>(nr, ni, xr, xi, br[1], bi[1]);
-        inv_cross<G, 2>(nr, ni, xr, xi, br[2], bi[2]);
-        inv_cross<G, 3>(nr, ni, xr, xi, br[3], bi[3]);
-    }
+    (inv_step<S>(nr, ni, xrow), ...);
 }
 
 // ------------------------------------------------------------------ shared memory
@@ -253,6 +218,7 @@ struct Smem {
     };
     Set set[2];
     float2 tot[4][MP];           // per producer wave: product of alpha, sum of theta / 2 pi
+    float2 xs[4][16][18];        // per producer wave: X of its diagonal block (fp32, padded)
 };
 
 struct Args {
@@ -576,22 +542,19 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         u32x4 pq[TPL], pk[TPL];           // q, k of the 4 channels (complex bf16)
         u32 pbeta = 0;
 
-        auto load_p = [&](int ch) {
+        // alpha, theta of chunk ch (consumed by the scan, a phase before the rest)
+        auto load_at = [&](int ch) {
             const int t0 = ch * C;
             const long e0 = base_tm + static_cast<long>(t0) * m;
             const int rows = T - t0;
             const rsrc_t ra = make_rsrc(args.alpha + e0, rows * m * 2);
             const rsrc_t rt = make_rsrc(args.theta + e0, rows * m * 2);
-            const rsrc_t rq = make_rsrc(args.q + 2 * e0, rows * m * 4);
-            const rsrc_t rk = make_rsrc(args.k + 2 * e0, rows * m * 4);
             if (wide) {
 #pragma unroll
                 for (int u = 0; u < TPL; ++u) {
                     const u32x2 a = ld64(ra, poff2[u]), t = ld64(rt, poff2[u]);
                     pa[u] = make_uint2(a.x, a.y);
                     pt[u] = make_uint2(t.x, t.y);
-                    pq[u] = ld128(rq, poff4[u]);
-                    pk[u] = ld128(rk, poff4[u]);
                 }
             } else {                    // any m: one channel per load
 #pragma unroll
@@ -603,12 +566,35 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                         const bool ok = pc0 + k < m;
                         a4[k] = ld16(ra, ok ? e * 2u : OOB);
                         t4[k] = ld16(rt, ok ? e * 2u : OOB);
-                        pq[u][k] = ld32(rq, ok ? e * 4u : OOB);
-                        pk[u][k] = ld32(rk, ok ? e * 4u : OOB);
                     }
                     pa[u] = make_uint2(a4[0] | (a4[1] << 16), a4[2] | (a4[3] << 16));
                     pt[u] = make_uint2(t4[0] | (t4[1] << 16), t4[2] | (t4[3] << 16));
                 }
+            }
+        };
+        // q, k, beta of chunk ch
+        auto load_qk = [&](int ch) {
+            const int t0 = ch * C;
+            const long e0 = base_tm + static_cast<long>(t0) * m;
+            const int rows = T - t0;
+            const rsrc_t rq = make_rsrc(args.q + 2 * e0, rows * m * 4);
+            const rsrc_t rk = make_rsrc(args.k + 2 * e0, rows * m * 4);
+            if (wide) {
+#pragma unroll
+                for (int u = 0; u < TPL; ++u) {
+                    pq[u] = ld128(rq, poff4[u]);
+                    pk[u] = ld128(rk, poff4[u]);
+                }
+            } else {
+#pragma unroll
+                for (int u = 0; u < TPL; ++u)
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        const u32 e = static_cast<u32>((tl0 + u) * m + pc0 + k);
+                        const bool ok = pc0 + k < m;
+                        pq[u][k] = ld32(rq, ok ? e * 4u : OOB);
+                        pk[u][k] = ld32(rk, ok ? e * 4u : OOB);
+                    }
             }
             const rsrc_t rb = make_rsrc(args.beta + base_t + t0, rows * 2);
             pbeta = ld16(rb, static_cast<u32>(lane & (C - 1)) * 2u);
@@ -713,43 +699,50 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             const Set& st = sm.set[ch & 1];
             CAcc z;
             gram(S, OFF_KG, pw, pw, z);
-            f32x4 xr, xi;          // X = -(D_beta L') on the diagonal block, zero on and above
+            // X = -(D_beta L') on the diagonal block, zero on and above the diagonal, to the
+            // wave's scratch; each lane then reads back one row
             const float4 bt = *reinterpret_cast<const float4*>(&st.beta[pw * 16 + 4 * g]);
             const float btr[4] = {bt.x, bt.y, bt.z, bt.w};
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const bool low = c < 4 * g + r;
-                xr[r] = low ? -btr[r] * z.re[r] : 0.f;
-                xi[r] = low ? -btr[r] * z.im[r] : 0.f;
+                sm.xs[pw][4 * g + r][c] = make_float2(low ? -btr[r] * z.re[r] : 0.f,
+                                                      low ? -btr[r] * z.im[r] : 0.f);
             }
-            const int jj = c;
+            const int i = c, cgi = g;
+            float2 xrow[16];
+#pragma unroll
+            for (int s2 = 0; s2 < 16; s2 += 2) {
+                const float4 x2 = *reinterpret_cast<const float4*>(&sm.xs[pw][i][s2]);
+                xrow[s2] = make_float2(x2.x, x2.y);
+                xrow[s2 + 1] = make_float2(x2.z, x2.w);
+            }
             float nr[4], ni[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) { nr[r] = 4 * g + r == jj ? 1.f : 0.f; ni[r] = 0.f; }
-            inv_block<0>(nr, ni, xr, xi, g, jj);
-            inv_block<1>(nr, ni, xr, xi, g, jj);
-            inv_block<2>(nr, ni, xr, xi, g, jj);
-            inv_block<3>(nr, ni, xr, xi, g, jj);
-            char* ndb = S + OFF_ND + pw * 1024;
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-                *reinterpret_cast<u32*>(ndb + blk_off(4 * g + r, jj)) = pack_bf16(nr[r], ni[r]);
+            for (int k = 0; k < 4; ++k) { nr[k] = i == 4 * cgi + k ? 1.f : 0.f; ni[k] = 0.f; }
+            inv_steps(nr, ni, xrow, std::make_integer_sequence<int, 15>{});
+            const u32x4 w = {pack_bf16(nr[0], ni[0]), pack_bf16(nr[1], ni[1]),
+                             pack_bf16(nr[2], ni[2]), pack_bf16(nr[3], ni[3])};
+            *reinterpret_cast<u32x4*>(S + OFF_ND + pw * 1024 + blk_frag(i, cgi)) = w;
         };
 
         // phase 2: diagonal blocks of L' and their inverses, chunk ch; then the first two
-        // scan levels of chunk ch + 1, whose inputs are fetched at the start of the phase
+        // scan levels of chunk ch + 1 (alpha, theta fetched a phase earlier)
         auto produce2 = [&](int ch) {
-            if (ch + 1 < nchunks) load_p(ch + 1);
+            if (ch + 1 < nchunks) load_qk(ch + 1);
             if (pw < NRB) invert_diag(ch);
             if (ch + 1 < nchunks) pretot();
         };
 
         if (nchunks > 0) {
-            load_p(0);
+            load_at(0);
+            load_qk(0);
             pretot();
         }
         __syncthreads();          // wave totals of chunk 0
         for (int ch = -1; ch < nchunks; ++ch) {
+            // alpha and theta two chunks ahead: the scan of chunk ch + 1 has consumed them
+            if (ch + 2 < nchunks) load_at(ch + 2);
             if (ch + 1 < nchunks) produce1(ch + 1);
             __syncthreads();
             if (ch + 1 < nchunks) produce2(ch + 1);
