@@ -31,8 +31,8 @@ METRIC = "SFDA fwd tokens/s (H=16,d_k=128,d_v=128,T=4096,C=64) + % MFMA/HBM peak
 HBM_PEAK_GBS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2516.6
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = ["paper_2607_11897_amd/csrc/sfda_chunk.hip", "paper_2607_11897_amd/csrc/sfda_step.hip",
-                  "paper_2607_11897_amd/csrc/sfda_device.h"]
+KERNEL_SOURCES = ["paper_2607_11897_amd/csrc/sfda_chunk_bf16.hip", "paper_2607_11897_amd/csrc/sfda_chunk.hip",
+                  "paper_2607_11897_amd/csrc/sfda_step.hip", "paper_2607_11897_amd/csrc/sfda_device.h"]
 
 
 def kernel_hash() -> str:
@@ -135,7 +135,7 @@ def bench_chunk(args, stream):
         roofline={"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                   "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                   "traffic": traffic,
-                  "kernel": "sfda::chunk_kernel<bf16, C=64>",
+                  "kernel": "sfda::pipe::chunk_pipe_kernel<bf16 out, C=64>",
                   "bytes_per_launch": int(bytes_alg),
                   "bytes_per_token_head": chunk_bytes_per_token_head(m, n, T, 2, 2),
                   "mfma": {"peak_tflops": BF16_MFMA_PEAK_TFLOPS,
