@@ -13,7 +13,8 @@ Also reported on the same JSON line:
   cpu_baseline  the CPU oracle (complex128 recurrence) on a bounded sample of the workload
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--only chunk|decode]
-       [--no-cpu-baseline] [--mode copy]   (copy: a plain device copy, for counter scaling)
+       [--no-cpu-baseline] [--mode copy|rmw]   (copy: a plain device copy, for counter
+       scaling; rmw: an in-place pass over 1 GiB, the decode step's access pattern)
 """
 from __future__ import annotations
 
@@ -209,6 +210,17 @@ def copy_calibration(args):
                       "ms_per_copy": ms, "GBps": 2 * nbytes / (ms / 1e3) / 1e9}), flush=True)
 
 
+def rmw_calibration(args):
+    """An in-place scaling of a 1 GiB fp32 tensor (read and write of the same bytes, the
+    access pattern of the decode step), repeated."""
+    import torch
+    nbytes = 1 << 30
+    x = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    ms = timed(lambda: x.mul_(1.0), max(5, args.steps), 2, torch.cuda.current_stream())
+    print(json.dumps({"mode": "rmw", "bytes_read": nbytes, "bytes_written": nbytes,
+                      "ms_per_pass": ms, "GBps": 2 * nbytes / (ms / 1e3) / 1e9}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -216,7 +228,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--only", choices=["chunk", "decode"], default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=["bench", "copy"], default="bench")
+    ap.add_argument("--mode", choices=["bench", "copy", "rmw"], default="bench")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported. The (batch, head) "
@@ -232,6 +244,9 @@ def main():
     sfda.load_library()
     if args.mode == "copy":
         copy_calibration(args)
+        return
+    if args.mode == "rmw":
+        rmw_calibration(args)
         return
     stream = torch.cuda.current_stream()
     out = {}
