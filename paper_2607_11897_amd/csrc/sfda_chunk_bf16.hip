@@ -188,8 +188,8 @@ __device__ __forceinline__ void inv_step(float (&nr)[4], float (&ni)[4], const f
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const float pr = row_lane<S>(nr[k]), pi = row_lane<S>(ni[k]);
-        nr[k] += xr * pr - xi * pi;
-        ni[k] += xr * pi + xi * pr;
+        nr[k] = __builtin_fmaf(xr, pr, __builtin_fmaf(-xi, pi, nr[k]));
+        ni[k] = __builtin_fmaf(xr, pi, __builtin_fmaf(xi, pr, ni[k]));
     }
 }
 template <int... S>
@@ -254,10 +254,11 @@ __device__ __forceinline__ int l_units(int nrb, int wv, int (&units)[2][2])
 {
     units[0][0] = 1; units[0][1] = 0; units[1][0] = 1; units[1][1] = 0;
     if (nrb == 4) {
-        const int tab[4][2][2] = {{{3, 0}, {1, 0}}, {{3, 1}, {2, 0}}, {{3, 2}, {1, 0}}, {{2, 1}, {1, 0}}};
+        // waves 0, 1 carry three A units, so they take one L' unit and waves 2, 3 two
+        const int tab[4][2][2] = {{{3, 0}, {1, 0}}, {{3, 1}, {1, 0}}, {{3, 2}, {1, 0}}, {{2, 1}, {2, 0}}};
 #pragma unroll
         for (int k = 0; k < 2; ++k) { units[k][0] = tab[wv][k][0]; units[k][1] = tab[wv][k][1]; }
-        return wv < 2 ? 2 : 1;
+        return wv < 2 ? 1 : 2;
     }
     if (nrb == 2) return wv == 0 ? 1 : 0;
     return 0;
@@ -336,22 +337,42 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             }
         };
 
+        // The products below run as software pipelines: the LDS operand fragments of stage
+        // s + 1 are requested before the MFMAs of stage s, and a scheduling barrier keeps the
+        // compiler from sinking the reads back next to their uses.
         auto consume1 = [&](int ch) {          // Delta of chunk ch
             const char* S = set_ptr(ch & 1);
             const Set& st = sm.set[ch & 1];
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) sb[kb] = bsplit(Sa[kb]);
-            // P = conj(K)G S for all row blocks: independent accumulator chains
+            // P = conj(K)G S: stage kb multiplies the kb-th channel block of every row block
             CAcc R[NRB];
 #pragma unroll
             for (int p = 0; p < NRB; ++p) czero(R[p]);
+            u32x4 buf[2][NRB];
+            auto kg_load = [&](int kb, u32x4 (&f)[NRB]) {
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
+                for (int p = 0; p < NRB; ++p)
+                    f[p] = *reinterpret_cast<const u32x4*>(S + OFF_KG + rm_frag(p * 16 + c, kb * 4 + g));
+            };
+            kg_load(0, buf[0]);
 #pragma unroll
-                for (int p = 0; p < NRB; ++p) {
-                    const u32x4 a = *reinterpret_cast<const u32x4*>(S + OFF_KG + rm_frag(p * 16 + c, kb * 4 + g));
-                    cmma(R[p], a, sb[kb]);
-                }
+            for (int kb = 0; kb < 4; ++kb) {
+                if (kb + 1 < 4) kg_load(kb + 1, buf[(kb + 1) & 1]);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int p = 0; p < NRB; ++p) cmma(R[p], buf[kb & 1][p], sb[kb]);
+            }
+            // the substitution's operands (diagonal inverses, off-diagonal blocks) in flight
+            // while R is formed
+            constexpr int NLBK = NRB * (NRB - 1) / 2;
+            u32x4 fn[NRB], fl[NLBK > 0 ? NLBK : 1];
+#pragma unroll
+            for (int p = 0; p < NRB; ++p)
+                fn[p] = *reinterpret_cast<const u32x4*>(S + OFF_ND + p * 1024 + blk_frag(c, g));
+#pragma unroll
+            for (int e = 0; e < NLBK; ++e)
+                fl[e] = *reinterpret_cast<const u32x4*>(S + OFF_LB + e * 1024 + blk_frag(c, g));
             // R = D_beta (conj(V) - P)
 #pragma unroll
             for (int p = 0; p < NRB; ++p) {
@@ -368,14 +389,10 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
 #pragma unroll
             for (int p = 0; p < NRB; ++p) {
 #pragma unroll
-                for (int q2 = 0; q2 < p; ++q2) {
-                    const u32x4 a = *reinterpret_cast<const u32x4*>(S + OFF_LB + (p * (p - 1) / 2 + q2) * 1024 + blk_frag(c, g));
-                    cmma(R[p], a, db[q2]);
-                }
-                const u32x4 a = *reinterpret_cast<const u32x4*>(S + OFF_ND + p * 1024 + blk_frag(c, g));
+                for (int q2 = 0; q2 < p; ++q2) cmma(R[p], fl[p * (p - 1) / 2 + q2], db[q2]);
                 CAcc d;
                 czero(d);
-                cmma(d, a, bsplit(R[p]));
+                cmma(d, fn[p], bsplit(R[p]));
                 db[p] = bsplit(d);
             }
         };
@@ -385,43 +402,69 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             const char* S = set_ptr(ch & 1);
             const Set& st = sm.set[ch & 1];
             const int t0 = ch * C;
-            // O^* = conj(Q)G S + tril(A) Delta, all blocks before any store
+            // stages: conj(Q)G S by channel block (4), tril(A) Delta by key block (NRB), then
+            // the state update (K/G)^T Delta two fragments at a time (2 NRB)
+            constexpr int NQ = 4, NA = NRB, NK = 2 * NRB, NST = NQ + NA + NK;
+            // state-update stage i multiplies fragments (tb, 2 kb2) and (tb', 2 kb2 + 1), tb' half
+            // the blocks away: independent accumulators, and the two fragments' rows far apart
+            // so that the compiler pairs each fragment's own reads
+            auto ki_tb = [&](int i, int e) { return e == 0 ? i % NRB : (i % NRB + NRB / 2) % NRB; };
+            auto ki_kb = [&](int i, int e) { return 2 * (i / NRB) + e; };
             CAcc O[NRB];
 #pragma unroll
             for (int rb = 0; rb < NRB; ++rb) czero(O[rb]);
+            u32x4 buf[2][4];
+            auto load = [&](int sg, u32x4 (&f)[4]) {
+                if (sg < NQ) {
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
+                    for (int rb = 0; rb < NRB; ++rb)
+                        f[rb] = *reinterpret_cast<const u32x4*>(S + OFF_QG + rm_frag(rb * 16 + c, sg * 4 + g));
+                } else if (sg < NQ + NA) {
+                    const int jb = sg - NQ;
 #pragma unroll
-                for (int rb = 0; rb < NRB; ++rb) {
-                    const u32x4 a = *reinterpret_cast<const u32x4*>(S + OFF_QG + rm_frag(rb * 16 + c, kb * 4 + g));
-                    cmma(O[rb], a, sb[kb]);
+                    for (int rb = 0; rb < NRB; ++rb)
+                        if (rb >= jb)
+                            f[rb] = *reinterpret_cast<const u32x4*>(S + OFF_AQ + (rb * (rb + 1) / 2 + jb) * 1024 + blk_frag(c, g));
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) {
+                        const int tb = ki_tb(sg - NQ - NA, e), kb = ki_kb(sg - NQ - NA, e);
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            f[e][r] = *reinterpret_cast<const u32*>(S + OFF_KI + rm_off(tb * 16 + 4 * g + r, kb * 16 + c));
+                    }
                 }
+            };
+            auto mma = [&](int sg, const u32x4 (&f)[4]) {
+                if (sg < NQ) {
 #pragma unroll
-            for (int rb = 0; rb < NRB; ++rb)
+                    for (int rb = 0; rb < NRB; ++rb) cmma(O[rb], f[rb], sb[sg]);
+                } else if (sg < NQ + NA) {
+                    const int jb = sg - NQ;
 #pragma unroll
-                for (int jb = 0; jb <= rb; ++jb) {
-                    const u32x4 a = *reinterpret_cast<const u32x4*>(S + OFF_AQ + (rb * (rb + 1) / 2 + jb) * 1024 + blk_frag(c, g));
-                    cmma(O[rb], a, db[jb]);
+                    for (int rb = 0; rb < NRB; ++rb)
+                        if (rb >= jb) cmma(O[rb], f[rb], db[jb]);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) cmma(Sa[ki_kb(sg - NQ - NA, e)], f[e], db[ki_tb(sg - NQ - NA, e)]);
                 }
+            };
+            load(0, buf[0]);
+#pragma unroll
+            for (int sg = 0; sg < NST; ++sg) {
+                if (sg + 1 < NST) load(sg + 1, buf[(sg + 1) & 1]);
+                __builtin_amdgcn_sched_barrier(0);
+                mma(sg, buf[sg & 1]);
+            }
             // S <- diag(g_C) (S + (K/G)^T Delta)
-#pragma unroll
-            for (int tb = 0; tb < NRB; ++tb)
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb) {
-                    u32x4 a;
-#pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        a[r] = *reinterpret_cast<const u32*>(S + OFF_KI + rm_off(tb * 16 + 4 * g + r, kb * 16 + c));
-                    cmma(Sa[kb], a, db[tb]);
-                }
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const float2 gg = st.gc[kb * 16 + 4 * g + r];
                     const float sr = Sa[kb].re[r], si = Sa[kb].im[r];
-                    Sa[kb].re[r] = gg.x * sr - gg.y * si;
-                    Sa[kb].im[r] = gg.x * si + gg.y * sr;
+                    Sa[kb].re[r] = __builtin_fmaf(gg.x, sr, -gg.y * si);
+                    Sa[kb].im[r] = __builtin_fmaf(gg.x, si, gg.y * sr);
                 }
             // o = conj(O^*); rows past T and columns past the slice are dropped by the buffer
 #pragma unroll
@@ -610,7 +653,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         constexpr float INV_2PI = 0.15915494309189535f;
         float lm[TPL][4], lph[TPL][4];    // inclusive over the lane's tokens
         float qm[4], qph[4];              // exclusive over the wave's earlier segments
-        auto pretot = [&]() {             // first two levels, wave totals to LDS
+        auto pretot_body = [&](auto padded) {
             const bool s0 = tsg == 0, s01 = tsg < 2;
             float tm[4], tp[4];
 #pragma unroll
@@ -622,7 +665,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     const u32 wt = k < 2 ? pt[u].x : pt[u].y;
                     float a = (k & 1) ? bf_hi(wa) : bf_lo(wa);
                     const float th = (k & 1) ? bf_hi(wt) : bf_lo(wt);
-                    a = a == 0.f ? 1.f : a;
+                    if constexpr (decltype(padded)::value) a = a == 0.f ? 1.f : a;
                     rm *= a;
                     rp = __builtin_fmaf(th, INV_2PI, rp);
                     lm[u][k] = rm;
@@ -646,6 +689,13 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 tw[0] = make_float4(tm[0], tp[0], tm[1], tp[1]);
                 tw[1] = make_float4(tm[2], tp[2], tm[3], tp[3]);
             }
+        };
+
+        // first two levels for chunk ch (inputs in pa, pt), wave totals to LDS.  Only a chunk
+        // with padding (ragged tail, m < 64) needs the alpha = 0 -> 1 substitution.
+        auto pretot = [&](int ch) {
+            if ((ch + 1) * C <= T && m == MP) pretot_body(std::false_type{});
+            else pretot_body(std::true_type{});
         };
 
         // phase 1: g and the operands conj(Q)G, conj(K)G, K/G of chunk ch into set ch & 1
@@ -673,12 +723,13 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     const float ei = __builtin_amdgcn_rcpf(A);
                     const float sn = __builtin_amdgcn_sinf(Ph), cs = __builtin_amdgcn_cosf(Ph);
                     const float gr = A * cs, gi = A * sn;
-                    const float hr = ei * cs, hi = -ei * sn;         // 1 / g
                     const u32 qw = pq[u][k], kw = pk[u][k];
                     const float qr = bf_lo(qw), qi = bf_hi(qw), kr = bf_lo(kw), ki = bf_hi(kw);
-                    wq[k] = pack_bf16(qr * gr + qi * gi, qr * gi - qi * gr);
-                    wk[k] = pack_bf16(kr * gr + ki * gi, kr * gi - ki * gr);
-                    wi[k] = pack_bf16(kr * hr - ki * hi, kr * hi + ki * hr);
+                    // conj(k) e^{i phi}; conj(k) g = |g| of it, k / g = its conjugate / |g|
+                    const float kur = __builtin_fmaf(kr, cs, ki * sn), kui = __builtin_fmaf(kr, sn, -ki * cs);
+                    wq[k] = pack_bf16(__builtin_fmaf(qr, gr, qi * gi), __builtin_fmaf(qr, gi, -qi * gr));
+                    wk[k] = pack_bf16(A * kur, A * kui);
+                    wi[k] = pack_bf16(ei * kur, -ei * kui);
                     gl[k] = make_float2(gr, gi);
                 }
                 *reinterpret_cast<u32x4*>(S + OFF_QG + rm_off(tl, pc0)) = wq;
@@ -731,13 +782,13 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         auto produce2 = [&](int ch) {
             if (ch + 1 < nchunks) load_qk(ch + 1);
             if (pw < NRB) invert_diag(ch);
-            if (ch + 1 < nchunks) pretot();
+            if (ch + 1 < nchunks) pretot(ch + 1);
         };
 
         if (nchunks > 0) {
             load_at(0);
             load_qk(0);
-            pretot();
+            pretot(0);
         }
         __syncthreads();          // wave totals of chunk 0
         for (int ch = -1; ch < nchunks; ++ch) {
