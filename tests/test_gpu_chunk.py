@@ -222,3 +222,93 @@ def test_zero_heads_is_noop():
     say("B=0")
     o, S = sfda.chunk_fwd(e, e, e, e[..., 0], e[..., 0], e[..., 0, 0], None, C=64)
     assert o.numel() == 0 and S.numel() == 0
+
+
+# --------------------------------------------------------------------------- bf16 pipeline kernel
+# bf16 inputs run a different kernel (producer/consumer pipeline with range-checked buffer
+# loads and stores); its ragged tails, narrow shapes and slices are covered here.
+
+@pytest.mark.parametrize("C", [16, 32, 64])
+def test_bf16_chunk_sizes_ragged(C):
+    check(small(T=3 * C + 5, dtype="bf16"), C, 2e-2, label=f"bf16 C{C}")
+
+
+@pytest.mark.parametrize("T", [1, 15, 64, 65])
+def test_bf16_short_sequences(T):
+    check(small(T=T, dtype="bf16"), 64, 2e-2, label=f"bf16 T{T}")
+
+
+@pytest.mark.parametrize("m,n", [(5, 3), (16, 8), (33, 24), (60, 40), (64, 80), (48, 130)])
+def test_bf16_odd_shapes(m, n):
+    # m % 4 != 0 loads one channel per instruction; m < 64 leaves channel groups past m;
+    # n that is not a multiple of 16 leaves a partial consumer wave
+    check(small(T=70, m=m, n=n, B=2, H=1, dtype="bf16"), 16, 2e-2, label=f"bf16 m{m}n{n}")
+
+
+@pytest.mark.parametrize("slice", [8, 16, 24, 32, 40, 64])
+def test_bf16_slices(slice):
+    check(small(T=130, n=64, dtype="bf16"), 64, 2e-2, slice=slice, label=f"bf16 slice{slice}")
+
+
+def test_bf16_in_f32_out():
+    check(small(T=150, dtype="bf16"), 64, 2e-2, out_dtype="f32", label="bf16 in, f32 out")
+
+
+def test_bf16_zero_state_and_strong_decay():
+    laws = I.Laws(alpha=("uniform", 0.4, 0.41), theta=("uniform", -math.pi, math.pi),
+                  beta=("uniform", 0.0, 1.0), s0_scale=None)
+    check(small(T=200, laws=laws, dtype="bf16"), 64, 2e-2, label="bf16 S0=0 alpha0.4")
+
+
+def test_bf16_resume_in_place():
+    """bf16 inputs: three calls carrying S_T in place equal one call over the whole sequence."""
+    import torch
+    from paper_2607_11897_amd import sfda
+    x = small(T=150, dtype="bf16")
+    d = upload(x)
+    say("bf16 resume")
+    S = d["S0"].clone()
+    outs = []
+    for (a, b) in ((0, 37), (37, 101), (101, 150)):
+        sl = lambda t: t[:, :, a:b].contiguous()
+        o, _ = sfda.chunk_fwd(sl(d["q"]), sl(d["k"]), sl(d["v"]), sl(d["alpha"]), sl(d["theta"]),
+                              sl(d["beta"]), S, C=64, S_T=S)
+        outs.append(o)
+    torch.cuda.synchronize()
+    o_ref, S_ref = run_oracle(x)
+    assert rel_err(to_complex(torch.cat(outs, dim=2)), o_ref) <= 2e-2
+    assert rel_err(to_complex(S), S_ref) <= 2e-2
+
+
+def test_bf16_T0_copies_state():
+    import torch
+    from paper_2607_11897_amd import sfda
+    x = small(T=0, dtype="bf16")
+    d = upload(x)
+    say("bf16 T=0")
+    o, S = sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], d["S0"], C=64)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_complex(S), x.S0)
+
+
+def test_bf16_guard_bands_untouched():
+    """Canary words around o (bf16) and S_T stay intact: the dropped out-of-range stores of the
+    ragged tail and of the columns past n never reach neighbouring memory."""
+    import torch
+    from paper_2607_11897_amd import sfda
+    x = small(T=77, m=40, n=24, B=2, H=2, dtype="bf16")
+    d = upload(x)
+    B, H, T, m, n = x.shape
+    pad = 256
+    canary = -12288.0
+    ob = torch.full((2 * pad + B * H * T * n * 2,), canary, device="cuda", dtype=torch.bfloat16)
+    sb = torch.full((2 * pad + B * H * m * n * 2,), canary, device="cuda")
+    o = ob[pad:pad + B * H * T * n * 2].view(B, H, T, n, 2)
+    S = sb[pad:pad + B * H * m * n * 2].view(B, H, m, n, 2)
+    say("bf16 guard bands")
+    sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], d["S0"], C=32, o=o, S_T=S)
+    torch.cuda.synchronize()
+    for buf in (ob, sb):
+        assert torch.all(buf[:pad] == canary) and torch.all(buf[-pad:] == canary)
+    o_ref, S_ref = run_oracle(x)
+    assert rel_err(to_complex(o), o_ref) <= 2e-2 and rel_err(to_complex(S), S_ref) <= 2e-2
