@@ -8,9 +8,11 @@
 // which reads S once and writes it once -- the step is bound by HBM bandwidth.
 //
 // Launch: one 256-thread workgroup per (head, slice of NP value columns); NP is a power of
-// two <= 64.  Thread (rg, j) owns column j and rows rg, rg + G, rg + 2G, ... (G = 256 / NP),
-// so each wave reads and writes whole contiguous row segments.  Column sums over rows are
-// reduced in a fixed order through LDS (deterministic; no atomics).
+// two <= 64.  Thread (rg, j) owns column j (for even n: the column pair 2j, 2j + 1, so every
+// state access is 16 bytes) and rows rg, rg + G, rg + 2G, ... (G = 256 / threads per row),
+// so each wave reads and writes whole contiguous row segments.  The state is read with
+// non-temporal loads (it is streamed once per step; measured faster than cached loads).
+// Column sums over rows are reduced in a fixed order through LDS (deterministic; no atomics).
 #include "sfda_device.h"
 #include "sfda_launch.h"
 
@@ -125,6 +127,124 @@ __global__ __launch_bounds__(256) void step_kernel(
     }
 }
 
+// Column-pair variant for even n: thread (rg, jp) owns columns 2 jp, 2 jp + 1 of the slice.
+template <typename TIN, typename TOUT, int NP>
+__global__ __launch_bounds__(256) void step_pair_kernel(
+    const TIN* __restrict__ q, const TIN* __restrict__ k, const TIN* __restrict__ v,
+    const TIN* __restrict__ alpha, const TIN* __restrict__ theta, const TIN* __restrict__ beta,
+    float* __restrict__ S, TOUT* __restrict__ o, int m, int n, int n_slices)
+{
+    constexpr int NPR = NP / 2;                  // column pairs per workgroup
+    constexpr int G = 256 / NPR;                 // row groups
+    constexpr int RPT = (64 + G - 1) / G;        // rows per thread (m <= 64)
+    typedef float f32v4 __attribute__((ext_vector_type(4)));
+    const long bh = blockIdx.x / n_slices;
+    const int sl = blockIdx.x - static_cast<int>(bh) * n_slices;
+    const int tid = threadIdx.x;
+    const int jp = tid % NPR;
+    const int rg = tid / NPR;
+    const int j = sl * NP + 2 * jp;              // first column of the pair
+    const bool colok = j < n;                    // n even: j + 1 < n as well
+
+    __shared__ float2 lam_s[64], k_s[64], q_s[64];
+    __shared__ float4 red_a[G][NPR], red_b[G][NPR];
+    __shared__ float4 delta_s[NPR];
+    __shared__ float2 qk_s;
+
+    float* Sh = S + bh * m * n * 2;
+    float4 s[RPT];
+#pragma unroll
+    for (int r = 0; r < RPT; ++r) {
+        const int i = rg + G * r;
+        if (i < m && colok) {
+            const f32v4 x = __builtin_nontemporal_load(reinterpret_cast<const f32v4*>(Sh + 2 * (static_cast<long>(i) * n + j)));
+            s[r] = make_float4(x.x, x.y, x.z, x.w);
+        } else {
+            s[r] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    }
+
+    if (tid < 64) {
+        float2 qk = make_float2(0.f, 0.f);
+        if (tid < m) {
+            const long e = bh * m + tid;
+            const float a = Elem<TIN>::load(alpha, e);
+            float sn, cs;
+            sincosf(Elem<TIN>::load(theta, e), &sn, &cs);
+            lam_s[tid] = make_float2(a * cs, a * sn);
+            const float2 kk = Elem<TIN>::load2(k, e);
+            const float2 qq = Elem<TIN>::load2(q, e);
+            k_s[tid] = kk;
+            q_s[tid] = qq;
+            qk = make_float2(qq.x * kk.x + qq.y * kk.y, qq.x * kk.y - qq.y * kk.x);  // conj(q) k
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+            qk.x += __shfl_xor(qk.x, off);
+            qk.y += __shfl_xor(qk.y, off);
+        }
+        if (tid == 0) qk_s = qk;
+    }
+    __syncthreads();
+
+    // S' = Lambda S and the column partial sums a = k^* S', b = q^* S' (both columns)
+    float4 pa = make_float4(0.f, 0.f, 0.f, 0.f), pb = pa;
+#pragma unroll
+    for (int r = 0; r < RPT; ++r) {
+        const int i = rg + G * r;
+        if (i < m) {
+            const float2 l = lam_s[i], kk = k_s[i], qq = q_s[i];
+            const float4 x = s[r];
+            const float4 y = make_float4(l.x * x.x - l.y * x.y, l.x * x.y + l.y * x.x,
+                                         l.x * x.z - l.y * x.w, l.x * x.w + l.y * x.z);
+            s[r] = y;
+            pa.x += kk.x * y.x + kk.y * y.y; pa.y += kk.x * y.y - kk.y * y.x;
+            pa.z += kk.x * y.z + kk.y * y.w; pa.w += kk.x * y.w - kk.y * y.z;
+            pb.x += qq.x * y.x + qq.y * y.y; pb.y += qq.x * y.y - qq.y * y.x;
+            pb.z += qq.x * y.z + qq.y * y.w; pb.w += qq.x * y.w - qq.y * y.z;
+        }
+    }
+    red_a[rg][jp] = pa;
+    red_b[rg][jp] = pb;
+    __syncthreads();
+
+    if (rg == 0) {
+        float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
+#pragma unroll
+        for (int gi = 0; gi < G; ++gi) {
+            const float4 x = red_a[gi][jp], y = red_b[gi][jp];
+            a.x += x.x; a.y += x.y; a.z += x.z; a.w += x.w;
+            b.x += y.x; b.y += y.y; b.z += y.z; b.w += y.w;
+        }
+        float4 d = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (colok) {
+            const float bt = Elem<TIN>::load(beta, bh);
+            const float2 v0 = Elem<TIN>::load2(v, bh * n + j), v1 = Elem<TIN>::load2(v, bh * n + j + 1);
+            d = make_float4(bt * (v0.x - a.x), bt * (-v0.y - a.y), bt * (v1.x - a.z), bt * (-v1.y - a.w));
+            const float2 qk = qk_s;
+            const float4 ob = make_float4(b.x + qk.x * d.x - qk.y * d.y, b.y + qk.x * d.y + qk.y * d.x,
+                                          b.z + qk.x * d.z - qk.y * d.w, b.w + qk.x * d.w + qk.y * d.z);
+            Elem<TOUT>::store2(o, bh * n + j, ob.x, -ob.y);
+            Elem<TOUT>::store2(o, bh * n + j + 1, ob.z, -ob.w);
+        }
+        delta_s[jp] = d;
+    }
+    __syncthreads();
+
+    const float4 d = delta_s[jp];
+#pragma unroll
+    for (int r = 0; r < RPT; ++r) {
+        const int i = rg + G * r;
+        if (i < m && colok) {
+            const float2 kk = k_s[i];
+            const float4 x = s[r];
+            *reinterpret_cast<float4*>(Sh + 2 * (static_cast<long>(i) * n + j)) =
+                make_float4(x.x + kk.x * d.x - kk.y * d.y, x.y + kk.x * d.y + kk.y * d.x,
+                            x.z + kk.x * d.z - kk.y * d.w, x.w + kk.x * d.w + kk.y * d.z);
+        }
+    }
+}
+
 template <typename TIN, typename TOUT>
 static hipError_t launch_step_t(const StepLaunch& L, hipStream_t st)
 {
@@ -144,12 +264,26 @@ static hipError_t launch_step_t(const StepLaunch& L, hipStream_t st)
         hipLaunchKernelGGL((step_kernel<TIN, TOUT, NP_>), grid, dim3(256), 0, st, q, k, v, a, \
                            th, b, L.S, o, L.m, L.n, n_slices);                           \
         break;
+#define SFDA_STEP_PAIR_CASE(NP_)                                                         \
+    case NP_:                                                                            \
+        hipLaunchKernelGGL((step_pair_kernel<TIN, TOUT, NP_>), grid, dim3(256), 0, st, q, k, v, \
+                           a, th, b, L.S, o, L.m, L.n, n_slices);                        \
+        break;
+    if ((L.n & 1) == 0 && np >= 2) {   // 16-byte state accesses (row starts stay 16-byte aligned)
+        switch (np) {
+            SFDA_STEP_PAIR_CASE(2) SFDA_STEP_PAIR_CASE(4) SFDA_STEP_PAIR_CASE(8)
+            SFDA_STEP_PAIR_CASE(16) SFDA_STEP_PAIR_CASE(32) SFDA_STEP_PAIR_CASE(64)
+            default: return hipErrorInvalidValue;
+        }
+        return hipGetLastError();
+    }
     switch (np) {
         SFDA_STEP_CASE(1) SFDA_STEP_CASE(2) SFDA_STEP_CASE(4) SFDA_STEP_CASE(8)
         SFDA_STEP_CASE(16) SFDA_STEP_CASE(32) SFDA_STEP_CASE(64)
         default: return hipErrorInvalidValue;
     }
 #undef SFDA_STEP_CASE
+#undef SFDA_STEP_PAIR_CASE
     return hipGetLastError();
 }
 
