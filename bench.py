@@ -173,7 +173,7 @@ def bench_decode(args, stream):
             "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS,
                          "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
                          "traffic": load_traffic("step", D["name"]),
-                         "kernel": "sfda::step_kernel<f32, 64>",
+                         "kernel": "sfda::step_pair_kernel<f32, 64>",
                          "bytes_per_launch": int(bytes_step)}}
 
 
@@ -224,8 +224,8 @@ def rmw_calibration(args):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--only", choices=["chunk", "decode"], default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--mode", choices=["bench", "copy", "rmw"], default="bench")
@@ -250,12 +250,13 @@ def main():
         return
     stream = torch.cuda.current_stream()
     out = {}
-    if args.only in (None, "decode"):
-        out["decode"] = bench_decode(args, stream)
     if args.only == "decode":
+        out["decode"] = bench_decode(args, stream)
         print(json.dumps(out), flush=True)
         return
     r = bench_chunk(args, stream)
+    if args.only is None:
+        out["decode"] = bench_decode(args, stream)
     w = r["w"]
     line = {
         "metric": METRIC, "value": round(r["tokens_per_s"], 1), "unit": "tokens/s", "n_gpus": 1,
