@@ -113,7 +113,8 @@ sfda_status_t sfda_chunk_fwd_sliced(const void* q, const void* k, const void* v,
  *   q, k, v, alpha, theta, beta : one token per head (device, in_dtype), layouts above.
  *   S : [B,H,m,n] complex float32, read and overwritten.
  *   o : [B,H,n] complex (device, out_dtype).  o must not overlap S or any input.
- *   B, H >= 0; 1 <= m <= 64; n >= 1.
+ *   B, H >= 0; 1 <= m <= 64; 1 <= n < 2^22 (each head's state rows are addressed with
+ *   32-bit offsets); SFDA_ERR_SHAPE otherwise.
  */
 sfda_status_t sfda_step(const void* q, const void* k, const void* v,
                         const void* alpha, const void* theta, const void* beta,

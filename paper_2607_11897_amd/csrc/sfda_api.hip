@@ -129,6 +129,7 @@ sfda_status_t sfda_step(const void* q, const void* k, const void* v, const void*
 {
     if (!dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return SFDA_ERR_DTYPE;
     if (B < 0 || H < 0 || m < 1 || m > 64 || n < 1) return SFDA_ERR_SHAPE;
+    if (n >= (1 << 22)) return SFDA_ERR_SHAPE;   // state rows addressed with 32-bit offsets
     const long BH = static_cast<long>(B) * H;
     int np = 1;
     while (np < n && np < 64) np <<= 1;

@@ -77,6 +77,7 @@ def test_chunk_argument_errors(lib):
 def test_step_argument_errors(lib):
     assert step(lib, S=None) == 1
     assert step(lib, m=0) == 2 and step(lib, m=65) == 2 and step(lib, n=0) == 2
+    assert step(lib, n=1 << 22) == 2                  # state rows use 32-bit offsets
     assert step(lib, din=5) == 4
     assert step(lib, v=P[2] + 4) == 5
     assert step(lib, o=P[6]) == 6                     # o on top of S

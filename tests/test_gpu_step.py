@@ -26,7 +26,9 @@ def _head_list(B, H):
 
 @pytest.mark.parametrize("B,H,m,n,dtype", [(2, 3, 64, 64, "f32"), (1, 2, 5, 3, "f32"),
                                            (2, 2, 64, 100, "f32"), (1, 1, 16, 8, "f32"),
-                                           (2, 3, 64, 64, "bf16"), (3, 1, 33, 17, "f32")])
+                                           (2, 3, 64, 64, "bf16"), (3, 1, 33, 17, "f32"),
+                                           (2, 2, 60, 40, "f32"), (1, 3, 50, 130, "bf16"),
+                                           (2, 1, 7, 2, "f32"), (1, 2, 64, 4, "bf16")])
 def test_step_small(B, H, m, n, dtype):
     import torch
     import oracle
@@ -48,6 +50,36 @@ def test_step_small(B, H, m, n, dtype):
         assert eo <= tol and es <= tol, (step, eo, es)
         if dtype == "f32":
             S = to_complex(Sd)   # keep both sides on the same state (checks one step at a time)
+
+
+@pytest.mark.parametrize("m,n", [(64, 64), (60, 40), (50, 130), (7, 2)])
+def test_step_guard_bands_untouched(m, n):
+    """Canary words around S and o stay intact: rows past m, columns past n in a ragged last
+    slice and the last head's state never write outside their buffers."""
+    import torch
+    import oracle
+    from paper_2607_11897_amd import sfda
+    B, H = 2, 2
+    heads = _head_list(B, H)
+    pad = 256
+    canary = -12288.0
+    S = np.stack([I.decode_state_head(b, h, m, n) for (b, h) in heads]).reshape(B, H, m, n)
+    sb = torch.full((2 * pad + B * H * m * n * 2,), canary, device="cuda")
+    ob = torch.full((2 * pad + B * H * n * 2,), canary, device="cuda")
+    Sd = sb[pad:pad + B * H * m * n * 2].view(B, H, m, n, 2)
+    Sd.copy_(to_device(I.to_storage(S, "f32"), "f32"))
+    o = ob[pad:pad + B * H * n * 2].view(B, H, n, 2)
+    x = I.decode_step_heads(0, heads, m, n)
+    st = x.storage()
+    d = {k: to_device(st[k], "f32").reshape((B, H) + st[k].shape[2:]) for k in st}
+    say("step guard bands", m, n)
+    sfda.step(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], Sd, o=o)
+    torch.cuda.synchronize()
+    for buf in (sb, ob):
+        assert torch.all(buf[:pad] == canary) and torch.all(buf[-pad:] == canary)
+    rs = lambda a: a.reshape((B, H) + a.shape[2:])
+    o_ref, S_ref = oracle.step(rs(x.q), rs(x.k), rs(x.v), rs(x.alpha), rs(x.theta), rs(x.beta), S)
+    assert rel_err(to_complex(o), o_ref) <= 1e-4 and rel_err(to_complex(Sd), S_ref) <= 1e-4
 
 
 def test_decode_f32_b512h32_1024_steps_sampled_heads():
