@@ -179,14 +179,17 @@ __device__ __forceinline__ int blk_frag(int row, int chunk) {
 // N = (I - X)^{-1} for X strictly lower triangular (X = -(D_beta L') on a diagonal block),
 // i.e. N = I + X N, by forward substitution over the pivots s = 0 .. 14.  Lane (i, cg) --
 // i = lane % 16, cg = lane / 16 -- holds row i of X (zero on and above the diagonal, so
-// rows i <= s take no update) and row i, columns 4cg .. 4cg+3 of N; the pivot row
-// N(s, 4cg .. 4cg+3) is lane s of the lane's own 16-lane row (DPP row broadcast).
+// rows i <= s take no update) and row i, columns cg, cg + 4, cg + 8, cg + 12 of N (slot k
+// holds column 4k + cg); the pivot row N(s, .) is lane s of the lane's own 16-lane row (DPP
+// row broadcast).  N is lower triangular, so the pivot row is zero past column s and slot
+// k takes part only in the steps s >= 4k: 36 slot-steps instead of 60.
 template <int S>
 __device__ __forceinline__ void inv_step(float (&nr)[4], float (&ni)[4], const float2 (&xrow)[16])
 {
     const float xr = xrow[S].x, xi = xrow[S].y;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
+        if (4 * k > S) continue;
         const float pr = row_lane<S>(nr[k]), pi = row_lane<S>(ni[k]);
         nr[k] = __builtin_fmaf(xr, pr, __builtin_fmaf(-xi, pi, nr[k]));
         ni[k] = __builtin_fmaf(xr, pi, __builtin_fmaf(xi, pr, ni[k]));
@@ -770,11 +773,12 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             }
             float nr[4], ni[4];
 #pragma unroll
-            for (int k = 0; k < 4; ++k) { nr[k] = i == 4 * cgi + k ? 1.f : 0.f; ni[k] = 0.f; }
+            for (int k = 0; k < 4; ++k) { nr[k] = i == 4 * k + cgi ? 1.f : 0.f; ni[k] = 0.f; }
             inv_steps(nr, ni, xrow, std::make_integer_sequence<int, 15>{});
-            const u32x4 w = {pack_bf16(nr[0], ni[0]), pack_bf16(nr[1], ni[1]),
-                             pack_bf16(nr[2], ni[2]), pack_bf16(nr[3], ni[3])};
-            *reinterpret_cast<u32x4*>(S + OFF_ND + pw * 1024 + blk_frag(i, cgi)) = w;
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                *reinterpret_cast<u32*>(S + OFF_ND + pw * 1024 + blk_off(i, 4 * k + cgi)) =
+                    pack_bf16(nr[k], ni[k]);
         };
 
         // phase 2: diagonal blocks of L' and their inverses, chunk ch; then the first two
@@ -799,6 +803,10 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             if (ch + 1 < nchunks) produce2(ch + 1);
             __syncthreads();
         }
+        // The compiler joins the two roles' control flow after the producer's exit, and the
+        // wait-count analysis then treats the producer's last loads as in flight inside the
+        // consumer loop; clearing them here keeps that loop from waiting on its own V loads.
+        __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
     }
 }
 
