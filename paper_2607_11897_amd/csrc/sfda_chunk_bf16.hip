@@ -398,6 +398,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 cmma(d, fn[p], bsplit(R[p]));
                 db[p] = bsplit(d);
             }
+            if (ch + 1 < nchunks) load_v(ch + 1);   // v of this chunk is consumed
         };
 
         TOUT* const go = static_cast<TOUT*>(args.o);
@@ -452,12 +453,28 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     for (int e = 0; e < 2; ++e) cmma(Sa[ki_kb(sg - NQ - NA, e)], f[e], db[ki_tb(sg - NQ - NA, e)]);
                 }
             };
+            // o = conj(O^*) is final after the tril(A) Delta stages; its stores are spread
+            // over the state-update stages (two rows of four per stage), so they issue while
+            // those products run.  Rows past T and columns past the slice are dropped by the
+            // buffer range.
+            auto store_o = [&](int q) {
+                const int rb = q / 4, r = q % 4;
+                const int tr = t0 + rb * 16;
+                const rsrc_t ro = make_rsrc(go + 2 * (base_tn + static_cast<long>(tr) * n),
+                                            max(T - tr, 0) * n * Out<TOUT>::BYTES);
+                Out<TOUT>::store(ro, voff_o[r], O[rb].re[r], -O[rb].im[r]);
+            };
+            constexpr int SPS = 4 * NRB / NK;      // stores per state-update stage
             load(0, buf[0]);
 #pragma unroll
             for (int sg = 0; sg < NST; ++sg) {
                 if (sg + 1 < NST) load(sg + 1, buf[(sg + 1) & 1]);
                 __builtin_amdgcn_sched_barrier(0);
                 mma(sg, buf[sg & 1]);
+                if (sg >= NQ + NA) {
+#pragma unroll
+                    for (int e = 0; e < SPS; ++e) store_o((sg - NQ - NA) * SPS + e);
+                }
             }
             // S <- diag(g_C) (S + (K/G)^T Delta)
 #pragma unroll
@@ -469,16 +486,6 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     Sa[kb].re[r] = __builtin_fmaf(gg.x, sr, -gg.y * si);
                     Sa[kb].im[r] = __builtin_fmaf(gg.x, si, gg.y * sr);
                 }
-            // o = conj(O^*); rows past T and columns past the slice are dropped by the buffer
-#pragma unroll
-            for (int rb = 0; rb < NRB; ++rb) {
-                const int tr = t0 + rb * 16;
-                const rsrc_t ro = make_rsrc(go + 2 * (base_tn + static_cast<long>(tr) * n),
-                                            max(T - tr, 0) * n * Out<TOUT>::BYTES);
-#pragma unroll
-                for (int r = 0; r < 4; ++r) Out<TOUT>::store(ro, voff_o[r], O[rb].re[r], -O[rb].im[r]);
-            }
-            if (ch + 1 < nchunks) load_v(ch + 1);
         };
 
         auto consume_gram = [&](int ch) {      // A blocks of chunk ch (set ch & 1)
