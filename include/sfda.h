@@ -21,8 +21,9 @@
  * For the decode step drop the T axis: q, k [B, H, m], v, o [B, H, n], alpha, theta [B, H, m],
  * beta [B, H].
  *
- * Ownership: the caller allocates and frees every buffer and owns the stream; the library
- * allocates no device memory and keeps no state between calls (calls are reentrant; calls
+ * Ownership: the caller allocates and frees every buffer (including the workspace of
+ * sfda_chunk_fwd_segmented) and owns the stream; the library allocates no device memory
+ * and keeps no state between calls (calls are reentrant; calls
  * that write the same buffers on different streams race, as any two kernels would).
  *
  * Errors: all argument checks run on the host before anything is enqueued; on any error
@@ -35,6 +36,8 @@
  */
 #ifndef SFDA_H
 #define SFDA_H
+
+#include <stddef.h>
 
 #ifdef __cplusplus
 extern "C" {
@@ -104,6 +107,38 @@ sfda_status_t sfda_chunk_fwd_sliced(const void* q, const void* k, const void* v,
                                     int B, int H, int T, int m, int n, int C, int slice,
                                     sfda_dtype_t in_dtype, sfda_dtype_t out_dtype,
                                     sfda_stream_t stream);
+
+/*
+ * sfda_chunk_fwd_segmented -- sfda_chunk_fwd with each head's sequence cut into G
+ * segments of T / G tokens that are scanned in parallel (for few heads over long
+ * sequences, where one workgroup per head leaves most of the GPU idle).  It uses the
+ * exact affine law of a stretch of tokens (Thm 4.4: S_end = P S_in + B, P the product of
+ * the stretch's transitions, B its write from the zero state) composed along the segments
+ * (Lemma A.2, the boundary-state scan of Thm 6.1 at segment granularity): every segment's
+ * P_g (final state from S0 = I with v = 0) and B_g (final state from S0 = 0) come from
+ * the chunk kernel, a fold gives S_in[g + 1] = P_g S_in[g] + B_g and S_T = S_in[G], and
+ * a last chunk pass writes o from the exact incoming states.  About three times the work
+ * of sfda_chunk_fwd, spread over G times as many workgroups; results agree with it to
+ * rounding.
+ *   Arguments and errors as sfda_chunk_fwd, plus:
+ *   G >= 1 with T a multiple of G * C (SFDA_ERR_SHAPE otherwise; T == 0 is as
+ *   sfda_chunk_fwd).
+ *   workspace : device memory of at least sfda_chunk_fwd_segmented_workspace_bytes(B, H,
+ *               m, n, G) bytes (SFDA_ERR_SHAPE if smaller, SFDA_ERR_NULL if NULL),
+ *               16-byte aligned, not overlapping any other argument (SFDA_ERR_ALIAS);
+ *               no initial contents needed.  Holds, per segment, P_g (m x m), B_g and
+ *               the incoming state (m x n), complex float32.
+ *   S_T == S0 (in place) is allowed.
+ */
+size_t sfda_chunk_fwd_segmented_workspace_bytes(int B, int H, int m, int n, int G);
+
+sfda_status_t sfda_chunk_fwd_segmented(const void* q, const void* k, const void* v,
+                                       const void* alpha, const void* theta, const void* beta,
+                                       const float* S0, void* o, float* S_T,
+                                       int B, int H, int T, int m, int n, int C, int G,
+                                       sfda_dtype_t in_dtype, sfda_dtype_t out_dtype,
+                                       void* workspace, size_t workspace_bytes,
+                                       sfda_stream_t stream);
 
 /*
  * sfda_step -- one recurrent decode token per (b, h) (Sec. 3, Eq. (sfda) and the readout),

@@ -50,7 +50,8 @@ static sfda_status_t chunk_fwd_impl(const void* q, const void* k, const void* v,
                                     const void* alpha, const void* theta, const void* beta,
                                     const float* S0, void* o, float* S_T, int B, int H, int T,
                                     int m, int n, int C, sfda_dtype_t in_dtype,
-                                    sfda_dtype_t out_dtype, sfda_stream_t stream, int slice)
+                                    sfda_dtype_t out_dtype, sfda_stream_t stream, int slice,
+                                    void* = nullptr, size_t = 0, bool check_only = false)
 {
     if (!dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return SFDA_ERR_DTYPE;
     if (B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1) return SFDA_ERR_SHAPE;
@@ -92,6 +93,7 @@ static sfda_status_t chunk_fwd_impl(const void* q, const void* k, const void* v,
             return SFDA_ERR_ALIAS;
     }
 
+    if (check_only) return SFDA_OK;
     sfda::ChunkLaunch L;
     L.q = q; L.k = k; L.v = v; L.alpha = alpha; L.theta = theta; L.beta = beta;
     L.S0 = S0; L.o = o; L.S_T = S_T;
@@ -120,6 +122,77 @@ sfda_status_t sfda_chunk_fwd_sliced(const void* q, const void* k, const void* v,
 {
     return chunk_fwd_impl(q, k, v, alpha, theta, beta, S0, o, S_T, B, H, T, m, n, C, in_dtype,
                           out_dtype, stream, slice);
+}
+
+size_t sfda_chunk_fwd_segmented_workspace_bytes(int B, int H, int m, int n, int G)
+{
+    if (B <= 0 || H <= 0 || m < 1 || m > 64 || n < 1 || G < 1) return 0;
+    const long segs = static_cast<long>(B) * H * G;
+    return static_cast<size_t>(segs) * (static_cast<size_t>(m) * m + 2 * static_cast<size_t>(m) * n) * 8;
+}
+
+sfda_status_t sfda_chunk_fwd_segmented(const void* q, const void* k, const void* v,
+                                       const void* alpha, const void* theta, const void* beta,
+                                       const float* S0, void* o, float* S_T, int B, int H, int T,
+                                       int m, int n, int C, int G, sfda_dtype_t in_dtype,
+                                       sfda_dtype_t out_dtype, void* workspace,
+                                       size_t workspace_bytes, sfda_stream_t stream)
+{
+    if (G < 1) return SFDA_ERR_SHAPE;
+    const int slice_n = n <= 64 ? ((n + 7) / 8) * 8 : 64;
+    // the shared checks (and the whole call when there is nothing to split)
+    if (T == 0 || static_cast<long>(B) * H == 0 || !dtype_ok(in_dtype) || !dtype_ok(out_dtype) ||
+        B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1 || (C != 16 && C != 32 && C != 64))
+        return chunk_fwd_impl(q, k, v, alpha, theta, beta, S0, o, S_T, B, H, T, m, n, C, in_dtype,
+                              out_dtype, stream, slice_n);
+    if (T % (static_cast<long>(G) * C) != 0) return SFDA_ERR_SHAPE;
+    const long BH = static_cast<long>(B) * H;
+    if (BH * G > 0x7FFFFFFFL) return SFDA_ERR_SHAPE;
+    if (!workspace) return SFDA_ERR_NULL;
+    if (!aligned16(workspace)) return SFDA_ERR_ALIGN;
+    const size_t need = sfda_chunk_fwd_segmented_workspace_bytes(B, H, m, n, G);
+    if (workspace_bytes < need) return SFDA_ERR_SHAPE;
+    // validate the buffers the way sfda_chunk_fwd does (nothing is launched on error)
+    {
+        const sfda_status_t st0 = chunk_fwd_impl(q, k, v, alpha, theta, beta, S0, o, S_T, B, H, T,
+                                                 m, n, C, in_dtype, out_dtype, stream, slice_n,
+                                                 nullptr, 0, /*check_only=*/true);
+        if (st0 != SFDA_OK) return st0;
+    }
+    const long ei = esize(in_dtype), eo = esize(out_dtype), BHT = BH * T;
+    const Range rw = range_of(workspace, static_cast<long>(need));
+    const Range all[] = {range_of(q, BHT * m * 2 * ei), range_of(k, BHT * m * 2 * ei),
+                         range_of(v, BHT * n * 2 * ei), range_of(alpha, BHT * m * ei),
+                         range_of(theta, BHT * m * ei), range_of(beta, BHT * ei),
+                         range_of(o, BHT * n * 2 * eo), range_of(S0, BH * m * n * 2 * 4),
+                         range_of(S_T, BH * m * n * 2 * 4)};
+    for (const Range& r : all)
+        if (overlap(rw, r)) return SFDA_ERR_ALIAS;
+
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    const long segs = BH * G;
+    float* P = static_cast<float*>(workspace);                      // [segs][m][m]
+    float* Bs = P + segs * m * m * 2;                               // [segs][m][n]
+    float* Sin = Bs + segs * static_cast<long>(m) * n * 2;          // [segs][m][n]
+    // [B, H, T, .] with T = G * Ts is [B*H*G, Ts, .]: each segment runs as a head
+    sfda::ChunkLaunch L;
+    L.q = q; L.k = k; L.alpha = alpha; L.theta = theta; L.beta = beta;
+    L.B = static_cast<int>(segs); L.H = 1; L.T = T / G; L.m = m; L.C = C;
+    L.in_bf16 = in_dtype == SFDA_BF16;
+    L.out_bf16 = out_dtype == SFDA_BF16;
+    // P_g: S0 = I, v = 0 (in place on the identity), no output
+    if (sfda::launch_identity(P, segs, m, st) != hipSuccess) return SFDA_ERR_HIP;
+    L.v = nullptr; L.S0 = P; L.S_T = P; L.o = nullptr; L.n = m; L.slice = ((m + 7) / 8) * 8;
+    if (sfda::launch_chunk(L, st) != hipSuccess) return SFDA_ERR_HIP;
+    // B_g: S0 = 0, no output
+    L.v = v; L.S0 = nullptr; L.S_T = Bs; L.o = nullptr; L.n = n; L.slice = slice_n;
+    if (sfda::launch_chunk(L, st) != hipSuccess) return SFDA_ERR_HIP;
+    // incoming states and S_T
+    if (sfda::launch_fold(P, Bs, Sin, S0, S_T, BH, G, m, n, st) != hipSuccess) return SFDA_ERR_HIP;
+    // outputs from the exact incoming states
+    L.S0 = Sin; L.S_T = nullptr; L.o = o;
+    if (sfda::launch_chunk(L, st) != hipSuccess) return SFDA_ERR_HIP;
+    return SFDA_OK;
 }
 
 sfda_status_t sfda_step(const void* q, const void* k, const void* v, const void* alpha,

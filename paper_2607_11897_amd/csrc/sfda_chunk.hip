@@ -136,7 +136,9 @@ __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
                 for (int r = 0; r < 4; ++r) {
                     const int t = t0 + kb * 16 + 4 * g + r;
                     const bool ok = cb < ncb && j < n && t < T;
-                    const float2 x = Elem<TIN>::load2(gv, base_tn + static_cast<long>(min(t, T - 1)) * n + min(j, n - 1));
+                    float2 x = make_float2(0.f, 0.f);
+                    if (gv != nullptr)      // v == NULL reads as zeros (uniform branch)
+                        x = Elem<TIN>::load2(gv, base_tn + static_cast<long>(min(t, T - 1)) * n + min(j, n - 1));
                     vf[w][kb][r] = masked(ok, x);
                 }
         }
@@ -464,7 +466,7 @@ __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
                     }
                     mma<P>(acc, a, db[jb]);
                 }
-                if (j < n) {
+                if (j < n && go != nullptr) {     // o == NULL: no output
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
                         const int t = t0 + rb * 16 + 4 * g + r;

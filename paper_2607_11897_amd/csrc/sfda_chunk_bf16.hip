@@ -333,8 +333,9 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
 #pragma unroll
             for (int p = 0; p < NRB; ++p) {
                 const int t0 = ch * C + p * 16;
-                const rsrc_t rv = make_rsrc(args.v + 2 * (base_tn + static_cast<long>(t0) * n),
-                                            max(T - t0, 0) * n * 4);
+                // v == NULL reads as zeros (an empty range)
+                const rsrc_t rv = make_rsrc(args.v ? args.v + 2 * (base_tn + static_cast<long>(t0) * n) : args.v,
+                                            args.v ? max(T - t0, 0) * n * 4 : 0);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) vv[p][r] = ld32(rv, voff_v[r]);
             }
@@ -460,8 +461,9 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             auto store_o = [&](int q) {
                 const int rb = q / 4, r = q % 4;
                 const int tr = t0 + rb * 16;
-                const rsrc_t ro = make_rsrc(go + 2 * (base_tn + static_cast<long>(tr) * n),
-                                            max(T - tr, 0) * n * Out<TOUT>::BYTES);
+                // o == NULL drops the stores (an empty range)
+                const rsrc_t ro = make_rsrc(go ? go + 2 * (base_tn + static_cast<long>(tr) * n) : go,
+                                            go ? max(T - tr, 0) * n * Out<TOUT>::BYTES : 0);
                 Out<TOUT>::store(ro, voff_o[r], O[rb].re[r], -O[rb].im[r]);
             };
             constexpr int SPS = 4 * NRB / NK;      // stores per state-update stage

@@ -15,9 +15,9 @@ struct StepLaunch {
 };
 
 struct ChunkLaunch {
-    const void *q, *k, *v, *alpha, *theta, *beta;
+    const void *q, *k, *v, *alpha, *theta, *beta;   // v may be null (zero values)
     const float* S0;   // may be null (zero state)
-    void* o;
+    void* o;           // may be null (no output)
     float* S_T;        // may be null
     int B, H, T, m, n, C;
     int slice;         // value columns per workgroup (multiple of 8, <= 64)
@@ -27,5 +27,9 @@ struct ChunkLaunch {
 hipError_t launch_step(const StepLaunch& L, hipStream_t st);
 hipError_t launch_chunk(const ChunkLaunch& L, hipStream_t st);
 hipError_t launch_chunk_bf16(const ChunkLaunch& L, hipStream_t st);   // bf16 inputs
+// segment-parallel scan: identity fill and the fold of the segments' affine maps
+hipError_t launch_identity(float* P, long count, int m, hipStream_t st);
+hipError_t launch_fold(const float* P, const float* Bs, float* Sin, const float* S0, float* S_T,
+                       long heads, int G, int m, int n, hipStream_t st);
 
 }  // namespace sfda

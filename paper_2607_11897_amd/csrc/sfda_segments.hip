@@ -1,0 +1,131 @@
+// Segment-parallel scan helpers: a long sequence of a head is cut into G segments that
+// run as independent heads of the chunk kernel; the state entering each segment then
+// follows from the affine law of a segment (Thm 4.4: the state after a stretch of tokens
+// is P S_in + B, with P the product of the stretch's transitions A_t and B its write from
+// the zero state) composed along the segments (Lemma A.2):
+//   S_in[0] = S0,   S_in[g + 1] = P_g S_in[g] + B_g,   S_T = S_in[G].
+// P_g is the chunk kernel's final state for S0 = I and v = 0 (then every B_t = 0), B_g its
+// final state for S0 = 0.  This file holds the identity fill for the first and the fold.
+#include <stdint.h>
+
+#include "sfda_launch.h"
+
+namespace sfda {
+namespace seg {
+
+constexpr int NT = 256;
+constexpr int MP = 64;      // state rows (m <= 64)
+constexpr int CB = 16;      // value columns per workgroup in the fold
+
+// P[s] = I (m x m complex), s < count
+__global__ __launch_bounds__(NT) void identity_kernel(float* P, long count, int m)
+{
+    const long mm = static_cast<long>(m) * m;
+    const long total = count * mm;
+    for (long e = blockIdx.x * static_cast<long>(NT) + threadIdx.x; e < total;
+         e += static_cast<long>(gridDim.x) * NT) {
+        const long r = e % mm;
+        const int i = static_cast<int>(r / m), j = static_cast<int>(r % m);
+        reinterpret_cast<float2*>(P)[e] = make_float2(i == j ? 1.f : 0.f, 0.f);
+    }
+}
+
+// One workgroup per (head, block of CB value columns).  Column j of the state only mixes
+// with column j, so a block of columns runs the fold on its own, held in LDS.
+// P: [heads * G][m][m], Bs, Sin: [heads * G][m][n], S0, S_T: [heads][m][n] (complex
+// float32; S0 may be null = zero state, S_T may be null).
+__global__ __launch_bounds__(NT) void fold_kernel(const float* __restrict__ P,
+                                                  const float* __restrict__ Bs,
+                                                  float* __restrict__ Sin,
+                                                  const float* __restrict__ S0,
+                                                  float* __restrict__ S_T,
+                                                  int G, int m, int n, int ncb)
+{
+    __shared__ float2 S[MP][CB];
+    const long h = blockIdx.x / ncb;
+    const int j0 = static_cast<int>(blockIdx.x - h * ncb) * CB;
+    const int tid = threadIdx.x;
+    const int i = tid >> 2;             // state row
+    const int jq = (tid & 3) * 4;       // first of this thread's 4 columns in the block
+    const long mn = static_cast<long>(m) * n;
+    const float2* P2 = reinterpret_cast<const float2*>(P);
+    const float2* B2 = reinterpret_cast<const float2*>(Bs);
+    float2* Sin2 = reinterpret_cast<float2*>(Sin);
+
+    auto col_ok = [&](int c) { return j0 + jq + c < n; };
+    float2 s[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        s[c] = make_float2(0.f, 0.f);
+        if (S0 != nullptr && i < m && col_ok(c))
+            s[c] = reinterpret_cast<const float2*>(S0)[h * mn + static_cast<long>(i) * n + j0 + jq + c];
+        S[i][jq + c] = s[c];
+    }
+    __syncthreads();
+    for (int gi = 0; gi < G; ++gi) {
+        const long seg = h * G + gi;
+        // the state entering segment gi
+        if (i < m) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                if (col_ok(c)) Sin2[seg * mn + static_cast<long>(i) * n + j0 + jq + c] = s[c];
+        }
+        // row i of P_gi S + B_gi
+        float2 acc[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[c] = make_float2(0.f, 0.f);
+        if (i < m) {
+            const float2* prow = P2 + seg * static_cast<long>(m) * m + static_cast<long>(i) * m;
+            for (int l = 0; l < m; ++l) {
+                const float2 p = prow[l];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const float2 x = S[l][jq + c];
+                    acc[c].x = __builtin_fmaf(p.x, x.x, __builtin_fmaf(-p.y, x.y, acc[c].x));
+                    acc[c].y = __builtin_fmaf(p.x, x.y, __builtin_fmaf(p.y, x.x, acc[c].y));
+                }
+            }
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                if (!col_ok(c)) continue;
+                const float2 b = B2[seg * mn + static_cast<long>(i) * n + j0 + jq + c];
+                acc[c].x += b.x;
+                acc[c].y += b.y;
+            }
+        }
+        __syncthreads();                // every row of S read
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            s[c] = acc[c];
+            S[i][jq + c] = acc[c];
+        }
+        __syncthreads();
+    }
+    if (S_T != nullptr && i < m) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            if (col_ok(c)) reinterpret_cast<float2*>(S_T)[h * mn + static_cast<long>(i) * n + j0 + jq + c] = s[c];
+    }
+}
+
+}  // namespace seg
+
+hipError_t launch_identity(float* P, long count, int m, hipStream_t st)
+{
+    const long total = count * m * m;
+    const long blocks = (total + seg::NT - 1) / seg::NT;
+    const unsigned grid = static_cast<unsigned>(blocks < 4096 ? (blocks > 0 ? blocks : 1) : 4096);
+    hipLaunchKernelGGL(seg::identity_kernel, dim3(grid), dim3(seg::NT), 0, st, P, count, m);
+    return hipGetLastError();
+}
+
+hipError_t launch_fold(const float* P, const float* Bs, float* Sin, const float* S0, float* S_T,
+                       long heads, int G, int m, int n, hipStream_t st)
+{
+    const int ncb = (n + seg::CB - 1) / seg::CB;
+    const dim3 grid(static_cast<unsigned>(heads * ncb));
+    hipLaunchKernelGGL(seg::fold_kernel, grid, dim3(seg::NT), 0, st, P, Bs, Sin, S0, S_T, G, m, n, ncb);
+    return hipGetLastError();
+}
+
+}  // namespace sfda

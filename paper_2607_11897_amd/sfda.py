@@ -17,7 +17,8 @@ LIB_PATH = os.path.join(HERE, "libsfda.so")
 SFDA_F32, SFDA_BF16 = 0, 1
 STATUS = {0: "SFDA_OK", 1: "SFDA_ERR_NULL", 2: "SFDA_ERR_SHAPE", 3: "SFDA_ERR_CHUNK",
           4: "SFDA_ERR_DTYPE", 5: "SFDA_ERR_ALIGN", 6: "SFDA_ERR_ALIAS", 7: "SFDA_ERR_HIP"}
-EXPORTS = ("sfda_chunk_fwd", "sfda_chunk_fwd_sliced", "sfda_step", "sfda_status_string",
+EXPORTS = ("sfda_chunk_fwd", "sfda_chunk_fwd_sliced", "sfda_chunk_fwd_segmented",
+           "sfda_chunk_fwd_segmented_workspace_bytes", "sfda_step", "sfda_status_string",
            "sfda_abi_version")
 
 _lib = None
@@ -44,6 +45,10 @@ def load_library(path: str = LIB_PATH):
     lib.sfda_chunk_fwd.restype = i
     lib.sfda_chunk_fwd_sliced.argtypes = [vp] * 9 + [i] * 7 + [i, i, vp]
     lib.sfda_chunk_fwd_sliced.restype = i
+    lib.sfda_chunk_fwd_segmented.argtypes = [vp] * 9 + [i] * 7 + [i, i, vp, ctypes.c_size_t, vp]
+    lib.sfda_chunk_fwd_segmented.restype = i
+    lib.sfda_chunk_fwd_segmented_workspace_bytes.argtypes = [i] * 5
+    lib.sfda_chunk_fwd_segmented_workspace_bytes.restype = ctypes.c_size_t
     lib.sfda_step.argtypes = [vp] * 8 + [i] * 4 + [i, i, vp]
     lib.sfda_step.restype = i
     lib.sfda_status_string.argtypes = [i]
@@ -79,10 +84,13 @@ def _stream(stream):
 
 def chunk_fwd(q, k, v, alpha, theta, beta, S0=None, C: int = 64, *, o=None, S_T=None,
               out_dtype=None, want_state: bool = True, slice: Optional[int] = None,
-              stream=None) -> Tuple:
+              segments: Optional[int] = None, workspace=None, stream=None) -> Tuple:
     """SFDA chunkwise forward.  q, k: [B,H,T,m,2]; v: [B,H,T,n,2]; alpha, theta: [B,H,T,m];
     beta: [B,H,T] (all float32 or all bfloat16); S0: [B,H,m,n,2] float32 or None.
-    Returns (o [B,H,T,n,2] in out_dtype, S_T [B,H,m,n,2] float32 or None)."""
+    Returns (o [B,H,T,n,2] in out_dtype, S_T [B,H,m,n,2] float32 or None).
+    slice: value columns per workgroup (sfda_chunk_fwd_sliced); segments: G parallel
+    segments per head (sfda_chunk_fwd_segmented; `workspace` a uint8 device tensor of at
+    least segmented_workspace_bytes(...) bytes, allocated here when not given)."""
     import torch
     lib = load_library()
     B, H, T, m, _ = q.shape
@@ -100,6 +108,15 @@ def chunk_fwd(q, k, v, alpha, theta, beta, S0=None, C: int = 64, *, o=None, S_T=
         raise TypeError("S0 must be float32")
     args = [_ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(theta), _ptr(beta), _ptr(S0),
             _ptr(o), _ptr(S_T), B, H, T, m, n, C]
+    if segments is not None:
+        nws = lib.sfda_chunk_fwd_segmented_workspace_bytes(B, H, m, n, segments)
+        if workspace is None:
+            workspace = torch.empty(max(nws, 1), dtype=torch.uint8, device=q.device)
+        st = lib.sfda_chunk_fwd_segmented(*args, segments, in_code, _dtype_code(o), _ptr(workspace),
+                                          workspace.numel(), _stream(stream))
+        if st != 0:
+            raise SfdaError(st, "sfda_chunk_fwd_segmented")
+        return o, S_T
     if slice is None:
         st = lib.sfda_chunk_fwd(*args, in_code, _dtype_code(o), _stream(stream))
     else:
@@ -107,6 +124,10 @@ def chunk_fwd(q, k, v, alpha, theta, beta, S0=None, C: int = 64, *, o=None, S_T=
     if st != 0:
         raise SfdaError(st, "sfda_chunk_fwd")
     return o, S_T
+
+
+def segmented_workspace_bytes(B: int, H: int, m: int, n: int, G: int) -> int:
+    return int(load_library().sfda_chunk_fwd_segmented_workspace_bytes(B, H, m, n, G))
 
 
 def step(q, k, v, alpha, theta, beta, S, *, o=None, out_dtype=None, stream=None):

@@ -74,6 +74,29 @@ def test_chunk_argument_errors(lib):
     assert chunk(lib, B=0, q=None, o=None) == 0
 
 
+def seg(lib, T=64, G=2, C=16, ws=A * 20, nws=1 << 40, q=P[0], B=1, H=1, m=8, n=8, din=0):
+    return lib.sfda_chunk_fwd_segmented(q, *P[1:], B, H, T, m, n, C, G, din, 0, ws, nws, None)
+
+
+def test_segmented_workspace_size(lib):
+    # per segment: P_g (m x m) + B_g and the incoming state (m x n), complex float32
+    assert lib.sfda_chunk_fwd_segmented_workspace_bytes(2, 3, 64, 48, 4) == 24 * (64 * 64 + 2 * 64 * 48) * 8
+    assert lib.sfda_chunk_fwd_segmented_workspace_bytes(1, 1, 65, 8, 1) == 0
+    assert lib.sfda_chunk_fwd_segmented_workspace_bytes(1, 1, 8, 8, 0) == 0
+
+
+def test_segmented_argument_errors(lib):
+    assert seg(lib, G=0) == 2
+    assert seg(lib, T=48, G=2, C=16) == 2             # T not a multiple of G * C
+    assert seg(lib, ws=None) == 1
+    assert seg(lib, ws=A * 20 + 8) == 5
+    assert seg(lib, nws=100) == 2                     # workspace too small
+    assert seg(lib, ws=P[2]) == 6                     # workspace on top of v
+    assert seg(lib, q=None) == 1
+    assert seg(lib, C=8) == 3 and seg(lib, din=3) == 4
+    assert seg(lib, B=0, q=None, ws=None) == 0        # nothing to do
+
+
 def test_step_argument_errors(lib):
     assert step(lib, S=None) == 1
     assert step(lib, m=0) == 2 and step(lib, m=65) == 2 and step(lib, n=0) == 2
