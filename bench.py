@@ -13,8 +13,9 @@ Also reported on the same JSON line:
   cpu_baseline  the CPU oracle (complex128 recurrence) on a bounded sample of the workload
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--only chunk|decode]
-       [--no-cpu-baseline] [--mode copy|rmw]   (copy: a plain device copy, for counter
-       scaling; rmw: an in-place pass over 1 GiB, the decode step's access pattern)
+       [--no-cpu-baseline] [--mode copy|rmw|long]   (copy: a plain device copy, for counter
+       scaling; rmw: an in-place pass over 1 GiB, the decode step's access pattern; long:
+       the long-context workload, one workgroup per head against the segment-parallel scan)
 """
 from __future__ import annotations
 
@@ -200,6 +201,44 @@ def cpu_baseline(x, budget_s=12.0):
                       f"(complex128 recurrence), {el:.1f} s"}
 
 
+def long_context(args):
+    """The long-context float32 workload (B=1, H=16, T=65536, m=n=64, C=64): one
+    sfda_chunk_fwd launch (one workgroup per head) against sfda_chunk_fwd_segmented with
+    G segments per head (the scan split G ways, joined by the affine segment law)."""
+    import numpy as np
+    import torch
+    from paper_2607_11897_amd import inputs as I
+    from paper_2607_11897_amd import sfda
+    w = I.WORKLOADS["long_f32_h16_t64k"]
+    print(f"# generating inputs for {w.name}", file=sys.stderr, flush=True)
+    x = I.make_chunk_inputs(w)
+    st = x.storage()
+    d = {k: torch.from_numpy(np.ascontiguousarray(st[k], dtype=np.float32)).cuda()
+         for k in ("q", "k", "v", "alpha", "theta", "beta")}
+    S0 = torch.from_numpy(np.ascontiguousarray(st["S0"], dtype=np.float32)).cuda()
+    B, H, T, m, n = x.shape
+    o = torch.empty((B, H, T, n, 2), dtype=torch.float32, device="cuda")
+    S_T = torch.empty((B, H, m, n, 2), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    out = {"mode": "long", "workload": w.name, "B": B, "H": H, "T": T, "m": m, "n": n, "C": w.C,
+           "dtype": "f32", "ms": {}, "tokens_per_s": {}}
+    for G in (None, 4, 8, 16, 32):
+        ws = None if G is None else torch.empty(sfda.segmented_workspace_bytes(B, H, m, n, G),
+                                                dtype=torch.uint8, device="cuda")
+
+        def run():
+            sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], S0, C=w.C,
+                           o=o, S_T=S_T, segments=G, workspace=ws, stream=stream)
+
+        key = "plain" if G is None else f"segments_{G}"
+        print(f"# timing {key}", file=sys.stderr, flush=True)
+        ms = timed(run, 3 if G is None else 10, 1, stream)
+        out["ms"][key] = round(ms, 3)
+        out["tokens_per_s"][key] = round(B * T / (ms / 1e3), 1)
+    out["kernel_hash"] = kernel_hash()
+    print(json.dumps(out), flush=True)
+
+
 def copy_calibration(args):
     """A plain device-to-device copy of 1 GiB, repeated, for scaling HBM counters."""
     import torch
@@ -229,7 +268,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--only", choices=["chunk", "decode"], default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=["bench", "copy", "rmw"], default="bench")
+    ap.add_argument("--mode", choices=["bench", "copy", "rmw", "long"], default="bench")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported. The (batch, head) "
@@ -248,6 +287,9 @@ def main():
         return
     if args.mode == "rmw":
         rmw_calibration(args)
+        return
+    if args.mode == "long":
+        long_context(args)
         return
     stream = torch.cuda.current_stream()
     out = {}
