@@ -15,7 +15,8 @@ Also reported on the same JSON line:
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--only chunk|decode]
        [--no-cpu-baseline] [--mode copy|rmw|long]   (copy: a plain device copy, for counter
        scaling; rmw: an in-place pass over 1 GiB, the decode step's access pattern; long:
-       the long-context workload, one workgroup per head against the segment-parallel scan)
+       the long-context workload, one workgroup per head against the segment-parallel scan;
+       gated: the benchmarked shape through sfda_chunk_fwd_gated)
 """
 from __future__ import annotations
 
@@ -239,6 +240,37 @@ def long_context(args):
     print(json.dumps(out), flush=True)
 
 
+def gated(args):
+    """The benchmarked shape (bf16, B=8, H=16, T=4096, m=n=64, C=64) on pre-activations:
+    sfda_chunk_fwd_gated, alpha, theta, beta and the key normalisation formed inside the
+    kernel (compare with the default bench line, sfda_chunk_fwd on the same sizes)."""
+    import torch
+    from paper_2607_11897_amd import inputs as I
+    from paper_2607_11897_amd import sfda
+    B, H, T, m, n, C = 8, 16, 4096, 64, 64, 64
+    print("# generating gated inputs", file=sys.stderr, flush=True)
+    g = I.make_gated_inputs(B, H, T, m, n, "bf16", seed=2002)
+    st = g.storage()
+    import numpy as np
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
+    d = {k: up(st[k]) for k in ("q", "k_raw", "v", "a", "b", "c")}
+    S0 = torch.from_numpy(np.ascontiguousarray(st["S0"], dtype=np.float32)).cuda()
+    o = torch.empty((B, H, T, n, 2), dtype=torch.bfloat16, device="cuda")
+    S_T = torch.empty((B, H, m, n, 2), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    gp = dict(alpha_min=0.9, alpha_max=1.0, theta_max=0.5, eps=1e-6)
+
+    def run_gated():
+        sfda.chunk_fwd_gated(d["q"], d["k_raw"], d["v"], d["a"], d["b"], d["c"], S0, C=C, o=o,
+                             S_T=S_T, stream=stream, **gp)
+
+    ms_g = timed(run_gated, args.steps, args.warmup, stream)
+    out = {"mode": "gated", "workload": "gated_bf16_b8h16_t4k", "B": B, "H": H, "T": T, "m": m,
+           "n": n, "C": C, "gates": gp, "ms_gated": round(ms_g, 4),
+           "tokens_per_s_gated": round(B * T / (ms_g / 1e3), 1), "kernel_hash": kernel_hash()}
+    print(json.dumps(out), flush=True)
+
+
 def copy_calibration(args):
     """A plain device-to-device copy of 1 GiB, repeated, for scaling HBM counters."""
     import torch
@@ -268,7 +300,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--only", choices=["chunk", "decode"], default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=["bench", "copy", "rmw", "long"], default="bench")
+    ap.add_argument("--mode", choices=["bench", "copy", "rmw", "long", "gated"], default="bench")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported. The (batch, head) "
@@ -290,6 +322,9 @@ def main():
         return
     if args.mode == "long":
         long_context(args)
+        return
+    if args.mode == "gated":
+        gated(args)
         return
     stream = torch.cuda.current_stream()
     out = {}

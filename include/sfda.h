@@ -109,6 +109,28 @@ sfda_status_t sfda_chunk_fwd_sliced(const void* q, const void* k, const void* v,
                                     sfda_stream_t stream);
 
 /*
+ * sfda_chunk_fwd_gated -- sfda_chunk_fwd on pre-activations: the kernels map them to the
+ * recurrence's parameters as they load them (the stable parameterization of Sec. 3,
+ * equations param-alpha, param-theta, param-beta and param-key), with no separate pass:
+ *   alpha_t = alpha_min + (alpha_max - alpha_min) * sigmoid(a_t)    a:     [B,H,T,m] real
+ *   theta_t = theta_max * tanh(b_t)                                  b:     [B,H,T,m] real
+ *   beta_t  = sigmoid(c_t)                                           c:     [B,H,T]   real
+ *   k_t     = k_raw_t / (||k_raw_t||_2 + eps)   (norm over the m complex channels)
+ * q, v, S0, o, S_T, sizes, dtypes, layouts, errors and results as sfda_chunk_fwd (a, b, c,
+ * k_raw take the places of alpha, theta, beta, k).  Requires 0 < alpha_min <= alpha_max
+ * <= 1 and finite theta_max, eps >= 0 (SFDA_ERR_SHAPE otherwise); the decay-range
+ * precondition of sfda_chunk_fwd applies to alpha (alpha_min^C above about 1e-30 always
+ * satisfies it).  With eps == 0 an all-zero raw key gives k = 0.
+ */
+sfda_status_t sfda_chunk_fwd_gated(const void* q, const void* k_raw, const void* v,
+                                   const void* a, const void* b, const void* c,
+                                   const float* S0, void* o, float* S_T,
+                                   int B, int H, int T, int m, int n, int C,
+                                   float alpha_min, float alpha_max, float theta_max, float eps,
+                                   sfda_dtype_t in_dtype, sfda_dtype_t out_dtype,
+                                   sfda_stream_t stream);
+
+/*
  * sfda_chunk_fwd_segmented -- sfda_chunk_fwd with each head's sequence cut into G
  * segments of T / G tokens that are scanned in parallel (for few heads over long
  * sequences, where one workgroup per head leaves most of the GPU idle).  It uses the

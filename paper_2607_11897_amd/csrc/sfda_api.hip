@@ -51,7 +51,8 @@ static sfda_status_t chunk_fwd_impl(const void* q, const void* k, const void* v,
                                     const float* S0, void* o, float* S_T, int B, int H, int T,
                                     int m, int n, int C, sfda_dtype_t in_dtype,
                                     sfda_dtype_t out_dtype, sfda_stream_t stream, int slice,
-                                    void* = nullptr, size_t = 0, bool check_only = false)
+                                    void* = nullptr, size_t = 0, bool check_only = false,
+                                    const sfda::GateParams* gates = nullptr)
 {
     if (!dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return SFDA_ERR_DTYPE;
     if (B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1) return SFDA_ERR_SHAPE;
@@ -100,6 +101,11 @@ static sfda_status_t chunk_fwd_impl(const void* q, const void* k, const void* v,
     L.B = B; L.H = H; L.T = T; L.m = m; L.n = n; L.C = C; L.slice = slice;
     L.in_bf16 = in_dtype == SFDA_BF16;
     L.out_bf16 = out_dtype == SFDA_BF16;
+    if (gates) {
+        L.gated = gates->gated;
+        L.alpha_min = gates->alpha_min; L.alpha_max = gates->alpha_max;
+        L.theta_max = gates->theta_max; L.eps = gates->eps;
+    }
     const hipError_t e = sfda::launch_chunk(L, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? SFDA_OK : SFDA_ERR_HIP;
 }
@@ -122,6 +128,23 @@ sfda_status_t sfda_chunk_fwd_sliced(const void* q, const void* k, const void* v,
 {
     return chunk_fwd_impl(q, k, v, alpha, theta, beta, S0, o, S_T, B, H, T, m, n, C, in_dtype,
                           out_dtype, stream, slice);
+}
+
+sfda_status_t sfda_chunk_fwd_gated(const void* q, const void* k_raw, const void* v,
+                                   const void* a, const void* b, const void* c,
+                                   const float* S0, void* o, float* S_T, int B, int H, int T,
+                                   int m, int n, int C, float alpha_min, float alpha_max,
+                                   float theta_max, float eps, sfda_dtype_t in_dtype,
+                                   sfda_dtype_t out_dtype, sfda_stream_t stream)
+{
+    // 0 < alpha_min <= alpha_max <= 1 (a zero decay has no inverse in the chunk factors),
+    // theta_max and eps finite and >= 0 (NaN fails every comparison)
+    if (!(alpha_min > 0.f && alpha_min <= alpha_max && alpha_max <= 1.f)) return SFDA_ERR_SHAPE;
+    if (!(theta_max >= 0.f && theta_max < 3.4e38f && eps >= 0.f && eps < 3.4e38f)) return SFDA_ERR_SHAPE;
+    const int slice = n <= 64 ? ((n + 7) / 8) * 8 : 64;
+    sfda::GateParams gp{true, alpha_min, alpha_max, theta_max, eps};
+    return chunk_fwd_impl(q, k_raw, v, a, b, c, S0, o, S_T, B, H, T, m, n, C, in_dtype, out_dtype,
+                          stream, slice, nullptr, 0, false, &gp);
 }
 
 size_t sfda_chunk_fwd_segmented_workspace_bytes(int B, int H, int m, int n, int G)

@@ -30,6 +30,8 @@
 // chunk), so K / G grows like exp(-sum log alpha); the caller keeps the in-chunk decay
 // product above ~1e-30.  Accumulation and the state are fp32; with PREC_BF16 the matrix
 // products take bf16 operands (the solve always runs in fp32).
+#include <type_traits>
+
 #include "sfda_device.h"
 #include "sfda_launch.h"
 
@@ -45,7 +47,12 @@ struct ChunkArgs {
     void* o;
     float* S_T;
     int T, m, n, n_slices, slice;
+    // GATED: alpha = amin + aspan sigmoid(a), theta = tmax tanh(b), beta = sigmoid(c),
+    // k = k~ / (||k~|| + eps) from the pre-activations passed in alpha, theta, beta, k
+    float amin, aspan, tmax, eps;
 };
+
+__device__ __forceinline__ float sigmoid_acc(float x) { return 1.f / (1.f + expf(-x)); }
 
 template <int C>
 struct ChunkSmem {
@@ -60,7 +67,7 @@ struct ChunkSmem {
     float segp[4][MP];
 };
 
-template <int P, typename TIN, typename TOUT, int C>
+template <int P, typename TIN, typename TOUT, int C, bool GATED>
 __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
 {
     constexpr int NRB = C / 16;          // 16-token blocks per chunk
@@ -153,8 +160,12 @@ __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
                 const bool ok = t < T && i < m;
                 const long e = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
                 const float a_ld = pin(Elem<TIN>::load(ga, e));
-                const float a = ok ? a_ld : 1.f;
-                const float th = masked(ok, Elem<TIN>::load(gth, e));
+                float th = masked(ok, Elem<TIN>::load(gth, e));
+                float a = ok ? a_ld : 1.f;
+                if constexpr (GATED) {      // padding stays the identity token (alpha = 1, theta = 0)
+                    a = ok ? args.amin + args.aspan * sigmoid_acc(a_ld) : 1.f;
+                    th = ok ? args.tmax * tanhf(th) : 0.f;
+                }
                 sa += __logf(a);
                 sp += th;
                 la[u] = sa;
@@ -164,7 +175,8 @@ __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
             sm.segp[seg][i] = sp;
             {
                 const int tb = t0 + (tid & (C - 1));
-                const float bv = Elem<TIN>::load(gb, bh * static_cast<long>(T) + min(tb, T - 1));
+                float bv = Elem<TIN>::load(gb, bh * static_cast<long>(T) + min(tb, T - 1));
+                if constexpr (GATED) bv = sigmoid_acc(bv);
                 if (tid < C) sm.beta[tid] = masked(tb < T, bv);
             }
             __syncthreads();
@@ -190,6 +202,16 @@ __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
                 float2 qq = Elem<TIN>::load2(gq, e2), kk = Elem<TIN>::load2(gk, e2);
                 qq = masked(ok, qq);
                 kk = masked(ok, kk);
+                if constexpr (GATED) {
+                    // 1 / (||k~_t|| + eps): the wave holds channel i = lane of token t
+                    float s2 = kk.x * kk.x + kk.y * kk.y;
+#pragma unroll
+                    for (int sh = 1; sh < 64; sh <<= 1) s2 += __shfl_xor(s2, sh);
+                    const float den = sqrtf(s2) + args.eps;
+                    const float inv = den > 0.f ? 1.f / den : 0.f;
+                    kk.x *= inv;
+                    kk.y *= inv;
+                }
                 sm.qg[tl * LDX + i] = make_float2(qq.x * gr + qq.y * gi, qq.x * gi - qq.y * gr);
                 sm.kg[tl * LDX + i] = make_float2(kk.x * gr + kk.y * gi, kk.x * gi - kk.y * gr);
                 sm.ki[tl * LDX + i] = make_float2(kk.x * hr - kk.y * hi, kk.x * hi + kk.y * hr);
@@ -530,14 +552,19 @@ static hipError_t launch_chunk_t(const ChunkLaunch& L, hipStream_t st)
     a.S0 = L.S0; a.o = L.o; a.S_T = L.S_T;
     a.T = L.T; a.m = L.m; a.n = L.n; a.slice = L.slice;
     a.n_slices = (L.n + L.slice - 1) / L.slice;
+    a.amin = L.alpha_min; a.aspan = L.alpha_max - L.alpha_min; a.tmax = L.theta_max; a.eps = L.eps;
     const dim3 grid(static_cast<unsigned>(static_cast<long>(L.B) * L.H * a.n_slices));
-    switch (L.C) {
-        case 16: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 16>), grid, dim3(NTHR), 0, st, a); break;
-        case 32: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 32>), grid, dim3(NTHR), 0, st, a); break;
-        case 64: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 64>), grid, dim3(NTHR), 0, st, a); break;
-        default: return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
+    auto go = [&](auto gated) {
+        constexpr bool G = decltype(gated)::value;
+        switch (L.C) {
+            case 16: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 16, G>), grid, dim3(NTHR), 0, st, a); break;
+            case 32: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 32, G>), grid, dim3(NTHR), 0, st, a); break;
+            case 64: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 64, G>), grid, dim3(NTHR), 0, st, a); break;
+            default: return hipErrorInvalidValue;
+        }
+        return hipGetLastError();
+    };
+    return L.gated ? go(std::true_type{}) : go(std::false_type{});
 }
 
 hipError_t launch_chunk(const ChunkLaunch& L, hipStream_t st)

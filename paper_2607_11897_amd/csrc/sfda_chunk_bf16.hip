@@ -230,7 +230,19 @@ struct Args {
     void* o;
     float* S_T;
     int T, m, n, n_slices, slice;
+    // GATED: alpha = amin + aspan sigmoid(a), theta = tmax tanh(b), beta = sigmoid(c),
+    // k = k~ / (||k~|| + eps) from the pre-activations passed in alpha, theta, beta, k
+    float amin, aspan, tmax, eps;
 };
+
+// logistic function and tanh from the hardware exp2 and reciprocal (relative error a few
+// ulp; saturate to 0 / 1 and -1 / 1 without NaN for large arguments)
+__device__ __forceinline__ float sigmoid_f(float x) {
+    return __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-1.4426950408889634f * x));
+}
+__device__ __forceinline__ float tanh_f(float x) {
+    return 1.f - 2.f * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(2.8853900817779268f * x));
+}
 
 // Gram units: 16 x 16 blocks (rb, jb) of a C x C Gram matrix, split over the four consumer
 // waves.  a_units: all blocks jb <= rb (the A Gram); l_units: the blocks jb < rb (the
@@ -267,7 +279,7 @@ __device__ __forceinline__ int l_units(int nrb, int wv, int (&units)[2][2])
     return 0;
 }
 
-template <typename TOUT, int C>
+template <typename TOUT, int C, bool GATED>
 __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
 {
     constexpr int NRB = C / 16;
@@ -324,6 +336,10 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             voff_o[r] = col_ok ? e * static_cast<u32>(Out<TOUT>::BYTES) : OOB;
         }
 
+        // v == NULL reads as zeros and o == NULL drops the stores: their ranges are empty
+        // (an access outside a buffer range touches no memory)
+        const int v_row_bytes = args.v ? n * 4 : 0;
+        const int o_row_bytes = args.o ? n * Out<TOUT>::BYTES : 0;
         CAcc Sa[4];          // S rows kb*16 + 4g + r, column jw
         BPair sb[4];         // S at the start of the chunk, as right operands
         BPair db[NRB];       // Delta blocks as right operands
@@ -333,9 +349,8 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
 #pragma unroll
             for (int p = 0; p < NRB; ++p) {
                 const int t0 = ch * C + p * 16;
-                // v == NULL reads as zeros (an empty range)
-                const rsrc_t rv = make_rsrc(args.v ? args.v + 2 * (base_tn + static_cast<long>(t0) * n) : args.v,
-                                            args.v ? max(T - t0, 0) * n * 4 : 0);
+                const rsrc_t rv = make_rsrc(args.v + 2 * (base_tn + static_cast<long>(t0) * n),
+                                            max(T - t0, 0) * v_row_bytes);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) vv[p][r] = ld32(rv, voff_v[r]);
             }
@@ -461,9 +476,8 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             auto store_o = [&](int q) {
                 const int rb = q / 4, r = q % 4;
                 const int tr = t0 + rb * 16;
-                // o == NULL drops the stores (an empty range)
-                const rsrc_t ro = make_rsrc(go ? go + 2 * (base_tn + static_cast<long>(tr) * n) : go,
-                                            go ? max(T - tr, 0) * n * Out<TOUT>::BYTES : 0);
+                const rsrc_t ro = make_rsrc(go + 2 * (base_tn + static_cast<long>(tr) * n),
+                                            max(T - tr, 0) * o_row_bytes);
                 Out<TOUT>::store(ro, voff_o[r], O[rb].re[r], -O[rb].im[r]);
             };
             constexpr int SPS = 4 * NRB / NK;      // stores per state-update stage
@@ -665,7 +679,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         constexpr float INV_2PI = 0.15915494309189535f;
         float lm[TPL][4], lph[TPL][4];    // inclusive over the lane's tokens
         float qm[4], qph[4];              // exclusive over the wave's earlier segments
-        auto pretot_body = [&](auto padded) {
+        auto pretot_body = [&](int ch, auto padded) {
             const bool s0 = tsg == 0, s01 = tsg < 2;
             float tm[4], tp[4];
 #pragma unroll
@@ -676,8 +690,17 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     const u32 wa = k < 2 ? pa[u].x : pa[u].y;
                     const u32 wt = k < 2 ? pt[u].x : pt[u].y;
                     float a = (k & 1) ? bf_hi(wa) : bf_lo(wa);
-                    const float th = (k & 1) ? bf_hi(wt) : bf_lo(wt);
-                    if constexpr (decltype(padded)::value) a = a == 0.f ? 1.f : a;
+                    float th = (k & 1) ? bf_hi(wt) : bf_lo(wt);
+                    if constexpr (GATED) {
+                        // a, th hold the pre-activations; padding (past T or m) stays the
+                        // identity token: alpha = 1 there, and tanh(0) = 0
+                        a = args.amin + args.aspan * sigmoid_f(a);
+                        th = args.tmax * tanh_f(th);
+                        if constexpr (decltype(padded)::value)
+                            a = (ch * C + tl0 + u < T && pc0 + k < m) ? a : 1.f;
+                    } else {
+                        if constexpr (decltype(padded)::value) a = a == 0.f ? 1.f : a;
+                    }
                     rm *= a;
                     rp = __builtin_fmaf(th, INV_2PI, rp);
                     lm[u][k] = rm;
@@ -706,8 +729,8 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         // first two levels for chunk ch (inputs in pa, pt), wave totals to LDS.  Only a chunk
         // with padding (ragged tail, m < 64) needs the alpha = 0 -> 1 substitution.
         auto pretot = [&](int ch) {
-            if ((ch + 1) * C <= T && m == MP) pretot_body(std::false_type{});
-            else pretot_body(std::true_type{});
+            if ((ch + 1) * C <= T && m == MP) pretot_body(ch, std::false_type{});
+            else pretot_body(ch, std::true_type{});
         };
 
         // phase 1: g and the operands conj(Q)G, conj(K)G, K/G of chunk ch into set ch & 1
@@ -723,6 +746,28 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 em[0] *= t01.x; eph[0] += t01.y; em[1] *= t01.z; eph[1] += t01.w;
                 em[2] *= t23.x; eph[2] += t23.y; em[3] *= t23.z; eph[3] += t23.w;
             }
+            // GATED: 1 / (||k~_t|| + eps) of the lane's tokens; a token row lives on the 16
+            // lanes tsg + 4 cg (four per 16-lane row): rotate by 4 and 8 inside the row, then
+            // exchange across rows
+            float kinv[TPL];
+#pragma unroll
+            for (int u = 0; u < TPL; ++u) {
+                kinv[u] = 1.f;
+                if constexpr (GATED) {
+                    float s2 = 0.f;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        const float kr = bf_lo(pk[u][k]), ki = bf_hi(pk[u][k]);
+                        s2 = __builtin_fmaf(kr, kr, __builtin_fmaf(ki, ki, s2));
+                    }
+                    s2 += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s2), 0x124, 0xF, 0xF, false));
+                    s2 += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s2), 0x128, 0xF, 0xF, false));
+                    s2 += __shfl_xor(s2, 16);
+                    s2 += __shfl_xor(s2, 32);
+                    const float den = __builtin_sqrtf(s2) + args.eps;
+                    kinv[u] = den > 0.f ? __builtin_amdgcn_rcpf(den) : 0.f;
+                }
+            }
 #pragma unroll
             for (int u = 0; u < TPL; ++u) {
                 const int tl = tl0 + u;
@@ -733,6 +778,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     const float A = em[k] * lm[u][k];                // |g|
                     const float Ph = eph[k] + lph[u][k];             // arg g / 2 pi
                     const float ei = __builtin_amdgcn_rcpf(A);
+                    const float Ak = A * kinv[u], eik = ei * kinv[u];
                     const float sn = __builtin_amdgcn_sinf(Ph), cs = __builtin_amdgcn_cosf(Ph);
                     const float gr = A * cs, gi = A * sn;
                     const u32 qw = pq[u][k], kw = pk[u][k];
@@ -740,8 +786,8 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     // conj(k) e^{i phi}; conj(k) g = |g| of it, k / g = its conjugate / |g|
                     const float kur = __builtin_fmaf(kr, cs, ki * sn), kui = __builtin_fmaf(kr, sn, -ki * cs);
                     wq[k] = pack_bf16(__builtin_fmaf(qr, gr, qi * gi), __builtin_fmaf(qr, gi, -qi * gr));
-                    wk[k] = pack_bf16(A * kur, A * kui);
-                    wi[k] = pack_bf16(ei * kur, -ei * kui);
+                    wk[k] = pack_bf16(Ak * kur, Ak * kui);
+                    wi[k] = pack_bf16(eik * kur, -eik * kui);
                     gl[k] = make_float2(gr, gi);
                 }
                 *reinterpret_cast<u32x4*>(S + OFF_QG + rm_off(tl, pc0)) = wq;
@@ -753,7 +799,11 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     gp[1] = make_float4(gl[2].x, gl[2].y, gl[3].x, gl[3].y);
                 }
             }
-            if (pw == 0 && lane < C) st.beta[lane] = bf16_bits_to_f32(static_cast<uint16_t>(pbeta));
+            if (pw == 0 && lane < C) {
+                float bt = bf16_bits_to_f32(static_cast<uint16_t>(pbeta));
+                if constexpr (GATED) bt = ch * C + lane < T ? sigmoid_f(bt) : 0.f;
+                st.beta[lane] = bt;
+            }
         };
 
         // phase 2: diagonal blocks of L' and their inverses, chunk ch
@@ -832,11 +882,21 @@ static hipError_t launch_t(const ChunkLaunch& L, hipStream_t st)
     a.S0 = L.S0; a.o = L.o; a.S_T = L.S_T;
     a.T = L.T; a.m = L.m; a.n = L.n; a.slice = L.slice;
     a.n_slices = (L.n + L.slice - 1) / L.slice;
+    a.amin = L.alpha_min; a.aspan = L.alpha_max - L.alpha_min; a.tmax = L.theta_max; a.eps = L.eps;
     const dim3 grid(static_cast<unsigned>(static_cast<long>(L.B) * L.H * a.n_slices));
+    if (L.gated) {
+        switch (L.C) {
+            case 16: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 16, true>), grid, dim3(NTH), 0, st, a); break;
+            case 32: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 32, true>), grid, dim3(NTH), 0, st, a); break;
+            case 64: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 64, true>), grid, dim3(NTH), 0, st, a); break;
+            default: return hipErrorInvalidValue;
+        }
+        return hipGetLastError();
+    }
     switch (L.C) {
-        case 16: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 16>), grid, dim3(NTH), 0, st, a); break;
-        case 32: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 32>), grid, dim3(NTH), 0, st, a); break;
-        case 64: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 64>), grid, dim3(NTH), 0, st, a); break;
+        case 16: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 16, false>), grid, dim3(NTH), 0, st, a); break;
+        case 32: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 32, false>), grid, dim3(NTH), 0, st, a); break;
+        case 64: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 64, false>), grid, dim3(NTH), 0, st, a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

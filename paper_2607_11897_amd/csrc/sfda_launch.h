@@ -22,6 +22,16 @@ struct ChunkLaunch {
     int B, H, T, m, n, C;
     int slice;         // value columns per workgroup (multiple of 8, <= 64)
     bool in_bf16, out_bf16;
+    // gated: alpha, theta, beta, k hold the pre-activations a, b, c and the raw keys, mapped
+    // by alpha = alpha_min + (alpha_max - alpha_min) sigmoid(a), theta = theta_max tanh(b),
+    // beta = sigmoid(c), k = k~ / (||k~|| + eps)
+    bool gated = false;
+    float alpha_min = 0.f, alpha_max = 1.f, theta_max = 0.f, eps = 0.f;
+};
+
+struct GateParams {
+    bool gated;
+    float alpha_min, alpha_max, theta_max, eps;
 };
 
 hipError_t launch_step(const StepLaunch& L, hipStream_t st);

@@ -206,6 +206,69 @@ class ChunkInputs:
                            self.dtype)
 
 
+@dataclasses.dataclass
+class GatedInputs:
+    """Stored inputs of one gated chunk-forward call (pre-activations), as exact
+    float64/complex128 values.  q, k_raw: [B,H,T,m] complex; v: [B,H,T,n] complex;
+    a, b: [B,H,T,m]; c: [B,H,T]; S0: [B,H,m,n] complex or None."""
+    q: np.ndarray
+    k_raw: np.ndarray
+    v: np.ndarray
+    a: np.ndarray
+    b: np.ndarray
+    c: np.ndarray
+    S0: Optional[np.ndarray]
+    dtype: str
+
+    @property
+    def shape(self):
+        B, H, T, m = self.q.shape
+        return B, H, T, m, self.v.shape[-1]
+
+    def storage(self) -> dict:
+        d = {name: to_storage(getattr(self, name), self.dtype)
+             for name in ("q", "k_raw", "v", "a", "b", "c")}
+        d["S0"] = None if self.S0 is None else to_storage(self.S0, "f32")
+        return d
+
+    def head(self, b: int, h: int) -> "GatedInputs":
+        sl = (slice(b, b + 1), slice(h, h + 1))
+        return GatedInputs(self.q[sl], self.k_raw[sl], self.v[sl], self.a[sl], self.b[sl],
+                           self.c[sl], None if self.S0 is None else self.S0[sl], self.dtype)
+
+
+def make_gated_inputs(B: int, H: int, T: int, m: int, n: int, dtype: str, seed: int,
+                      a_mean: float = 2.0, a_std: float = 1.5, b_std: float = 1.0,
+                      c_std: float = 1.0, s0_scale: Optional[float] = 0.1,
+                      zero_key_every: int = 0) -> GatedInputs:
+    """Seeded pre-activations: q, k_raw, v complex Gaussian CN(0, 1) (raw keys not
+    normalised), a ~ N(a_mean, a_std^2), b ~ N(0, b_std^2), c ~ N(0, c_std^2) per head from
+    PCG64 streams seeded (seed, b, h), drawn in the order q, k_raw, v, a, b, c, S0; every
+    zero_key_every-th token (if > 0) gets an all-zero raw key.  Rounded to the storage
+    dtype, which both the oracle and the GPU read."""
+    shp = lambda *t: (B, H) + t
+    q = np.empty(shp(T, m), np.complex128); k_raw = np.empty_like(q)
+    v = np.empty(shp(T, n), np.complex128)
+    a = np.empty(shp(T, m)); bb = np.empty(shp(T, m)); c = np.empty(shp(T))
+    S0 = None if s0_scale is None else np.empty(shp(m, n), np.complex128)
+    for ib in range(B):
+        for ih in range(H):
+            rng = np.random.Generator(np.random.PCG64([seed, ib, ih]))
+            q[ib, ih] = _cn(rng, (T, m))
+            k_raw[ib, ih] = _cn(rng, (T, m))
+            v[ib, ih] = _cn(rng, (T, n))
+            a[ib, ih] = rng.normal(a_mean, a_std, (T, m))
+            bb[ib, ih] = rng.normal(0.0, b_std, (T, m))
+            c[ib, ih] = rng.normal(0.0, c_std, (T,))
+            if S0 is not None:
+                S0[ib, ih] = s0_scale * _cn(rng, (m, n))
+    if zero_key_every > 0:
+        k_raw[:, :, ::zero_key_every, :] = 0
+    st = lambda x: round_to_storage(x, dtype)
+    return GatedInputs(st(q), st(k_raw), st(v), st(a), st(bb), st(c),
+                       None if S0 is None else round_to_storage(S0, "f32"), dtype)
+
+
 def make_chunk_inputs(w: Workload, T: Optional[int] = None, B: Optional[int] = None,
                       H: Optional[int] = None, heads: Optional[Sequence] = None,
                       m: Optional[int] = None, n: Optional[int] = None) -> ChunkInputs:

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(HERE, "libsfda.so")
 SFDA_F32, SFDA_BF16 = 0, 1
 STATUS = {0: "SFDA_OK", 1: "SFDA_ERR_NULL", 2: "SFDA_ERR_SHAPE", 3: "SFDA_ERR_CHUNK",
           4: "SFDA_ERR_DTYPE", 5: "SFDA_ERR_ALIGN", 6: "SFDA_ERR_ALIAS", 7: "SFDA_ERR_HIP"}
-EXPORTS = ("sfda_chunk_fwd", "sfda_chunk_fwd_sliced", "sfda_chunk_fwd_segmented",
+EXPORTS = ("sfda_chunk_fwd", "sfda_chunk_fwd_sliced", "sfda_chunk_fwd_gated", "sfda_chunk_fwd_segmented",
            "sfda_chunk_fwd_segmented_workspace_bytes", "sfda_step", "sfda_status_string",
            "sfda_abi_version")
 
@@ -45,6 +45,9 @@ def load_library(path: str = LIB_PATH):
     lib.sfda_chunk_fwd.restype = i
     lib.sfda_chunk_fwd_sliced.argtypes = [vp] * 9 + [i] * 7 + [i, i, vp]
     lib.sfda_chunk_fwd_sliced.restype = i
+    f = ctypes.c_float
+    lib.sfda_chunk_fwd_gated.argtypes = [vp] * 9 + [i] * 6 + [f] * 4 + [i, i, vp]
+    lib.sfda_chunk_fwd_gated.restype = i
     lib.sfda_chunk_fwd_segmented.argtypes = [vp] * 9 + [i] * 7 + [i, i, vp, ctypes.c_size_t, vp]
     lib.sfda_chunk_fwd_segmented.restype = i
     lib.sfda_chunk_fwd_segmented_workspace_bytes.argtypes = [i] * 5
@@ -123,6 +126,36 @@ def chunk_fwd(q, k, v, alpha, theta, beta, S0=None, C: int = 64, *, o=None, S_T=
         st = lib.sfda_chunk_fwd_sliced(*args, slice, in_code, _dtype_code(o), _stream(stream))
     if st != 0:
         raise SfdaError(st, "sfda_chunk_fwd")
+    return o, S_T
+
+
+def chunk_fwd_gated(q, k_raw, v, a, b, c, S0=None, C: int = 64, *, alpha_min: float,
+                    alpha_max: float, theta_max: float, eps: float, o=None, S_T=None,
+                    out_dtype=None, want_state: bool = True, stream=None) -> Tuple:
+    """SFDA chunkwise forward on pre-activations (sfda_chunk_fwd_gated): alpha, theta, beta
+    and the keys are formed inside the kernel from a, b [B,H,T,m], c [B,H,T] and the raw
+    keys k_raw [B,H,T,m,2].  Shapes and results otherwise as chunk_fwd."""
+    import torch
+    lib = load_library()
+    B, H, T, m, _ = q.shape
+    n = v.shape[3]
+    in_code = _dtype_code(q)
+    for t in (k_raw, v, a, b, c):
+        if t.dtype != q.dtype:
+            raise TypeError("q, k_raw, v, a, b, c must share one dtype")
+    out_dtype = q.dtype if out_dtype is None else out_dtype
+    if o is None:
+        o = torch.empty((B, H, T, n, 2), dtype=out_dtype, device=q.device)
+    if S_T is None and want_state:
+        S_T = torch.empty((B, H, m, n, 2), dtype=torch.float32, device=q.device)
+    if S0 is not None and S0.dtype != torch.float32:
+        raise TypeError("S0 must be float32")
+    st = lib.sfda_chunk_fwd_gated(_ptr(q), _ptr(k_raw), _ptr(v), _ptr(a), _ptr(b), _ptr(c), _ptr(S0),
+                                  _ptr(o), _ptr(S_T), B, H, T, m, n, C, float(alpha_min),
+                                  float(alpha_max), float(theta_max), float(eps), in_code,
+                                  _dtype_code(o), _stream(stream))
+    if st != 0:
+        raise SfdaError(st, "sfda_chunk_fwd_gated")
     return o, S_T
 
 

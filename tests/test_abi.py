@@ -97,6 +97,21 @@ def test_segmented_argument_errors(lib):
     assert seg(lib, B=0, q=None, ws=None) == 0        # nothing to do
 
 
+def gated(lib, amin=0.9, amax=1.0, tmax=0.5, eps=0.0, C=16, q=P[0]):
+    f = ctypes.c_float
+    return lib.sfda_chunk_fwd_gated(q, *P[1:], 1, 1, 4, 8, 8, C, f(amin), f(amax), f(tmax), f(eps),
+                                    0, 0, None)
+
+
+def test_gated_argument_errors(lib):
+    assert gated(lib, amin=0.0) == 2                   # alpha must stay positive
+    assert gated(lib, amin=0.95, amax=0.9) == 2
+    assert gated(lib, amax=1.5) == 2
+    assert gated(lib, tmax=-0.1) == 2
+    assert gated(lib, eps=float("nan")) == 2 and gated(lib, tmax=float("inf")) == 2
+    assert gated(lib, q=None) == 1 and gated(lib, C=8) == 3
+
+
 def test_step_argument_errors(lib):
     assert step(lib, S=None) == 1
     assert step(lib, m=0) == 2 and step(lib, m=65) == 2 and step(lib, n=0) == 2

@@ -1,0 +1,110 @@
+"""GPU parity of sfda_chunk_fwd_gated (the stable parameterization of Sec. 3 applied to
+the pre-activations inside the kernels) against the oracle: the float64 gate map of
+oracle.gates followed by the complex128 recurrence, on the same stored inputs.
+
+Bars as for sfda_chunk_fwd: max-norm relative error <= 1e-4 (float32 inputs), <= 2e-2
+(bfloat16 inputs), on o and on S_T.  Cases cover ragged sequences, m < 64 (padded
+channels must stay identity channels), all-zero raw keys with eps = 0, every chunk length,
+and the benchmarked shape at full size on sampled heads.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from gpu_util import I, ensure_built, rel_err, to_complex, to_device
+
+pytestmark = pytest.mark.gpu
+
+GATES = dict(alpha_min=0.9, alpha_max=1.0, theta_max=0.5)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def lib():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return ensure_built()
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+
+
+def run_gated(g, C, eps, out_dtype=None):
+    import torch
+    from paper_2607_11897_amd import sfda
+    st = g.storage()
+    d = {k: to_device(st[k], g.dtype) for k in ("q", "k_raw", "v", "a", "b", "c")}
+    S0 = None if st["S0"] is None else to_device(st["S0"], "f32")
+    od = None if out_dtype is None else {"f32": torch.float32, "bf16": torch.bfloat16}[out_dtype]
+    o, S = sfda.chunk_fwd_gated(d["q"], d["k_raw"], d["v"], d["a"], d["b"], d["c"], S0, C=C,
+                                eps=eps, out_dtype=od, **GATES)
+    torch.cuda.synchronize()
+    return to_complex(o), to_complex(S)
+
+
+def oracle_gated(g, eps):
+    import oracle
+    from oracle import gates
+    alpha, theta, beta, k = gates.gates(g.a, g.b, g.c, g.k_raw, GATES["alpha_min"],
+                                        GATES["alpha_max"], GATES["theta_max"], eps)
+    return oracle.recurrence(g.q, k, g.v, alpha, theta, beta, g.S0)
+
+
+@pytest.mark.parametrize("dtype,B,H,T,m,n,C,eps,zero_every", [
+    ("f32", 1, 2, 100, 64, 64, 16, 1e-6, 0),
+    ("f32", 2, 1, 70, 33, 24, 32, 0.0, 9),
+    ("f32", 1, 2, 130, 64, 80, 64, 1e-3, 0),
+    ("f32", 1, 1, 50, 5, 3, 16, 0.0, 4),
+    ("bf16", 1, 2, 300, 64, 64, 64, 1e-6, 0),
+    ("bf16", 2, 1, 97, 33, 24, 32, 0.0, 11),
+    ("bf16", 1, 2, 65, 16, 8, 16, 1e-2, 0),
+    ("bf16", 1, 1, 40, 5, 3, 64, 0.0, 3),
+])
+def test_gated_matches_oracle(dtype, B, H, T, m, n, C, eps, zero_every):
+    g = I.make_gated_inputs(B, H, T, m, n, dtype, seed=31 + T, zero_key_every=zero_every)
+    say(dtype, (B, H, T, m, n), "C", C, "eps", eps, "zero keys every", zero_every)
+    o, S = run_gated(g, C, eps)
+    o_ref, S_ref = oracle_gated(g, eps)
+    eo, es = rel_err(o, o_ref), rel_err(S, S_ref)
+    say("err(o)", eo, "err(S_T)", es)
+    tol = 1e-4 if dtype == "f32" else 2e-2
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(S))
+    assert eo <= tol and es <= tol
+
+
+def test_gated_zero_state():
+    g = I.make_gated_inputs(1, 2, 96, 64, 64, "f32", seed=3, s0_scale=None)
+    o, S = run_gated(g, 32, 1e-6)
+    o_ref, S_ref = oracle_gated(g, 1e-6)
+    assert rel_err(o, o_ref) <= 1e-4 and rel_err(S, S_ref) <= 1e-4
+
+
+def test_gated_bad_parameters_raise():
+    import torch
+    from paper_2607_11897_amd import sfda
+    g = I.make_gated_inputs(1, 1, 16, 8, 8, "f32", seed=1)
+    st = g.storage()
+    d = {k: to_device(st[k], "f32") for k in ("q", "k_raw", "v", "a", "b", "c")}
+    for bad in (dict(alpha_min=0.0, alpha_max=1.0, theta_max=0.5, eps=0.0),
+                dict(alpha_min=0.9, alpha_max=0.8, theta_max=0.5, eps=0.0),
+                dict(alpha_min=0.9, alpha_max=1.1, theta_max=0.5, eps=0.0),
+                dict(alpha_min=0.9, alpha_max=1.0, theta_max=-1.0, eps=0.0),
+                dict(alpha_min=0.9, alpha_max=1.0, theta_max=0.5, eps=float("nan"))):
+        with pytest.raises(sfda.SfdaError):
+            sfda.chunk_fwd_gated(d["q"], d["k_raw"], d["v"], d["a"], d["b"], d["c"], None, C=16, **bad)
+    torch.cuda.synchronize()
+
+
+def test_gated_bf16_b8h16_t4k_full_sampled_heads():
+    """The benchmarked shape with gated inputs (the bench's --mode gated workload), full
+    size; four heads checked against the oracle."""
+    g = I.make_gated_inputs(8, 16, 4096, 64, 64, "bf16", seed=2002)
+    say("gated bf16 b8h16 t4k: running")
+    o, S = run_gated(g, 64, 1e-6)
+    for (b, h) in [(0, 0), (2, 7), (5, 11), (7, 15)]:
+        gh = g.head(b, h)
+        o_ref, S_ref = oracle_gated(gh, 1e-6)
+        eo, es = rel_err(o[b, h], o_ref[0, 0]), rel_err(S[b, h], S_ref[0, 0])
+        say((b, h), "err(o)", eo, "err(S_T)", es)
+        assert eo <= 2e-2 and es <= 2e-2
