@@ -42,6 +42,7 @@ __global__ __launch_bounds__(NT) void fold_kernel(const float* __restrict__ P,
                                                   int G, int m, int n, int ncb)
 {
     __shared__ float2 S[MP][CB];
+    __shared__ float2 Ps[MP][MP + 1];     // P_g, rows padded against bank conflicts
     const long h = blockIdx.x / ncb;
     const int j0 = static_cast<int>(blockIdx.x - h * ncb) * CB;
     const int tid = threadIdx.x;
@@ -61,6 +62,19 @@ __global__ __launch_bounds__(NT) void fold_kernel(const float* __restrict__ P,
             s[c] = reinterpret_cast<const float2*>(S0)[h * mn + static_cast<long>(i) * n + j0 + jq + c];
         S[i][jq + c] = s[c];
     }
+    // P_g is fetched a segment ahead into registers (coalesced: element e = r * m + l of the
+    // m x m block, NPF per thread), so its load overlaps the products of the segment before
+    constexpr int NPF = MP * MP / NT;
+    float2 pf[NPF];
+    auto fetch_p = [&](long seg) {
+        const float2* pg = P2 + seg * static_cast<long>(m) * m;
+#pragma unroll
+        for (int u = 0; u < NPF; ++u) {
+            const int e = u * NT + tid;
+            pf[u] = e < m * m ? pg[e] : make_float2(0.f, 0.f);
+        }
+    };
+    fetch_p(h * G);
     __syncthreads();
     for (int gi = 0; gi < G; ++gi) {
         const long seg = h * G + gi;
@@ -70,14 +84,20 @@ __global__ __launch_bounds__(NT) void fold_kernel(const float* __restrict__ P,
             for (int c = 0; c < 4; ++c)
                 if (col_ok(c)) Sin2[seg * mn + static_cast<long>(i) * n + j0 + jq + c] = s[c];
         }
+#pragma unroll
+        for (int u = 0; u < NPF; ++u) {
+            const int e = u * NT + tid;
+            if (e < m * m) Ps[e / m][e % m] = pf[u];
+        }
+        __syncthreads();
+        if (gi + 1 < G) fetch_p(seg + 1);
         // row i of P_gi S + B_gi
         float2 acc[4];
 #pragma unroll
         for (int c = 0; c < 4; ++c) acc[c] = make_float2(0.f, 0.f);
         if (i < m) {
-            const float2* prow = P2 + seg * static_cast<long>(m) * m + static_cast<long>(i) * m;
             for (int l = 0; l < m; ++l) {
-                const float2 p = prow[l];
+                const float2 p = Ps[i][l];
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
                     const float2 x = S[l][jq + c];
@@ -93,7 +113,7 @@ __global__ __launch_bounds__(NT) void fold_kernel(const float* __restrict__ P,
                 acc[c].y += b.y;
             }
         }
-        __syncthreads();                // every row of S read
+        __syncthreads();                // every row of S and of P_gi read
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
             s[c] = acc[c];
