@@ -16,7 +16,8 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--only chunk|decode]
        [--no-cpu-baseline] [--mode copy|rmw|long]   (copy: a plain device copy, for counter
        scaling; rmw: an in-place pass over 1 GiB, the decode step's access pattern; long:
        the long-context workload, one workgroup per head against the segment-parallel scan;
-       gated: the benchmarked shape through sfda_chunk_fwd_gated)
+       gated: the benchmarked shape through sfda_chunk_fwd_gated; bwd: sfda_chunk_bwd on the
+       benchmarked shape and on the float32 workload B=4, H=8, T=2048)
 """
 from __future__ import annotations
 
@@ -34,8 +35,11 @@ METRIC = "SFDA fwd tokens/s (H=16,d_k=128,d_v=128,T=4096,C=64) + % MFMA/HBM peak
 HBM_PEAK_GBS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2516.6
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = ["paper_2607_11897_amd/csrc/sfda_chunk_bf16.hip", "paper_2607_11897_amd/csrc/sfda_chunk.hip",
-                  "paper_2607_11897_amd/csrc/sfda_step.hip", "paper_2607_11897_amd/csrc/sfda_device.h"]
+# the sources of the kernels the default bench line times (the bf16 chunk kernel and the
+# decode step); a counter summary is used only while they are unchanged
+KERNEL_SOURCES = ["paper_2607_11897_amd/csrc/sfda_chunk_bf16.hip", "paper_2607_11897_amd/csrc/sfda_step.hip",
+                  "paper_2607_11897_amd/csrc/sfda_device.h"]
+FP32_MFMA_PEAK_TFLOPS = 157.3
 
 
 def kernel_hash() -> str:
@@ -271,6 +275,94 @@ def gated(args):
     print(json.dumps(out), flush=True)
 
 
+def bwd_flops_per_chunk_head(C, m, n):
+    """Real flops per chunk and head of sfda_chunk_bwd's three passes, causal halves counted
+    (a complex multiply-add is 8 real flops; X = C m n, Y = C^2 m / 2, Z = C^2 n / 2):
+    forward scan L' Y, solve C^3/6, T conj(V) Z, T (conj(K) G) Y, Wt S X, state update X;
+    adjoint scan L', A 2Y, solve C^3/6, conj(Y') G X, A^* G_R Z, N^* G_Delta Z, two state
+    products 2X; gradient pass L' Y, E X, L' Delta Z, G_A and G_N 2Z, G_Yp, G_R S^*,
+    G_E S^* 3X, four token products with conj(K/G), conj(conj(K)G), conj(conj(Q)G) 4Y."""
+    X, Y, Z = C * m * n, C * C * m / 2, C * C * n / 2
+    fwd = Y + C ** 3 / 6 + Z + Y + 2 * X
+    adj = 2 * Y + C ** 3 / 6 + X + 2 * Z + 2 * X
+    grd = Y + X + Z + 2 * Z + 3 * X + 4 * Y
+    return 8 * (fwd + adj + grd)
+
+
+def bwd_bytes_per_token_head(m, n, in_bytes, out_bytes):
+    """Algorithmic HBM bytes of the backward per token and head: the forward's inputs read
+    once, dL/do read once, every input gradient written once (state terms are amortised
+    over T and left out)."""
+    inputs = (2 * m * 2 + n * 2 + 2 * m + 1) * in_bytes
+    return inputs + n * 2 * out_bytes + inputs
+
+
+def backward(args):
+    """sfda_chunk_bwd (three launches: recording forward scan, adjoint scan, gradient pass)
+    on the benchmarked shape (bf16) and on the float32 workload B=4, H=8, T=2048, inputs and
+    upstream gradients resident in HBM."""
+    import torch
+    from paper_2607_11897_amd import inputs as I
+    from paper_2607_11897_amd import sfda
+    import numpy as np
+    res = {"mode": "bwd", "kernel_hash_bwd": bwd_hash(), "runs": []}
+    for name in ("fwd_bf16_b8h16_t4k", "fwd_f32_b4h8_t2k"):
+        w = I.WORKLOADS[name]
+        print(f"# generating inputs for {w.name}", file=sys.stderr, flush=True)
+        x = I.make_chunk_inputs(w)
+        dO, dS = I.make_cotangents(w.B, w.H, w.T, w.m, w.n, w.dtype, seed=w.seed + 77)
+        st = x.storage()
+
+        def up(a, dt):
+            if dt == "bf16":
+                return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
+            return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+        d = {k: up(st[k], w.dtype) for k in ("q", "k", "v", "alpha", "theta", "beta")}
+        S0 = up(st["S0"], "f32")
+        dO_t = up(I.to_storage(dO, w.dtype), w.dtype)
+        dS_t = up(I.to_storage(dS, "f32"), "f32")
+        B, H, T, m, n = x.shape
+        ws = torch.empty(sfda.bwd_workspace_bytes(B, H, T, m, n, w.C), dtype=torch.uint8, device="cuda")
+        stream = torch.cuda.current_stream()
+
+        def run():
+            sfda.chunk_bwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], S0, dO_t, dS_t,
+                           C=w.C, workspace=ws, stream=stream)
+
+        def run_fwd():
+            sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], S0, C=w.C,
+                           stream=stream)
+
+        print(f"# timing sfda_chunk_bwd on {w.name}", file=sys.stderr, flush=True)
+        ms = timed(run, max(5, args.steps // 5), max(2, args.warmup // 5), stream)
+        ms_f = timed(run_fwd, max(5, args.steps // 5), max(2, args.warmup // 5), stream)
+        chunks = B * H * ((T + w.C - 1) // w.C)
+        flops = bwd_flops_per_chunk_head(w.C, m, n) * chunks
+        eb = 2 if w.dtype == "bf16" else 4
+        nbytes = bwd_bytes_per_token_head(m, n, eb, eb) * B * H * T
+        res["runs"].append({
+            "workload": w.name, "B": B, "H": H, "T": T, "m": m, "n": n, "C": w.C, "dtype": w.dtype,
+            "ms_bwd": round(ms, 4), "ms_fwd": round(ms_f, 4), "bwd_over_fwd": round(ms / ms_f, 2),
+            "tokens_per_s_bwd": round(B * T / (ms / 1e3), 1),
+            "useful_tflops": round(flops / (ms / 1e3) / 1e12, 2),
+            "frac_fp32_mfma_peak": round(flops / (ms / 1e3) / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4),
+            "algorithmic_GBps": round(nbytes / (ms / 1e3) / 1e9, 1),
+            "workspace_bytes": int(ws.numel())})
+        del d, dO_t, dS_t, ws
+        torch.cuda.empty_cache()
+    print(json.dumps(res), flush=True)
+
+
+def bwd_hash() -> str:
+    h = hashlib.sha256()
+    for p in ("paper_2607_11897_amd/csrc/sfda_chunk.hip", "paper_2607_11897_amd/csrc/sfda_chunk_grad.hip",
+              "paper_2607_11897_amd/csrc/sfda_chunk_common.h", "paper_2607_11897_amd/csrc/sfda_device.h"):
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
 def copy_calibration(args):
     """A plain device-to-device copy of 1 GiB, repeated, for scaling HBM counters."""
     import torch
@@ -300,7 +392,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--only", choices=["chunk", "decode"], default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=["bench", "copy", "rmw", "long", "gated"], default="bench")
+    ap.add_argument("--mode", choices=["bench", "copy", "rmw", "long", "gated", "bwd"], default="bench")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported. The (batch, head) "
@@ -325,6 +417,9 @@ def main():
         return
     if args.mode == "gated":
         gated(args)
+        return
+    if args.mode == "bwd":
+        backward(args)
         return
     stream = torch.cuda.current_stream()
     out = {}

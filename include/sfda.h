@@ -21,9 +21,9 @@
  * For the decode step drop the T axis: q, k [B, H, m], v, o [B, H, n], alpha, theta [B, H, m],
  * beta [B, H].
  *
- * Ownership: the caller allocates and frees every buffer (including the workspace of
- * sfda_chunk_fwd_segmented) and owns the stream; the library allocates no device memory
- * and keeps no state between calls (calls are reentrant; calls
+ * Ownership: the caller allocates and frees every buffer (including the workspaces of
+ * sfda_chunk_fwd_segmented and sfda_chunk_bwd) and owns the stream; the library allocates
+ * no device memory and keeps no state between calls (calls are reentrant; calls
  * that write the same buffers on different streams race, as any two kernels would).
  *
  * Errors: all argument checks run on the host before anything is enqueued; on any error
@@ -161,6 +161,39 @@ sfda_status_t sfda_chunk_fwd_segmented(const void* q, const void* k, const void*
                                        sfda_dtype_t in_dtype, sfda_dtype_t out_dtype,
                                        void* workspace, size_t workspace_bytes,
                                        sfda_stream_t stream);
+
+/*
+ * sfda_chunk_bwd -- reverse-mode gradients through sfda_chunk_fwd for a real scalar loss L
+ * (the backward of the chunkwise forward, recomputing the chunk factors of Thm 4.2 /
+ * Cor. 4.3 instead of storing them).  Given dO = dL/do and dS_T = dL/dS_T it returns the
+ * gradients with respect to every input; the gradient of a complex variable z is
+ * dL/dRe(z) + i dL/dIm(z).  Three launches on the stream: a forward scan recording the
+ * state entering each chunk and the chunk's solve result, a reverse scan carrying dL/dS
+ * through the chunks (the adjoint of the boundary-state map of Thm 6.1; it writes dv and
+ * dS0), and one workgroup per (head, chunk) forming dq, dk, dalpha, dtheta and dbeta.
+ *   q, k, v, alpha, theta, beta, S0 : as sfda_chunk_fwd (in_dtype; S0 NULL = zero state).
+ *   dO   : [B,H,T,n] complex (device, out_dtype); dS_T : [B,H,m,n] complex float32 or NULL
+ *          (zero).
+ *   dq, dk : [B,H,T,m] complex; dv : [B,H,T,n] complex; dalpha, dtheta : [B,H,T,m];
+ *          dbeta : [B,H,T] (device, in_dtype, written).  dS0 : [B,H,m,n] complex float32
+ *          or NULL (not wanted).  No output may overlap an input, another output or the
+ *          workspace (SFDA_ERR_ALIAS).
+ *   workspace : device memory of at least sfda_chunk_bwd_workspace_bytes(B, H, T, m, n, C)
+ *          bytes (SFDA_ERR_SHAPE if smaller, SFDA_ERR_NULL if NULL and needed), 16-byte
+ *          aligned, no initial contents; holds per chunk the state entering it and dL/dS
+ *          leaving it (m x n) and two C x n blocks, complex float32.
+ *   Sizes, C and dtypes as sfda_chunk_fwd; T == 0 writes dS0 = dS_T (or zeros).
+ *   alpha must be nonzero wherever T > 0 (dalpha divides by it).
+ */
+size_t sfda_chunk_bwd_workspace_bytes(int B, int H, int T, int m, int n, int C);
+
+sfda_status_t sfda_chunk_bwd(const void* q, const void* k, const void* v, const void* alpha,
+                             const void* theta, const void* beta, const float* S0,
+                             const void* dO, const float* dS_T, void* dq, void* dk, void* dv,
+                             void* dalpha, void* dtheta, void* dbeta, float* dS0,
+                             int B, int H, int T, int m, int n, int C, sfda_dtype_t in_dtype,
+                             sfda_dtype_t out_dtype, void* workspace, size_t workspace_bytes,
+                             sfda_stream_t stream);
 
 /*
  * sfda_step -- one recurrent decode token per (b, h) (Sec. 3, Eq. (sfda) and the readout),

@@ -9,7 +9,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsfda.so")
-SOURCES = ["sfda_api.hip", "sfda_chunk.hip", "sfda_chunk_bf16.hip", "sfda_segments.hip", "sfda_step.hip"]
+SOURCES = ["sfda_api.hip", "sfda_chunk.hip", "sfda_chunk_grad.hip", "sfda_chunk_bf16.hip", "sfda_segments.hip",
+           "sfda_step.hip"]
 ARCH = "gfx950"
 
 

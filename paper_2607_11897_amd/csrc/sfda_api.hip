@@ -218,6 +218,89 @@ sfda_status_t sfda_chunk_fwd_segmented(const void* q, const void* k, const void*
     return SFDA_OK;
 }
 
+size_t sfda_chunk_bwd_workspace_bytes(int B, int H, int T, int m, int n, int C)
+{
+    if (B <= 0 || H <= 0 || T < 0 || m < 1 || m > 64 || n < 1) return 0;
+    if (C != 16 && C != 32 && C != 64) return 0;
+    const size_t chunks = static_cast<size_t>(B) * H * ((static_cast<size_t>(T) + C - 1) / C);
+    // per chunk: S entering and dL/dS leaving (m x n each), Delta and G_F (C x n each)
+    return chunks * (2 * static_cast<size_t>(m) * n + 2 * static_cast<size_t>(C) * n) * 8;
+}
+
+sfda_status_t sfda_chunk_bwd(const void* q, const void* k, const void* v, const void* alpha,
+                             const void* theta, const void* beta, const float* S0,
+                             const void* dO, const float* dS_T, void* dq, void* dk, void* dv,
+                             void* dalpha, void* dtheta, void* dbeta, float* dS0, int B, int H,
+                             int T, int m, int n, int C, sfda_dtype_t in_dtype,
+                             sfda_dtype_t out_dtype, void* workspace, size_t workspace_bytes,
+                             sfda_stream_t stream)
+{
+    if (!dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return SFDA_ERR_DTYPE;
+    if (B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1) return SFDA_ERR_SHAPE;
+    if (C != 16 && C != 32 && C != 64) return SFDA_ERR_CHUNK;
+    const long BH = static_cast<long>(B) * H;
+    const int slice = n <= 64 ? ((n + 7) / 8) * 8 : 64;
+    const long nchunks = (static_cast<long>(T) + C - 1) / C;
+    if (BH * ((n + slice - 1) / slice) > 0x7FFFFFFFL || BH * nchunks > 0x7FFFFFFFL) return SFDA_ERR_SHAPE;
+    if (BH == 0) return SFDA_OK;
+    const bool need_inputs = T > 0;
+    if (need_inputs && (!q || !k || !v || !alpha || !theta || !beta || !dO || !dq || !dk || !dv ||
+                        !dalpha || !dtheta || !dbeta))
+        return SFDA_ERR_NULL;
+    const size_t need = sfda_chunk_bwd_workspace_bytes(B, H, T, m, n, C);
+    if (need > 0 && !workspace) return SFDA_ERR_NULL;
+    const void* ptrs[] = {q, k, v, alpha, theta, beta, S0, dO, dS_T, dq, dk, dv, dalpha, dtheta,
+                          dbeta, dS0, workspace};
+    for (const void* p : ptrs)
+        if (p && !aligned16(p)) return SFDA_ERR_ALIGN;
+    if (workspace_bytes < need) return SFDA_ERR_SHAPE;
+
+    const long ei = esize(in_dtype), eo = esize(out_dtype), BHT = BH * T;
+    const Range ins[] = {range_of(q, BHT * m * 2 * ei), range_of(k, BHT * m * 2 * ei),
+                         range_of(v, BHT * n * 2 * ei), range_of(alpha, BHT * m * ei),
+                         range_of(theta, BHT * m * ei), range_of(beta, BHT * ei),
+                         range_of(S0, BH * m * n * 2 * 4), range_of(dO, BHT * n * 2 * eo),
+                         range_of(dS_T, BH * m * n * 2 * 4)};
+    const Range outs[] = {range_of(dq, BHT * m * 2 * ei), range_of(dk, BHT * m * 2 * ei),
+                          range_of(dv, BHT * n * 2 * ei), range_of(dalpha, BHT * m * ei),
+                          range_of(dtheta, BHT * m * ei), range_of(dbeta, BHT * ei),
+                          range_of(dS0, BH * m * n * 2 * 4),
+                          range_of(workspace, static_cast<long>(need))};
+    for (int a = 0; a < 8; ++a) {
+        for (const Range& r : ins)
+            if (overlap(outs[a], r)) return SFDA_ERR_ALIAS;
+        for (int b = a + 1; b < 8; ++b)
+            if (overlap(outs[a], outs[b])) return SFDA_ERR_ALIAS;
+    }
+
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    float* S_rec = static_cast<float*>(workspace);
+    float* G_rec = S_rec + BH * nchunks * m * n * 2;
+    float* D_rows = G_rec + BH * nchunks * m * n * 2;
+    float* F_rows = D_rows + BH * nchunks * C * n * 2;
+    sfda::ChunkLaunch L;
+    L.q = q; L.k = k; L.v = v; L.alpha = alpha; L.theta = theta; L.beta = beta;
+    L.B = B; L.H = H; L.T = T; L.m = m; L.n = n; L.C = C; L.slice = slice;
+    L.in_bf16 = in_dtype == SFDA_BF16;
+    L.out_bf16 = out_dtype == SFDA_BF16;
+    L.o = nullptr;
+    // forward scan (the state entering every chunk and Delta) and reverse scan (dL/dS leaving
+    // every chunk, G_F, dv and dS0; with T == 0 only dS0 = dS_T), in one launch
+    sfda::ChunkLaunch F = L;
+    F.S0 = S0; F.S_T = nullptr; F.ck_state = S_rec; F.ck_rows = D_rows;
+    L.S0 = dS_T; L.S_T = dS0; L.ck_state = G_rec; L.ck_rows = F_rows; L.dO = dO; L.dv = dv;
+    if (sfda::launch_bwd_scans(F, L, st) != hipSuccess) return SFDA_ERR_HIP;
+    if (!need_inputs) return SFDA_OK;
+    sfda::GradLaunch Gl;
+    Gl.q = q; Gl.k = k; Gl.v = v; Gl.alpha = alpha; Gl.theta = theta; Gl.beta = beta; Gl.dO = dO;
+    Gl.S_rec = S_rec; Gl.G_rec = G_rec; Gl.D_rows = D_rows; Gl.F_rows = F_rows;
+    Gl.dq = dq; Gl.dk = dk; Gl.dalpha = dalpha; Gl.dtheta = dtheta; Gl.dbeta = dbeta;
+    Gl.B = B; Gl.H = H; Gl.T = T; Gl.m = m; Gl.n = n; Gl.C = C;
+    Gl.in_bf16 = L.in_bf16; Gl.out_bf16 = L.out_bf16;
+    if (sfda::launch_chunk_grad(Gl, st) != hipSuccess) return SFDA_ERR_HIP;
+    return SFDA_OK;
+}
+
 sfda_status_t sfda_step(const void* q, const void* k, const void* v, const void* alpha,
                         const void* theta, const void* beta, float* S, void* o, int B, int H,
                         int m, int n, sfda_dtype_t in_dtype, sfda_dtype_t out_dtype,

@@ -30,63 +30,173 @@
 // chunk), so K / G grows like exp(-sum log alpha); the caller keeps the in-chunk decay
 // product above ~1e-30.  Accumulation and the state are fp32; with PREC_BF16 the matrix
 // products take bf16 operands (the solve always runs in fp32).
+//
+// The same kernel runs the two scans of the backward: MODE 1 is the forward recording the
+// state entering each chunk and Delta; MODE 2 walks the chunks in reverse carrying dL/dS
+// (the adjoint of the chunk map, adjoint_chunk below) and records it with G_F.
 #include <type_traits>
 
-#include "sfda_device.h"
-#include "sfda_launch.h"
+#include "sfda_chunk_common.h"
 
 namespace sfda {
 
-constexpr int MP = 64;            // key channels handled per workgroup (m is zero-padded)
-constexpr int LDX = MP + 1;       // complex row stride of the C x MP operand arrays
-constexpr int NTHR = 256;
+// ---------------------------------------------------------------- adjoint scan (MODE 2)
+// The reverse-mode sweep over the chunks for dL/dS (the backward of the chunk map): with
+// G = dL/dS_out of this chunk and G_R = conj(dL/do) the adjoint of O^*, the chunk relations
+//   Delta = N D_beta (conj(V) - (conj(K) G) S),  O^* = (conj(Q) G) S + tril(A) Delta,
+//   S_out = diag(g_C) S + Y'^T Delta,  Y' = (K / G) diag(g_C)
+// give, column by column of the value dimension,
+//   G_Delta = conj(Y') G + A^* G_R,  G_F = N^* G_Delta,  G_E = D_beta G_F,
+//   dL/dS   = diag(conj(g_C)) G + (conj(Q) G)^* G_R - (conj(K) G)^* G_E,
+// and dL/dv = conj(G_E).  G_F is recorded per token (ck_rows) for the gradient pass; the
+// caller records G itself before the chunk.  A^* is read from A^T in g2's upper part, N^*
+// from N in its strict lower part.
+template <int P, typename TIN, int C>
+__device__ __forceinline__ void adjoint_chunk(ChunkSmem<C>& sm, const ChunkArgs& args,
+                                              f32x4 (&Sacc)[2][MP / 16],
+                                              const float2 (&vf)[2][C / 16][4], long bh, int t0,
+                                              int nchunks, int n0, int ncb, int tid)
+{
+    constexpr int NRB = C / 16;
+    constexpr int LDG = ChunkSmem<C>::LDG;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int c = lane & 15, g = lane >> 4, qp = lane & 1;
+    const int T = args.T, n = args.n;
+    const long base_tn = bh * static_cast<long>(T) * n;
+    TIN* __restrict__ gdv = static_cast<TIN*>(args.dv);
+#pragma unroll
+    for (int w = 0; w < 2; ++w) {
+        const int cb = wave + 4 * w;
+        if (cb >= ncb) continue;
+        const int j = n0 + cb * 8 + (c >> 1);
+        Frag8 br[NRB];                   // G_R = conj(dL/do), K = token
+#pragma unroll
+        for (int kb = 0; kb < NRB; ++kb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) bpair(br[kb], r, vf[w][kb][r].x, -vf[w][kb][r].y, qp);
+        Frag8 sb[MP / 16];
+#pragma unroll
+        for (int kb = 0; kb < MP / 16; ++kb) sb[kb] = bfrag_from_acc(Sacc[w][kb], qp);
+        // G_Delta = conj(Y') G + A^* G_R
+        f32x4 gd[NRB];
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb) {
+            const int row = rb * 16 + c;
+            f32x4 acc = zero4();
+#pragma unroll
+            for (int kb = 0; kb < MP / 16; ++kb) {
+                Frag8 a;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int i = kb * 16 + 4 * g + r;
+                    const float2 x = sm.ki[row * LDX + i], gg = sm.gc[i];
+                    a.v[2 * r] = x.x * gg.x - x.y * gg.y;
+                    a.v[2 * r + 1] = -(x.x * gg.y + x.y * gg.x);
+                }
+                mma<P>(acc, a, sb[kb]);
+            }
+#pragma unroll
+            for (int jb = rb; jb < NRB; ++jb) {
+                Frag8 a;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int jt = jb * 16 + 4 * g + r;
+                    const float2 x = masked(jt >= row, pin(sm.g2[row * LDG + jt]));   // A[jt][row]
+                    a.v[2 * r] = x.x;
+                    a.v[2 * r + 1] = -x.y;
+                }
+                mma<P>(acc, a, br[jb]);
+            }
+            gd[rb] = acc;
+        }
+        Frag8 gdb[NRB];
+#pragma unroll
+        for (int kb = 0; kb < NRB; ++kb) gdb[kb] = bfrag_from_acc(gd[kb], qp);
+        // G_F = N^* G_Delta (upper triangular, unit diagonal)
+        f32x4 ge[NRB];
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb) {
+            const int row = rb * 16 + c;
+            f32x4 acc = zero4();
+#pragma unroll
+            for (int kb = rb; kb < NRB; ++kb) {
+                Frag8 a;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int jt = kb * 16 + 4 * g + r;
+                    float2 x = pin(sm.g2[jt * LDG + row]);                        // N[jt][row]
+                    x = jt > row ? x : make_float2(jt == row ? 1.f : 0.f, 0.f);
+                    a.v[2 * r] = x.x;
+                    a.v[2 * r + 1] = -x.y;
+                }
+                mma<P>(acc, a, gdb[kb]);
+            }
+            // record G_F, write dL/dv = conj(beta G_F), keep G_E = beta G_F
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int tl = rb * 16 + 4 * g + r;
+                const float bt = sm.beta[tl];
+                if (j < n) {
+                    const long tr = static_cast<long>(nchunks) * C * bh + t0 + tl;
+                    args.ck_rows[2 * (tr * n + j) + qp] = acc[r];
+                    if (t0 + tl < T)
+                        Elem<TIN>::store(gdv, 2 * (base_tn + static_cast<long>(t0 + tl) * n + j) + qp,
+                                         qp ? -bt * acc[r] : bt * acc[r]);
+                }
+                acc[r] *= bt;
+            }
+            ge[rb] = acc;
+        }
+        Frag8 geb[NRB];
+#pragma unroll
+        for (int kb = 0; kb < NRB; ++kb) geb[kb] = bfrag_from_acc(ge[kb], qp);
+        // G <- diag(conj(g_C)) G + (conj(Q) G)^* G_R - (conj(K) G)^* G_E
+#pragma unroll
+        for (int kb = 0; kb < MP / 16; ++kb) {
+            const int irow = kb * 16 + c;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float2 gg = sm.gc[kb * 16 + 4 * g + r];
+                const float own = Sacc[w][kb][r];
+                const float oth = partner(own);
+                Sacc[w][kb][r] = qp ? (gg.x * own - gg.y * oth) : (gg.x * own + gg.y * oth);
+            }
+#pragma unroll
+            for (int tb = 0; tb < NRB; ++tb) {
+                Frag8 a, b;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int tl = tb * 16 + 4 * g + r;
+                    const float2 x = sm.qg[tl * LDX + irow], y = sm.kg[tl * LDX + irow];
+                    a.v[2 * r] = x.x;
+                    a.v[2 * r + 1] = -x.y;
+                    b.v[2 * r] = -y.x;
+                    b.v[2 * r + 1] = y.y;
+                }
+                mma<P>(Sacc[w][kb], a, br[tb]);
+                mma<P>(Sacc[w][kb], b, geb[tb]);
+            }
+        }
+    }
+}
 
-struct ChunkArgs {
-    const void *q, *k, *v, *alpha, *theta, *beta;
-    const float* S0;
-    void* o;
-    float* S_T;
-    int T, m, n, n_slices, slice;
-    // GATED: alpha = amin + aspan sigmoid(a), theta = tmax tanh(b), beta = sigmoid(c),
-    // k = k~ / (||k~|| + eps) from the pre-activations passed in alpha, theta, beta, k
-    float amin, aspan, tmax, eps;
-};
-
-__device__ __forceinline__ float sigmoid_acc(float x) { return 1.f / (1.f + expf(-x)); }
-
-template <int C>
-struct ChunkSmem {
-    static constexpr int LDG = C + 1;
-    float2 qg[C * LDX];      // conj(q_t) * g_t
-    float2 kg[C * LDX];      // conj(k_t) * g_t, later Wt = T (conj(K) * G)
-    float2 ki[C * LDX];      // k_t / g_t
-    float2 g2[C * LDG];      // packed: L' (strict lower) -> N; A^T (strict upper); A diag
-    float beta[C];
-    float2 gc[MP];           // g_C
-    float sega[4][MP];
-    float segp[4][MP];
-};
-
-template <int P, typename TIN, typename TOUT, int C, bool GATED>
-__global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
+// MODE 0: the forward.  MODE 1: the forward recording, per chunk, the state entering it
+// (ck_state) and Delta (ck_rows), for the backward.  MODE 2: the adjoint scan of the
+// backward, chunks in reverse order (below).
+template <int P, typename TIN, typename TOUT, int C, bool GATED, int MODE>
+__device__ __forceinline__ void chunk_scan(ChunkSmem<C>& sm, const ChunkArgs& args, unsigned block)
 {
     constexpr int NRB = C / 16;          // 16-token blocks per chunk
     constexpr int SEG = C / 4;           // tokens per thread in the cumulative sums
     constexpr int LDG = ChunkSmem<C>::LDG;
     constexpr int CBW = 2;               // value column blocks (8 complex columns) per wave
-    __shared__ ChunkSmem<C> sm;
 
-    const TIN* __restrict__ gq = static_cast<const TIN*>(args.q);
-    const TIN* __restrict__ gk = static_cast<const TIN*>(args.k);
     const TIN* __restrict__ gv = static_cast<const TIN*>(args.v);
-    const TIN* __restrict__ ga = static_cast<const TIN*>(args.alpha);
-    const TIN* __restrict__ gth = static_cast<const TIN*>(args.theta);
-    const TIN* __restrict__ gb = static_cast<const TIN*>(args.beta);
     TOUT* __restrict__ go = static_cast<TOUT*>(args.o);
 
     const int T = args.T, m = args.m, n = args.n;
-    const long bh = blockIdx.x / args.n_slices;
-    const int sl = blockIdx.x - static_cast<int>(bh) * args.n_slices;
+    const long bh = block / args.n_slices;
+    const int sl = block - static_cast<int>(bh) * args.n_slices;
     const int n0 = sl * args.slice;                       // first value column of the slice
     const int ncb = (min(args.slice, n - n0) + 7) / 8;    // active column blocks
 
@@ -97,15 +207,15 @@ __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
     const int g = lane >> 4;          // lane group
     const int qp = lane & 1;          // part (re / im) of this lane's output column
 
-    float* qgf = reinterpret_cast<float*>(sm.qg);
     float* kgf = reinterpret_cast<float*>(sm.kg);
     float* g2f = reinterpret_cast<float*>(sm.g2);
 
-    const long base_tm = bh * static_cast<long>(T) * m;   // [b,h,0,0] of q, k, alpha, theta
     const long base_tn = bh * static_cast<long>(T) * n;   // [b,h,0,0] of v, o
     const long base_mn = bh * static_cast<long>(m) * n;   // [b,h,0,0] of S0, S_T
+    const int nchunks = (T + C - 1) / C;
 
     // ---------------------------------------------------------------- state in registers
+    // (MODE 2: the adjoint of the state, starting from dL/dS_T)
     f32x4 Sacc[CBW][MP / 16];
 #pragma unroll
     for (int w = 0; w < CBW; ++w) {
@@ -126,12 +236,31 @@ __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
         }
     }
 
-    const int nchunks = (T + C - 1) / C;
-    for (int ch = 0; ch < nchunks; ++ch) {
+    for (int it_ch = 0; it_ch < nchunks; ++it_ch) {
+        const int ch = MODE == 2 ? nchunks - 1 - it_ch : it_ch;
         const int t0 = ch * C;
+        if constexpr (MODE != 0) {
+            // this wave's share of the chunk's [m][n] record: the state entering it (MODE 1)
+            // or the adjoint of the state leaving it (MODE 2)
+            const long base = (bh * nchunks + ch) * static_cast<long>(m) * n;
+#pragma unroll
+            for (int w = 0; w < CBW; ++w) {
+                const int cb = wave + 4 * w;
+                const int j = n0 + cb * 8 + (c >> 1);
+                if (cb >= ncb || j >= n) continue;
+#pragma unroll
+                for (int kb = 0; kb < MP / 16; ++kb)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int i = kb * 16 + 4 * g + r;
+                        if (i < m) args.ck_state[2 * (base + static_cast<long>(i) * n + j) + qp] = Sacc[w][kb][r];
+                    }
+            }
+        }
 
         // ============================================================ L: load, g, operands
         // this wave's conj(V) B-fragments for U = T conj(V): v[t0 + kb*16 + 4g + r][col]
+        // (MODE 2: dL/do, whose conjugate is the adjoint of O^*)
         float2 vf[CBW][NRB][4];
 #pragma unroll
         for (int w = 0; w < CBW; ++w) {
@@ -144,121 +273,22 @@ __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
                     const int t = t0 + kb * 16 + 4 * g + r;
                     const bool ok = cb < ncb && j < n && t < T;
                     float2 x = make_float2(0.f, 0.f);
-                    if (gv != nullptr)      // v == NULL reads as zeros (uniform branch)
-                        x = Elem<TIN>::load2(gv, base_tn + static_cast<long>(min(t, T - 1)) * n + min(j, n - 1));
+                    const long e = base_tn + static_cast<long>(min(t, T - 1)) * n + min(j, n - 1);
+                    if constexpr (MODE == 2)
+                        x = Elem<TOUT>::load2(static_cast<const TOUT*>(args.dO), e);
+                    else if (gv != nullptr)      // v == NULL reads as zeros (uniform branch)
+                        x = Elem<TIN>::load2(gv, e);
                     vf[w][kb][r] = masked(ok, x);
                 }
         }
         {
-            const int i = tid & 63;
-            const int seg = tid >> 6;
-            float la[SEG], ph[SEG];
-            float sa = 0.f, sp = 0.f;
-#pragma unroll
-            for (int u = 0; u < SEG; ++u) {
-                const int t = t0 + seg * SEG + u;
-                const bool ok = t < T && i < m;
-                const long e = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
-                const float a_ld = pin(Elem<TIN>::load(ga, e));
-                float th = masked(ok, Elem<TIN>::load(gth, e));
-                float a = ok ? a_ld : 1.f;
-                if constexpr (GATED) {      // padding stays the identity token (alpha = 1, theta = 0)
-                    a = ok ? args.amin + args.aspan * sigmoid_acc(a_ld) : 1.f;
-                    th = ok ? args.tmax * tanhf(th) : 0.f;
-                }
-                sa += __logf(a);
-                sp += th;
-                la[u] = sa;
-                ph[u] = sp;
-            }
-            sm.sega[seg][i] = sa;
-            sm.segp[seg][i] = sp;
-            {
-                const int tb = t0 + (tid & (C - 1));
-                float bv = Elem<TIN>::load(gb, bh * static_cast<long>(T) + min(tb, T - 1));
-                if constexpr (GATED) bv = sigmoid_acc(bv);
-                if (tid < C) sm.beta[tid] = masked(tb < T, bv);
-            }
-            __syncthreads();
-            float oa = 0.f, op = 0.f;
-            for (int s2 = 0; s2 < seg; ++s2) {
-                oa += sm.sega[s2][i];
-                op += sm.segp[s2][i];
-            }
-#pragma unroll
-            for (int u = 0; u < SEG; ++u) {
-                const int tl = seg * SEG + u;
-                const int t = t0 + tl;
-                const float A = la[u] + oa;
-                const float Ph = ph[u] + op;
-                const float e = __expf(A);
-                const float ei = __expf(-A);
-                float sn, cs;
-                __sincosf(Ph, &sn, &cs);
-                const float gr = e * cs, gi = e * sn;        // g_t
-                const float hr = ei * cs, hi = -ei * sn;     // 1 / g_t
-                const bool ok = t < T && i < m;
-                const long e2 = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
-                float2 qq = Elem<TIN>::load2(gq, e2), kk = Elem<TIN>::load2(gk, e2);
-                qq = masked(ok, qq);
-                kk = masked(ok, kk);
-                if constexpr (GATED) {
-                    // 1 / (||k~_t|| + eps): the wave holds channel i = lane of token t
-                    float s2 = kk.x * kk.x + kk.y * kk.y;
-#pragma unroll
-                    for (int sh = 1; sh < 64; sh <<= 1) s2 += __shfl_xor(s2, sh);
-                    const float den = sqrtf(s2) + args.eps;
-                    const float inv = den > 0.f ? 1.f / den : 0.f;
-                    kk.x *= inv;
-                    kk.y *= inv;
-                }
-                sm.qg[tl * LDX + i] = make_float2(qq.x * gr + qq.y * gi, qq.x * gi - qq.y * gr);
-                sm.kg[tl * LDX + i] = make_float2(kk.x * gr + kk.y * gi, kk.x * gi - kk.y * gr);
-                sm.ki[tl * LDX + i] = make_float2(kk.x * hr - kk.y * hi, kk.x * hi + kk.y * hr);
-                if (tl == C - 1) sm.gc[i] = make_float2(gr, gi);
-            }
+            float2 gkeep[SEG];
+            stage_load<TIN, C, GATED>(sm, args, bh, t0, tid, gkeep);
         }
         __syncthreads();
 
         // ============================================================ G: L' and A
-        {
-            constexpr int NCB = C / 8;                       // real column blocks of C x C
-            constexpr int NT1 = NRB * (NRB + 1);             // causal tiles per matrix
-            for (int tile = wave; tile < 2 * NT1; tile += 4) {
-                const int mat = tile / NT1;                  // 0: L' from conj(K)G, 1: A from conj(Q)G
-                int rem = tile - mat * NT1, rb = 0;
-                while (rem >= min(NCB, 2 * rb + 2)) { rem -= min(NCB, 2 * rb + 2); ++rb; }
-                const int cb = rem;
-                const float2* X = mat ? sm.qg : sm.kg;
-                const int row = rb * 16 + c;
-                const int jcol = cb * 8 + (c >> 1);
-                f32x4 acc = zero4();
-#pragma unroll
-                for (int kb = 0; kb < MP / 16; ++kb) {
-                    Frag8 a, b;
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int i = kb * 16 + 4 * g + r;
-                        const float2 x = X[row * LDX + i];
-                        a.v[2 * r] = x.x;
-                        a.v[2 * r + 1] = x.y;
-                        const float2 y = sm.ki[jcol * LDX + i];   // B(i, j) = (K/G)^T
-                        bpair(b, r, y.x, y.y, qp);
-                    }
-                    mma<P>(acc, a, b);
-                }
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int t = rb * 16 + 4 * g + r;
-                    if (mat == 0) {
-                        if (jcol < t) g2f[2 * (t * LDG + jcol) + qp] = acc[r];
-                    } else {
-                        if (jcol < t) g2f[2 * (jcol * LDG + t) + qp] = acc[r];
-                        else if (jcol == t) g2f[2 * (t * LDG + t) + qp] = acc[r];
-                    }
-                }
-            }
-        }
+        stage_gram<P, C, true>(sm, tid);
         __syncthreads();
 
         // ============================================================ S: N = (I + D_beta L')^{-1}
@@ -345,6 +375,13 @@ __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
                 }
             }
             __syncthreads();
+        }
+
+
+        if constexpr (MODE == 2) {
+            adjoint_chunk<P, TIN, C>(sm, args, Sacc, vf, bh, t0, nchunks, n0, ncb, tid);
+            __syncthreads();
+            continue;
         }
 
         // ============================================================ W: U and Wt
@@ -453,13 +490,22 @@ __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
                     mma<P>(pw, a, sb[kb]);
                 }
                 D[w][rb] = D[w][rb] - pw;
+                if constexpr (MODE == 1) {
+                    if (j < n) {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const long t = static_cast<long>(nchunks) * C * bh + t0 + rb * 16 + 4 * g + r;
+                            args.ck_rows[2 * (t * n + j) + qp] = D[w][rb][r];
+                        }
+                    }
+                }
             }
             Frag8 db[NRB];
 #pragma unroll
             for (int rb = 0; rb < NRB; ++rb) db[rb] = bfrag_from_acc(D[w][rb], qp);
-            // O^* = conj(Q)G S + tril(A) Delta ; o = conj(O^*)
+            // O^* = conj(Q)G S + tril(A) Delta ; o = conj(O^*)   (not needed for the record)
 #pragma unroll
-            for (int rb = 0; rb < NRB; ++rb) {
+            for (int rb = 0; rb < (MODE == 0 ? NRB : 0); ++rb) {
                 f32x4 acc = zero4();
                 const int row = rb * 16 + c;
 #pragma unroll
@@ -544,8 +590,27 @@ __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
     }
 }
 
-template <int P, typename TIN, typename TOUT>
-static hipError_t launch_chunk_t(const ChunkLaunch& L, hipStream_t st)
+template <int P, typename TIN, typename TOUT, int C, bool GATED, int MODE>
+__global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
+{
+    __shared__ ChunkSmem<C> sm;
+    chunk_scan<P, TIN, TOUT, C, GATED, MODE>(sm, args, blockIdx.x);
+}
+
+// The backward's two scans in one launch: the first nfwd workgroups run the recording
+// forward scan, the rest the adjoint scan (they read the same inputs and write disjoint
+// records), so both fill the GPU together.
+template <int P, typename TIN, typename TOUT, int C>
+__global__ __launch_bounds__(NTHR, 1) void scan_pair_kernel(ChunkArgs fwd, ChunkArgs adj, unsigned nfwd)
+{
+    __shared__ ChunkSmem<C> sm;
+    if (blockIdx.x < nfwd)
+        chunk_scan<P, TIN, float, C, false, 1>(sm, fwd, blockIdx.x);
+    else
+        chunk_scan<P, TIN, TOUT, C, false, 2>(sm, adj, blockIdx.x - nfwd);
+}
+
+static ChunkArgs make_args(const ChunkLaunch& L)
 {
     ChunkArgs a;
     a.q = L.q; a.k = L.k; a.v = L.v; a.alpha = L.alpha; a.theta = L.theta; a.beta = L.beta;
@@ -553,13 +618,21 @@ static hipError_t launch_chunk_t(const ChunkLaunch& L, hipStream_t st)
     a.T = L.T; a.m = L.m; a.n = L.n; a.slice = L.slice;
     a.n_slices = (L.n + L.slice - 1) / L.slice;
     a.amin = L.alpha_min; a.aspan = L.alpha_max - L.alpha_min; a.tmax = L.theta_max; a.eps = L.eps;
+    a.ck_state = L.ck_state; a.ck_rows = L.ck_rows; a.dO = L.dO; a.dv = L.dv;
+    return a;
+}
+
+template <int P, typename TIN, typename TOUT>
+static hipError_t launch_chunk_t(const ChunkLaunch& L, hipStream_t st)
+{
+    const ChunkArgs a = make_args(L);
     const dim3 grid(static_cast<unsigned>(static_cast<long>(L.B) * L.H * a.n_slices));
     auto go = [&](auto gated) {
         constexpr bool G = decltype(gated)::value;
         switch (L.C) {
-            case 16: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 16, G>), grid, dim3(NTHR), 0, st, a); break;
-            case 32: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 32, G>), grid, dim3(NTHR), 0, st, a); break;
-            case 64: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 64, G>), grid, dim3(NTHR), 0, st, a); break;
+            case 16: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 16, G, 0>), grid, dim3(NTHR), 0, st, a); break;
+            case 32: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 32, G, 0>), grid, dim3(NTHR), 0, st, a); break;
+            case 64: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 64, G, 0>), grid, dim3(NTHR), 0, st, a); break;
             default: return hipErrorInvalidValue;
         }
         return hipGetLastError();
@@ -572,6 +645,32 @@ hipError_t launch_chunk(const ChunkLaunch& L, hipStream_t st)
     if (L.in_bf16) return launch_chunk_bf16(L, st);
     return L.out_bf16 ? launch_chunk_t<PREC_F32, float, uint16_t>(L, st)
                       : launch_chunk_t<PREC_F32, float, float>(L, st);
+}
+
+// bf16 inputs take bf16 matrix-core operands (fp32 accumulation, fp32 state and records)
+template <int P, typename TIN, typename TOUT>
+static hipError_t launch_scans_t(const ChunkLaunch& F, const ChunkLaunch& A, hipStream_t st)
+{
+    const ChunkArgs af = make_args(F), aa = make_args(A);
+    const long nf = F.T > 0 ? static_cast<long>(F.B) * F.H * af.n_slices : 0;
+    const unsigned nfwd = static_cast<unsigned>(nf);
+    const dim3 grid(static_cast<unsigned>(nf + static_cast<long>(A.B) * A.H * aa.n_slices));
+    switch (F.C) {
+        case 16: hipLaunchKernelGGL((scan_pair_kernel<P, TIN, TOUT, 16>), grid, dim3(NTHR), 0, st, af, aa, nfwd); break;
+        case 32: hipLaunchKernelGGL((scan_pair_kernel<P, TIN, TOUT, 32>), grid, dim3(NTHR), 0, st, af, aa, nfwd); break;
+        case 64: hipLaunchKernelGGL((scan_pair_kernel<P, TIN, TOUT, 64>), grid, dim3(NTHR), 0, st, af, aa, nfwd); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_scans(const ChunkLaunch& F, const ChunkLaunch& A, hipStream_t st)
+{
+    if (F.in_bf16)
+        return A.out_bf16 ? launch_scans_t<PREC_BF16, uint16_t, uint16_t>(F, A, st)
+                          : launch_scans_t<PREC_BF16, uint16_t, float>(F, A, st);
+    return A.out_bf16 ? launch_scans_t<PREC_F32, float, uint16_t>(F, A, st)
+                      : launch_scans_t<PREC_F32, float, float>(F, A, st);
 }
 
 }  // namespace sfda

@@ -1,0 +1,191 @@
+// Shared pieces of the fp32-path chunk kernels (forward scan, adjoint scan, per-chunk
+// gradients): launch arguments, the LDS layout of one chunk's operands, and the two
+// state-independent stages every one of them starts a chunk with (the scans follow them
+// with the triangular inverse, inline in their kernel).
+//
+// Inside a chunk of C tokens (Thm 4.2 / Cor. 4.3 chunk-WY factors), with g_t the running
+// product of the decays lambda_1 ... lambda_t (the diagonal of Gamma_t):
+//   load   conj(Q) * G, conj(K) * G and K / G into LDS (the decay-scaled operands);
+//   gram   L'[t, j] = k_t^* diag(g_t / g_j) k_j (j < t) and A[r, j] = q_r^* diag(g_r / g_j) k_j
+//          (j <= r) on the matrix cores, packed in one C x C buffer.
+#pragma once
+
+#include "sfda_device.h"
+#include "sfda_launch.h"
+
+namespace sfda {
+
+constexpr int MP = 64;            // key channels handled per workgroup (m is zero-padded)
+constexpr int LDX = MP + 1;       // complex row stride of the C x MP operand arrays
+constexpr int NTHR = 256;
+
+struct ChunkArgs {
+    const void *q, *k, *v, *alpha, *theta, *beta;
+    const float* S0;     // adjoint scan: dL/dS_T (may be null)
+    void* o;
+    float* S_T;          // adjoint scan: dL/dS0
+    int T, m, n, n_slices, slice;
+    // GATED: alpha = amin + aspan sigmoid(a), theta = tmax tanh(b), beta = sigmoid(c),
+    // k = k~ / (||k~|| + eps) from the pre-activations passed in alpha, theta, beta, k
+    float amin, aspan, tmax, eps;
+    // backward passes: per-chunk records [heads][chunks][m][n] (state entering the chunk,
+    // or the adjoint of the state leaving it) and [heads][chunks * C][n] (Delta, or G_F)
+    float* ck_state;
+    float* ck_rows;
+    const void* dO;      // adjoint scan: dL/do, o's dtype
+    void* dv;            // adjoint scan: dL/dv, the inputs' dtype
+};
+
+__device__ __forceinline__ float sigmoid_acc(float x) { return 1.f / (1.f + expf(-x)); }
+
+template <int C>
+struct ChunkSmem {
+    static constexpr int LDG = C + 1;
+    float2 qg[C * LDX];      // conj(q_t) * g_t
+    float2 kg[C * LDX];      // conj(k_t) * g_t, later Wt = T (conj(K) * G)
+    float2 ki[C * LDX];      // k_t / g_t
+    float2 g2[C * LDG];      // packed: L' (strict lower) -> N; A^T (strict upper); A diag
+    float beta[C];
+    float2 gc[MP];           // g_C
+    float sega[4][MP];
+    float segp[4][MP];
+};
+
+// ----------------------------------------------------------------- load stage
+// Thread (channel i = tid % 64, segment tid / 64) walks C / 4 consecutive tokens of the
+// chunk starting at t0: running sums of log alpha and theta give g_t; the decay-scaled
+// operands go to LDS.  Padding past T (and channels past m) are identity tokens.  With
+// KEEP, g_t of the thread's tokens is returned in gkeep.
+template <typename TIN, int C, bool GATED, bool KEEP = false>
+__device__ __forceinline__ void stage_load(ChunkSmem<C>& sm, const ChunkArgs& args, long bh,
+                                           int t0, int tid, float2 (&gkeep)[C / 4])
+{
+    constexpr int SEG = C / 4;
+    const TIN* __restrict__ gq = static_cast<const TIN*>(args.q);
+    const TIN* __restrict__ gk = static_cast<const TIN*>(args.k);
+    const TIN* __restrict__ ga = static_cast<const TIN*>(args.alpha);
+    const TIN* __restrict__ gth = static_cast<const TIN*>(args.theta);
+    const TIN* __restrict__ gb = static_cast<const TIN*>(args.beta);
+    const int T = args.T, m = args.m;
+    const long base_tm = bh * static_cast<long>(T) * m;
+
+    const int i = tid & 63;
+    const int seg = tid >> 6;
+    float la[SEG], ph[SEG];
+    float sa = 0.f, sp = 0.f;
+#pragma unroll
+    for (int u = 0; u < SEG; ++u) {
+        const int t = t0 + seg * SEG + u;
+        const bool ok = t < T && i < m;
+        const long e = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
+        const float a_ld = pin(Elem<TIN>::load(ga, e));
+        float th = masked(ok, Elem<TIN>::load(gth, e));
+        float a = ok ? a_ld : 1.f;
+        if constexpr (GATED) {      // padding stays the identity token (alpha = 1, theta = 0)
+            a = ok ? args.amin + args.aspan * sigmoid_acc(a_ld) : 1.f;
+            th = ok ? args.tmax * tanhf(th) : 0.f;
+        }
+        sa += __logf(a);
+        sp += th;
+        la[u] = sa;
+        ph[u] = sp;
+    }
+    sm.sega[seg][i] = sa;
+    sm.segp[seg][i] = sp;
+    {
+        const int tb = t0 + (tid & (C - 1));
+        float bv = Elem<TIN>::load(gb, bh * static_cast<long>(T) + min(tb, T - 1));
+        if constexpr (GATED) bv = sigmoid_acc(bv);
+        if (tid < C) sm.beta[tid] = masked(tb < T, bv);
+    }
+    __syncthreads();
+    float oa = 0.f, op = 0.f;
+    for (int s2 = 0; s2 < seg; ++s2) {
+        oa += sm.sega[s2][i];
+        op += sm.segp[s2][i];
+    }
+#pragma unroll
+    for (int u = 0; u < SEG; ++u) {
+        const int tl = seg * SEG + u;
+        const int t = t0 + tl;
+        const float A = la[u] + oa;
+        const float Ph = ph[u] + op;
+        const float e = __expf(A);
+        const float ei = __expf(-A);
+        float sn, cs;
+        __sincosf(Ph, &sn, &cs);
+        const float gr = e * cs, gi = e * sn;        // g_t
+        const float hr = ei * cs, hi = -ei * sn;     // 1 / g_t
+        if constexpr (KEEP) gkeep[u] = make_float2(gr, gi);
+        const bool ok = t < T && i < m;
+        const long e2 = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
+        float2 qq = Elem<TIN>::load2(gq, e2), kk = Elem<TIN>::load2(gk, e2);
+        qq = masked(ok, qq);
+        kk = masked(ok, kk);
+        if constexpr (GATED) {
+            // 1 / (||k~_t|| + eps): the wave holds channel i = lane of token t
+            float s2 = kk.x * kk.x + kk.y * kk.y;
+#pragma unroll
+            for (int sh = 1; sh < 64; sh <<= 1) s2 += __shfl_xor(s2, sh);
+            const float den = sqrtf(s2) + args.eps;
+            const float inv = den > 0.f ? 1.f / den : 0.f;
+            kk.x *= inv;
+            kk.y *= inv;
+        }
+        sm.qg[tl * LDX + i] = make_float2(qq.x * gr + qq.y * gi, qq.x * gi - qq.y * gr);
+        sm.kg[tl * LDX + i] = make_float2(kk.x * gr + kk.y * gi, kk.x * gi - kk.y * gr);
+        sm.ki[tl * LDX + i] = make_float2(kk.x * hr - kk.y * hi, kk.x * hi + kk.y * hr);
+        if (tl == C - 1) sm.gc[i] = make_float2(gr, gi);
+    }
+}
+
+// ----------------------------------------------------------------- gram stage
+// L' (strict lower, at g2[t][j]) and, with WANT_A, A (A[r][j] for j < r at g2[j][r], the
+// diagonal at g2[r][r]).  Reads qg, kg, ki; the caller synchronises before and after.
+template <int P, int C, bool WANT_A>
+__device__ __forceinline__ void stage_gram(ChunkSmem<C>& sm, int tid)
+{
+    constexpr int NRB = C / 16;
+    constexpr int LDG = ChunkSmem<C>::LDG;
+    constexpr int NCB = C / 8;                       // real column blocks of C x C
+    constexpr int NT1 = NRB * (NRB + 1);             // causal tiles per matrix
+    const int lane = tid & 63, wave = tid >> 6;
+    const int c = lane & 15, g = lane >> 4, qp = lane & 1;
+    float* g2f = reinterpret_cast<float*>(sm.g2);
+    for (int tile = wave; tile < (WANT_A ? 2 : 1) * NT1; tile += 4) {
+        const int mat = tile / NT1;                  // 0: L' from conj(K)G, 1: A from conj(Q)G
+        int rem = tile - mat * NT1, rb = 0;
+        while (rem >= min(NCB, 2 * rb + 2)) { rem -= min(NCB, 2 * rb + 2); ++rb; }
+        const int cb = rem;
+        const float2* X = mat ? sm.qg : sm.kg;
+        const int row = rb * 16 + c;
+        const int jcol = cb * 8 + (c >> 1);
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int kb = 0; kb < MP / 16; ++kb) {
+            Frag8 a, b;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int i = kb * 16 + 4 * g + r;
+                const float2 x = X[row * LDX + i];
+                a.v[2 * r] = x.x;
+                a.v[2 * r + 1] = x.y;
+                const float2 y = sm.ki[jcol * LDX + i];   // B(i, j) = (K/G)^T
+                bpair(b, r, y.x, y.y, qp);
+            }
+            mma<P>(acc, a, b);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int t = rb * 16 + 4 * g + r;
+            if (mat == 0) {
+                if (jcol < t) g2f[2 * (t * LDG + jcol) + qp] = acc[r];
+            } else {
+                if (jcol < t) g2f[2 * (jcol * LDG + t) + qp] = acc[r];
+                else if (jcol == t) g2f[2 * (t * LDG + t) + qp] = acc[r];
+            }
+        }
+    }
+}
+
+}  // namespace sfda

@@ -27,6 +27,25 @@ struct ChunkLaunch {
     // beta = sigmoid(c), k = k~ / (||k~|| + eps)
     bool gated = false;
     float alpha_min = 0.f, alpha_max = 1.f, theta_max = 0.f, eps = 0.f;
+    // backward scans (launch_bwd_scans): per-chunk records
+    // [heads][chunks][m][n] and [heads][chunks * C][n] (complex fp32); the adjoint scan
+    // reads dL/do (o's dtype) and writes dL/dv (the inputs' dtype), and takes dL/dS_T in
+    // S0 and writes dL/dS0 to S_T
+    float* ck_state = nullptr;
+    float* ck_rows = nullptr;
+    const void* dO = nullptr;
+    void* dv = nullptr;
+};
+
+// per-chunk gradient pass of the backward (one workgroup per head and chunk)
+struct GradLaunch {
+    const void *q, *k, *v, *alpha, *theta, *beta;   // the forward's inputs
+    const void* dO;                                 // dL/do, o's dtype
+    const float *S_rec, *G_rec;                     // [heads][chunks][m][n]: S entering, dL/dS leaving
+    const float *D_rows, *F_rows;                   // [heads][chunks * C][n]: Delta, G_F
+    void *dq, *dk, *dalpha, *dtheta, *dbeta;        // the inputs' dtype
+    int B, H, T, m, n, C;
+    bool in_bf16, out_bf16;
 };
 
 struct GateParams {
@@ -37,6 +56,10 @@ struct GateParams {
 hipError_t launch_step(const StepLaunch& L, hipStream_t st);
 hipError_t launch_chunk(const ChunkLaunch& L, hipStream_t st);
 hipError_t launch_chunk_bf16(const ChunkLaunch& L, hipStream_t st);   // bf16 inputs
+// backward: the forward scan recording states and Delta (F; none when F.T == 0) and the
+// reverse adjoint scan (A) in one launch, then the per-chunk gradient pass
+hipError_t launch_bwd_scans(const ChunkLaunch& F, const ChunkLaunch& A, hipStream_t st);
+hipError_t launch_chunk_grad(const GradLaunch& L, hipStream_t st);
 // segment-parallel scan: identity fill and the fold of the segments' affine maps
 hipError_t launch_identity(float* P, long count, int m, hipStream_t st);
 hipError_t launch_fold(const float* P, const float* Bs, float* Sin, const float* S0, float* S_T,

@@ -294,6 +294,26 @@ def make_chunk_inputs(w: Workload, T: Optional[int] = None, B: Optional[int] = N
                        stack(6, "f32"), w.dtype)
 
 
+def make_cotangents(B: int, H: int, T: int, m: int, n: int, out_dtype: str, seed: int,
+                    dS_scale: Optional[float] = 1.0, heads: Optional[Sequence] = None):
+    """Seeded upstream gradients for the backward: dO = dL/do [B,H,T,n] ~ CN(0, 1) rounded
+    to o's storage dtype, and dS_T = dL/dS_T [B,H,m,n] ~ dS_scale CN(0, 1) rounded to
+    float32 (None when dS_scale is None).  Per head from PCG64 streams seeded
+    (seed, b, h, 1), drawn in the order dO, dS_T; ``heads`` as in make_chunk_inputs."""
+    pairs = [(b, h) for b in range(B) for h in range(H)] if heads is None else list(heads)
+    shape_bh = (B, H) if heads is None else (1, len(pairs))
+    dO = np.empty((len(pairs), T, n), np.complex128)
+    dS = None if dS_scale is None else np.empty((len(pairs), m, n), np.complex128)
+    for j, (b, h) in enumerate(pairs):
+        rng = np.random.Generator(np.random.PCG64([seed, b, h, 1]))
+        dO[j] = _cn(rng, (T, n))
+        if dS is not None:
+            dS[j] = dS_scale * _cn(rng, (m, n))
+    dO = round_to_storage(dO.reshape(shape_bh + (T, n)), out_dtype)
+    dS = None if dS is None else round_to_storage(dS.reshape(shape_bh + (m, n)), "f32")
+    return dO, dS
+
+
 # ---------------------------------------------------------------------------
 # decode-step inputs
 # ---------------------------------------------------------------------------

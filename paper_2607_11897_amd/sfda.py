@@ -18,8 +18,8 @@ SFDA_F32, SFDA_BF16 = 0, 1
 STATUS = {0: "SFDA_OK", 1: "SFDA_ERR_NULL", 2: "SFDA_ERR_SHAPE", 3: "SFDA_ERR_CHUNK",
           4: "SFDA_ERR_DTYPE", 5: "SFDA_ERR_ALIGN", 6: "SFDA_ERR_ALIAS", 7: "SFDA_ERR_HIP"}
 EXPORTS = ("sfda_chunk_fwd", "sfda_chunk_fwd_sliced", "sfda_chunk_fwd_gated", "sfda_chunk_fwd_segmented",
-           "sfda_chunk_fwd_segmented_workspace_bytes", "sfda_step", "sfda_status_string",
-           "sfda_abi_version")
+           "sfda_chunk_fwd_segmented_workspace_bytes", "sfda_chunk_bwd", "sfda_chunk_bwd_workspace_bytes",
+           "sfda_step", "sfda_status_string", "sfda_abi_version")
 
 _lib = None
 
@@ -52,6 +52,10 @@ def load_library(path: str = LIB_PATH):
     lib.sfda_chunk_fwd_segmented.restype = i
     lib.sfda_chunk_fwd_segmented_workspace_bytes.argtypes = [i] * 5
     lib.sfda_chunk_fwd_segmented_workspace_bytes.restype = ctypes.c_size_t
+    lib.sfda_chunk_bwd.argtypes = [vp] * 16 + [i] * 6 + [i, i, vp, ctypes.c_size_t, vp]
+    lib.sfda_chunk_bwd.restype = i
+    lib.sfda_chunk_bwd_workspace_bytes.argtypes = [i] * 6
+    lib.sfda_chunk_bwd_workspace_bytes.restype = ctypes.c_size_t
     lib.sfda_step.argtypes = [vp] * 8 + [i] * 4 + [i, i, vp]
     lib.sfda_step.restype = i
     lib.sfda_status_string.argtypes = [i]
@@ -157,6 +161,45 @@ def chunk_fwd_gated(q, k_raw, v, a, b, c, S0=None, C: int = 64, *, alpha_min: fl
     if st != 0:
         raise SfdaError(st, "sfda_chunk_fwd_gated")
     return o, S_T
+
+
+def chunk_bwd(q, k, v, alpha, theta, beta, S0, dO, dS_T=None, C: int = 64, *,
+              want_dS0: bool = True, workspace=None, stream=None) -> dict:
+    """Gradients of a real loss through the chunkwise forward (sfda_chunk_bwd), given
+    dO = dL/do [B,H,T,n,2] (o's dtype) and dS_T = dL/dS_T [B,H,m,n,2] float32 or None.
+    Inputs as chunk_fwd.  Returns dq, dk, dv, dalpha, dtheta, dbeta in the inputs' dtype and
+    dS0 (float32, or None without want_dS0); complex gradients are dL/dRe + i dL/dIm.
+    `workspace`: a uint8 device tensor of at least bwd_workspace_bytes(...) bytes, allocated
+    here when not given."""
+    import torch
+    lib = load_library()
+    B, H, T, m, _ = q.shape
+    n = v.shape[3]
+    in_code = _dtype_code(q)
+    for t in (k, v, alpha, theta, beta):
+        if t.dtype != q.dtype:
+            raise TypeError("q, k, v, alpha, theta, beta must share one dtype")
+    for t in (S0, dS_T):
+        if t is not None and t.dtype != torch.float32:
+            raise TypeError("S0 and dS_T must be float32")
+    g = dict(dq=torch.empty_like(q), dk=torch.empty_like(k), dv=torch.empty_like(v),
+             dalpha=torch.empty_like(alpha), dtheta=torch.empty_like(theta), dbeta=torch.empty_like(beta),
+             dS0=torch.empty((B, H, m, n, 2), dtype=torch.float32, device=q.device) if want_dS0 else None)
+    nws = lib.sfda_chunk_bwd_workspace_bytes(B, H, T, m, n, C)
+    if workspace is None:
+        workspace = torch.empty(max(nws, 1), dtype=torch.uint8, device=q.device)
+    st = lib.sfda_chunk_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(theta), _ptr(beta), _ptr(S0),
+                            _ptr(dO), _ptr(dS_T), _ptr(g["dq"]), _ptr(g["dk"]), _ptr(g["dv"]),
+                            _ptr(g["dalpha"]), _ptr(g["dtheta"]), _ptr(g["dbeta"]), _ptr(g["dS0"]),
+                            B, H, T, m, n, C, in_code, _dtype_code(dO), _ptr(workspace),
+                            workspace.numel(), _stream(stream))
+    if st != 0:
+        raise SfdaError(st, "sfda_chunk_bwd")
+    return g
+
+
+def bwd_workspace_bytes(B: int, H: int, T: int, m: int, n: int, C: int) -> int:
+    return int(load_library().sfda_chunk_bwd_workspace_bytes(B, H, T, m, n, C))
 
 
 def segmented_workspace_bytes(B: int, H: int, m: int, n: int, G: int) -> int:

@@ -132,3 +132,51 @@ def test_binding_fails_loudly_without_library(tmp_path):
             sfda.load_library(str(tmp_path / "missing.so"))
         finally:
             sfda._lib = old
+
+
+# --------------------------------------------------------------------------- backward
+PB = [A * (i + 1) for i in range(17)]       # 16 tensors + workspace
+
+
+def bwd(lib, ptrs=None, B=1, H=1, T=40, m=8, n=8, C=16, din=0, dout=0, ws_bytes=None):
+    p = list(PB if ptrs is None else ptrs)
+    need = lib.sfda_chunk_bwd_workspace_bytes(max(B, 1), max(H, 1), T, m, n, C)
+    ws = need if ws_bytes is None else ws_bytes
+    return lib.sfda_chunk_bwd(*p[:16], B, H, T, m, n, C, din, dout, p[16], ws, None)
+
+
+def test_bwd_workspace_bytes(lib):
+    # per chunk: two m x n and two C x n complex float32 blocks
+    assert lib.sfda_chunk_bwd_workspace_bytes(8, 16, 4096, 64, 64, 64) == 8 * 16 * 64 * (2 * 64 * 64 + 2 * 64 * 64) * 8
+    assert lib.sfda_chunk_bwd_workspace_bytes(1, 1, 65, 8, 8, 64) == 2 * (2 * 8 * 8 + 2 * 64 * 8) * 8
+    assert lib.sfda_chunk_bwd_workspace_bytes(1, 1, 0, 8, 8, 16) == 0
+    for bad in [(0, 1, 4, 8, 8, 16), (1, 1, 4, 65, 8, 16), (1, 1, 4, 8, 0, 16), (1, 1, 4, 8, 8, 48)]:
+        assert lib.sfda_chunk_bwd_workspace_bytes(*bad) == 0
+
+
+def test_bwd_argument_errors(lib):
+    assert bwd(lib, B=0) == 0                                  # nothing to do
+    assert bwd(lib, C=48) == 3
+    assert bwd(lib, din=5) == 4
+    assert bwd(lib, m=65) == 2
+    assert bwd(lib, T=-1) == 2
+    for idx in list(range(6)) + [7] + list(range(9, 15)):     # required: inputs, dO, gradients
+        p = list(PB)
+        p[idx] = 0
+        assert bwd(lib, p) == 1, idx
+    p = list(PB)
+    p[16] = 0
+    assert bwd(lib, p) == 1                                    # workspace needed
+    p = list(PB)
+    p[9] += 8
+    assert bwd(lib, p) == 5                                    # misaligned dq
+    assert bwd(lib, ws_bytes=100) == 2                         # workspace too small
+    p = list(PB)
+    p[9] = p[0]
+    assert bwd(lib, p) == 6                                    # dq over q
+    p = list(PB)
+    p[16] = p[12]
+    assert bwd(lib, p) == 6                                    # workspace over dtheta
+    p = list(PB)
+    p[15] = p[8]
+    assert bwd(lib, p) == 6                                    # dS0 over dS_T

@@ -1,0 +1,150 @@
+"""GPU parity of sfda_chunk_bwd (gradients of a real loss through the chunkwise forward)
+against the oracle's reverse-mode sweep over the token recurrence (oracle.backward, pinned
+by finite differences in test_oracle_backward.py), on the same stored inputs and upstream
+gradients.
+
+Bars, per gradient tensor, max |x - ref| / max |ref|: 1e-4 for float32 inputs (the whole
+backward runs in float32 with float32 records); 2e-2 for bfloat16 inputs and gradients
+(both sides read the same rounded inputs; the kernels keep float32 records and round each
+gradient to bfloat16 once, a relative 2^-9).  Cases cover ragged sequences, m < 64, n not a
+multiple of 16 and above 64 (several column slices in the scans, five K-blocks in the
+gradient pass), every chunk length, the zero state without dL/dS_T, T = 0, and the two
+benchmarked shapes at full size on sampled heads.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from gpu_util import I, ensure_built, rel_err, to_complex, to_device, upload
+
+pytestmark = pytest.mark.gpu
+
+NAMES = ("dq", "dk", "dv", "dalpha", "dtheta", "dbeta", "dS0")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def lib():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return ensure_built()
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+
+
+def as_np(t, complex_):
+    if t is None:
+        return None
+    return to_complex(t) if complex_ else t.float().cpu().numpy().astype(np.float64)
+
+
+def run_bwd(x, dO, dS, C, out_dtype):
+    import torch
+    from paper_2607_11897_amd import sfda
+    d = upload(x)
+    dO_t = to_device(I.to_storage(dO, out_dtype), out_dtype)
+    dS_t = None if dS is None else to_device(I.to_storage(dS, "f32"), "f32")
+    g = sfda.chunk_bwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], d["S0"], dO_t,
+                       dS_t, C=C)
+    torch.cuda.synchronize()
+    return {kk: as_np(g[kk], kk in ("dq", "dk", "dv", "dS0")) for kk in NAMES}
+
+
+def oracle_bwd(x, dO, dS):
+    from oracle import backward as BW
+    return BW.recurrence_backward(x.q, x.k, x.v, x.alpha, x.theta, x.beta, x.S0, dO, dS)
+
+
+def check(got, ref, tol, label):
+    errs = {kk: rel_err(got[kk], ref[kk]) for kk in NAMES}
+    say(label, {kk: f"{e:.2e}" for kk, e in errs.items()})
+    for kk in NAMES:
+        assert np.all(np.isfinite(got[kk])), kk
+    bad = {kk: e for kk, e in errs.items() if not e <= tol}
+    assert not bad, f"{label}: {bad}"
+
+
+def make(B, H, T, m, n, dtype, seed, zero_state=False):
+    laws = I.LAWS_MAIN
+    if zero_state:
+        laws = I.Laws(laws.alpha, laws.theta, laws.beta, None)
+    w = I.Workload("bwd", B, H, T, m, n, 64, dtype, laws, seed, 1e-4)
+    return I.make_chunk_inputs(w)
+
+
+@pytest.mark.parametrize("dtype,B,H,T,m,n,C", [
+    ("f32", 1, 2, 100, 64, 64, 16),
+    ("f32", 2, 1, 70, 33, 24, 32),
+    ("f32", 1, 2, 130, 64, 80, 64),
+    ("f32", 1, 1, 50, 5, 3, 16),
+    ("f32", 1, 1, 64, 64, 64, 64),
+    ("bf16", 1, 2, 300, 64, 64, 64),
+    ("bf16", 2, 1, 97, 33, 24, 32),
+    ("bf16", 1, 1, 40, 16, 8, 16),
+])
+def test_bwd_matches_oracle(dtype, B, H, T, m, n, C):
+    x = make(B, H, T, m, n, dtype, seed=400 + T)
+    dO, dS = I.make_cotangents(B, H, T, m, n, dtype, seed=500 + T)
+    say(dtype, (B, H, T, m, n), "C", C)
+    got = run_bwd(x, dO, dS, C, dtype)
+    ref = oracle_bwd(x, dO, dS)
+    check(got, ref, 1e-4 if dtype == "f32" else 2e-2, f"{dtype} {(B, H, T, m, n)} C{C}")
+
+
+def test_bwd_zero_state_and_no_state_gradient():
+    x = make(1, 2, 96, 64, 64, "f32", seed=9, zero_state=True)
+    dO, _ = I.make_cotangents(1, 2, 96, 64, 64, "f32", seed=10, dS_scale=None)
+    got = run_bwd(x, dO, None, 32, "f32")
+    ref = oracle_bwd(x, dO, None)
+    check(got, ref, 1e-4, "zero state, dS_T = 0")
+
+
+def test_bwd_f32_inputs_bf16_output_gradient():
+    x = make(1, 2, 80, 64, 48, "f32", seed=11)
+    dO, dS = I.make_cotangents(1, 2, 80, 64, 48, "bf16", seed=12)
+    got = run_bwd(x, dO, dS, 16, "bf16")
+    ref = oracle_bwd(x, dO, dS)
+    check(got, ref, 1e-4, "f32 inputs, bf16 dO")
+
+
+def test_bwd_empty_sequence_passes_state_gradient_through():
+    import torch
+    from paper_2607_11897_amd import sfda
+    B, H, m, n = 2, 3, 16, 8
+    z = lambda *s: torch.zeros(s, dtype=torch.float32, device="cuda")
+    dS = torch.randn(B, H, m, n, 2, device="cuda")
+    g = sfda.chunk_bwd(z(B, H, 0, m, 2), z(B, H, 0, m, 2), z(B, H, 0, n, 2), z(B, H, 0, m),
+                       z(B, H, 0, m), z(B, H, 0), None, z(B, H, 0, n, 2), dS, C=16)
+    torch.cuda.synchronize()
+    assert torch.equal(g["dS0"], dS)
+
+
+def test_bwd_is_deterministic():
+    import torch
+    x = make(1, 2, 130, 64, 64, "f32", seed=13)
+    dO, dS = I.make_cotangents(1, 2, 130, 64, 64, "f32", seed=14)
+    a = run_bwd(x, dO, dS, 64, "f32")
+    b = run_bwd(x, dO, dS, 64, "f32")
+    for kk in NAMES:
+        assert np.array_equal(a[kk], b[kk]), kk
+
+
+@pytest.mark.parametrize("name,heads", [
+    ("fwd_f32_b4h8_t2k", [(0, 0), (3, 7)]),
+    ("fwd_bf16_b8h16_t4k", [(0, 0), (5, 11)]),
+])
+def test_bwd_full_size_sampled_heads(name, heads):
+    """The two benchmarked shapes at full size in one call; sampled heads against the
+    oracle (heads are independent, so a head's oracle gradients are exact for it)."""
+    w = I.WORKLOADS[name]
+    say(name, "generating")
+    x = I.make_chunk_inputs(w)
+    dO, dS = I.make_cotangents(w.B, w.H, w.T, w.m, w.n, w.dtype, seed=w.seed + 77)
+    say(name, "running the backward")
+    got = run_bwd(x, dO, dS, w.C, w.dtype)
+    for (b, h) in heads:
+        ref = oracle_bwd(x.head(b, h), dO[b:b + 1, h:h + 1], dS[b:b + 1, h:h + 1])
+        gh = {kk: got[kk][b:b + 1, h:h + 1] for kk in NAMES}
+        check(gh, ref, w.tol, f"{name} head {(b, h)}")
