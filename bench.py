@@ -17,7 +17,8 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--only chunk|decode]
        scaling; rmw: an in-place pass over 1 GiB, the decode step's access pattern; long:
        the long-context workload, one workgroup per head against the segment-parallel scan;
        gated: the benchmarked shape through sfda_chunk_fwd_gated; bwd: sfda_chunk_bwd on the
-       benchmarked shape and on the float32 workload B=4, H=8, T=2048)
+       benchmarked shape and on the float32 workload B=4, H=8, T=2048; dec: the write-decoupled
+       variant on the benchmarked batch, heads and length with C=32)
 """
 from __future__ import annotations
 
@@ -354,6 +355,52 @@ def backward(args):
     print(json.dumps(res), flush=True)
 
 
+def dec_flops_per_chunk_head(C, m, n):
+    """Real flops per chunk and head of the write-decoupled forward, causal halves counted:
+    Gram blocks L'_kk, A_qk, L'_kr, A_qr (4 C^2 m / 2), Wt = T conj(K)G (C^2 m / 2), the solve
+    C^3 / 6, Y = L'_kr Delta_r and T Y (2 C^2 n / 2), A_qk Delta_k and A_qr Delta_r (2 C^2 n / 2),
+    Wt S, conj(Q)G S and the two state products (4 C m n)."""
+    return 8 * (5 * C * C * m / 2 + 4 * C * C * n / 2 + 4 * C * m * n + C ** 3 / 6)
+
+
+def decoupled(args):
+    """sfda_chunk_fwd_decoupled on the benchmarked batch, heads and length (bf16, C = 32),
+    beside sfda_chunk_fwd on the same sizes and chunk length."""
+    import numpy as np
+    import torch
+    from paper_2607_11897_amd import inputs as I
+    from paper_2607_11897_amd import sfda
+    B, H, T, m, n, C = 8, 16, 4096, 64, 64, 32
+    print("# generating write-decoupled inputs", file=sys.stderr, flush=True)
+    x = I.make_decoupled_inputs(B, H, T, m, n, "bf16", seed=3003)
+    st = x.storage()
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
+    d = {k: up(st[k]) for k in ("q", "k", "r", "v", "alpha", "theta", "eta", "beta")}
+    S0 = torch.from_numpy(np.ascontiguousarray(st["S0"], dtype=np.float32)).cuda()
+    o = torch.empty((B, H, T, n, 2), dtype=torch.bfloat16, device="cuda")
+    S_T = torch.empty((B, H, m, n, 2), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def run_dec():
+        sfda.chunk_fwd_decoupled(d["q"], d["k"], d["r"], d["v"], d["alpha"], d["theta"], d["eta"], d["beta"],
+                                 S0, C=C, o=o, S_T=S_T, stream=stream)
+
+    def run_tied():
+        sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], S0, C=C, o=o, S_T=S_T,
+                       stream=stream)
+
+    ms_d = timed(run_dec, max(5, args.steps // 5), max(2, args.warmup // 5), stream)
+    ms_t = timed(run_tied, max(5, args.steps // 5), max(2, args.warmup // 5), stream)
+    flops = dec_flops_per_chunk_head(C, m, n) * B * H * (T // C)
+    out = {"mode": "dec", "workload": "decoupled_bf16_b8h16_t4k_c32", "B": B, "H": H, "T": T, "m": m, "n": n,
+           "C": C, "ms_decoupled": round(ms_d, 4), "ms_tied_same_C": round(ms_t, 4),
+           "tokens_per_s_decoupled": round(B * T / (ms_d / 1e3), 1),
+           "useful_tflops": round(flops / (ms_d / 1e3) / 1e12, 2),
+           "frac_bf16_mfma_peak": round(flops / (ms_d / 1e3) / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
+           "kernel_hash_fp32_path": bwd_hash()}
+    print(json.dumps(out), flush=True)
+
+
 def bwd_hash() -> str:
     h = hashlib.sha256()
     for p in ("paper_2607_11897_amd/csrc/sfda_chunk.hip", "paper_2607_11897_amd/csrc/sfda_chunk_grad.hip",
@@ -392,7 +439,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--only", choices=["chunk", "decode"], default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=["bench", "copy", "rmw", "long", "gated", "bwd"], default="bench")
+    ap.add_argument("--mode", choices=["bench", "copy", "rmw", "long", "gated", "bwd", "dec"], default="bench")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported. The (batch, head) "
@@ -420,6 +467,9 @@ def main():
         return
     if args.mode == "bwd":
         backward(args)
+        return
+    if args.mode == "dec":
+        decoupled(args)
         return
     stream = torch.cuda.current_stream()
     out = {}

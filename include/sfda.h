@@ -131,6 +131,26 @@ sfda_status_t sfda_chunk_fwd_gated(const void* q, const void* k_raw, const void*
                                    sfda_stream_t stream);
 
 /*
+ * sfda_chunk_fwd_decoupled -- the write-decoupled variant (Sec. 3, write-decoupled
+ * variant): the erase direction and strength are separate from the write direction and
+ * strength,
+ *   S_t = (I - eta_t k_t k_t^*) Lambda_t S_{t-1} + beta_t r_t v_t^*,   o_t = S_t^* q_t,
+ * evaluated chunk by chunk (the erase rows solve a unit lower-triangular system in the
+ * k-k Gram block, the write rows are known; outputs and the state update add the q-r and
+ * r-state products).  r = k with eta = beta gives sfda_chunk_fwd's result.
+ *   r   : [B,H,T,m] complex write directions (device, in_dtype).
+ *   eta : [B,H,T] erase strengths; beta : [B,H,T] write strengths (device, in_dtype).
+ *   Other arguments and errors as sfda_chunk_fwd, except C in {16, 32} (SFDA_ERR_CHUNK for
+ *   64: the chunk's operands with R / G and the extra Gram block exceed one CU's LDS).
+ */
+sfda_status_t sfda_chunk_fwd_decoupled(const void* q, const void* k, const void* r, const void* v,
+                                       const void* alpha, const void* theta, const void* eta,
+                                       const void* beta, const float* S0, void* o, float* S_T,
+                                       int B, int H, int T, int m, int n, int C,
+                                       sfda_dtype_t in_dtype, sfda_dtype_t out_dtype,
+                                       sfda_stream_t stream);
+
+/*
  * sfda_chunk_fwd_segmented -- sfda_chunk_fwd with each head's sequence cut into G
  * segments of T / G tokens that are scanned in parallel (for few heads over long
  * sequences, where one workgroup per head leaves most of the GPU idle).  It uses the

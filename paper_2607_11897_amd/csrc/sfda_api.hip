@@ -147,6 +147,41 @@ sfda_status_t sfda_chunk_fwd_gated(const void* q, const void* k_raw, const void*
                           stream, slice, nullptr, 0, false, &gp);
 }
 
+sfda_status_t sfda_chunk_fwd_decoupled(const void* q, const void* k, const void* r, const void* v,
+                                       const void* alpha, const void* theta, const void* eta,
+                                       const void* beta, const float* S0, void* o, float* S_T,
+                                       int B, int H, int T, int m, int n, int C,
+                                       sfda_dtype_t in_dtype, sfda_dtype_t out_dtype,
+                                       sfda_stream_t stream)
+{
+    const int slice = n <= 64 ? ((n + 7) / 8) * 8 : 64;
+    // the shared checks, with the erase strengths in beta's place
+    const sfda_status_t st0 = chunk_fwd_impl(q, k, v, alpha, theta, eta, S0, o, S_T, B, H, T, m, n,
+                                             C, in_dtype, out_dtype, stream, slice, nullptr, 0,
+                                             /*check_only=*/true);
+    if (st0 != SFDA_OK) return st0;
+    if (C == 64) return SFDA_ERR_CHUNK;        // C = 16 or 32 (the kernel's LDS budget)
+    const long BH = static_cast<long>(B) * H;
+    if (BH == 0) return SFDA_OK;
+    if (T > 0 && (!r || !beta)) return SFDA_ERR_NULL;
+    if ((r && !aligned16(r)) || (beta && !aligned16(beta))) return SFDA_ERR_ALIGN;
+    const long ei = esize(in_dtype), eo = esize(out_dtype), BHT = BH * T;
+    const Range rr = range_of(r, BHT * m * 2 * ei), rb = range_of(beta, BHT * ei);
+    if (T > 0 && (overlap(range_of(o, BHT * n * 2 * eo), rr) || overlap(range_of(o, BHT * n * 2 * eo), rb)))
+        return SFDA_ERR_ALIAS;
+    if (S_T && T > 0 && (overlap(range_of(S_T, BH * m * n * 2 * 4), rr) || overlap(range_of(S_T, BH * m * n * 2 * 4), rb)))
+        return SFDA_ERR_ALIAS;
+    sfda::ChunkLaunch L;
+    L.q = q; L.k = k; L.v = v; L.alpha = alpha; L.theta = theta; L.beta = eta;
+    L.r = r; L.wbeta = beta;
+    L.S0 = S0; L.o = o; L.S_T = S_T;
+    L.B = B; L.H = H; L.T = T; L.m = m; L.n = n; L.C = C; L.slice = slice;
+    L.in_bf16 = in_dtype == SFDA_BF16;
+    L.out_bf16 = out_dtype == SFDA_BF16;
+    const hipError_t e = sfda::launch_chunk_decoupled(L, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? SFDA_OK : SFDA_ERR_HIP;
+}
+
 size_t sfda_chunk_fwd_segmented_workspace_bytes(int B, int H, int m, int n, int G)
 {
     if (B <= 0 || H <= 0 || m < 1 || m > 64 || n < 1 || G < 1) return 0;

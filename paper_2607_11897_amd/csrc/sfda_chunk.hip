@@ -180,11 +180,12 @@ __device__ __forceinline__ void adjoint_chunk(ChunkSmem<C>& sm, const ChunkArgs&
     }
 }
 
-// MODE 0: the forward.  MODE 1: the forward recording, per chunk, the state entering it
-// (ck_state) and Delta (ck_rows), for the backward.  MODE 2: the adjoint scan of the
+// MODE 0: the forward.  MODE 3: the write-decoupled forward (below).  MODE 1: the forward
+// recording, per chunk, the state entering it (ck_state) and Delta (ck_rows), for the
+// backward.  MODE 2: the adjoint scan of the
 // backward, chunks in reverse order (below).
-template <int P, typename TIN, typename TOUT, int C, bool GATED, int MODE>
-__device__ __forceinline__ void chunk_scan(ChunkSmem<C>& sm, const ChunkArgs& args, unsigned block)
+template <int P, typename TIN, typename TOUT, int C, bool GATED, int MODE, typename SM = ChunkSmem<C>>
+__device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsigned block)
 {
     constexpr int NRB = C / 16;          // 16-token blocks per chunk
     constexpr int SEG = C / 4;           // tokens per thread in the cumulative sums
@@ -239,7 +240,7 @@ __device__ __forceinline__ void chunk_scan(ChunkSmem<C>& sm, const ChunkArgs& ar
     for (int it_ch = 0; it_ch < nchunks; ++it_ch) {
         const int ch = MODE == 2 ? nchunks - 1 - it_ch : it_ch;
         const int t0 = ch * C;
-        if constexpr (MODE != 0) {
+        if constexpr (MODE == 1 || MODE == 2) {
             // this wave's share of the chunk's [m][n] record: the state entering it (MODE 1)
             // or the adjoint of the state leaving it (MODE 2)
             const long base = (bh * nchunks + ch) * static_cast<long>(m) * n;
@@ -283,12 +284,13 @@ __device__ __forceinline__ void chunk_scan(ChunkSmem<C>& sm, const ChunkArgs& ar
         }
         {
             float2 gkeep[SEG];
-            stage_load<TIN, C, GATED>(sm, args, bh, t0, tid, gkeep);
+            stage_load<TIN, C, GATED, false, MODE == 3>(sm, args, bh, t0, tid, gkeep);
         }
         __syncthreads();
 
         // ============================================================ G: L' and A
         stage_gram<P, C, true>(sm, tid);
+        if constexpr (MODE == 3) stage_gram<P, C, true, true>(sm, tid);   // L'_kr, A_qr
         __syncthreads();
 
         // ============================================================ S: N = (I + D_beta L')^{-1}
@@ -401,6 +403,7 @@ __device__ __forceinline__ void chunk_scan(ChunkSmem<C>& sm, const ChunkArgs& ar
             return a;
         };
         f32x4 D[CBW][NRB];
+        Frag8 bvr[CBW][NRB];     // MODE 3: the write rows Delta_r = D_beta conj(V), K = token
         {
             Frag8 bv[CBW][NRB];
 #pragma unroll
@@ -410,6 +413,44 @@ __device__ __forceinline__ void chunk_scan(ChunkSmem<C>& sm, const ChunkArgs& ar
 #pragma unroll
                     for (int r = 0; r < 4; ++r)
                         bpair(bv[w][kb], r, vf[w][kb][r].x, -vf[w][kb][r].y, qp);   // conj(v)
+            if constexpr (MODE == 3) {
+                // Delta_r, then Y = L'_kr Delta_r takes conj(V)'s place: U' = T Y
+#pragma unroll
+                for (int w = 0; w < CBW; ++w)
+#pragma unroll
+                    for (int kb = 0; kb < NRB; ++kb)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const float bw = sm.wb[kb * 16 + 4 * g + r];
+                            bpair(bvr[w][kb], r, bw * vf[w][kb][r].x, -bw * vf[w][kb][r].y, qp);
+                        }
+                f32x4 yacc[CBW][NRB];
+#pragma unroll
+                for (int w = 0; w < CBW; ++w)
+#pragma unroll
+                    for (int rb = 0; rb < NRB; ++rb) yacc[w][rb] = zero4();
+#pragma unroll
+                for (int rb = 0; rb < NRB; ++rb)
+#pragma unroll
+                    for (int kb = 0; kb <= rb; ++kb) {
+                        Frag8 a;
+                        const int row = rb * 16 + c;
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const int jt = kb * 16 + 4 * g + r;
+                            const float2 x = masked(jt < row, pin(sm.g3[row * LDG + jt]));   // L'_kr
+                            a.v[2 * r] = x.x;
+                            a.v[2 * r + 1] = x.y;
+                        }
+#pragma unroll
+                        for (int w = 0; w < CBW; ++w)
+                            if (wave + 4 * w < ncb) mma<P>(yacc[w][rb], a, bvr[w][kb]);
+                    }
+#pragma unroll
+                for (int w = 0; w < CBW; ++w)
+#pragma unroll
+                    for (int kb = 0; kb < NRB; ++kb) bv[w][kb] = bfrag_from_acc(yacc[w][kb], qp);
+            }
 #pragma unroll
             for (int w = 0; w < CBW; ++w)
 #pragma unroll
@@ -489,7 +530,10 @@ __device__ __forceinline__ void chunk_scan(ChunkSmem<C>& sm, const ChunkArgs& ar
                     }
                     mma<P>(pw, a, sb[kb]);
                 }
-                D[w][rb] = D[w][rb] - pw;
+                if constexpr (MODE == 3)
+                    D[w][rb] = -D[w][rb] - pw;            // Delta_k = -(U' + Wt S)
+                else
+                    D[w][rb] = D[w][rb] - pw;
                 if constexpr (MODE == 1) {
                     if (j < n) {
 #pragma unroll
@@ -505,7 +549,7 @@ __device__ __forceinline__ void chunk_scan(ChunkSmem<C>& sm, const ChunkArgs& ar
             for (int rb = 0; rb < NRB; ++rb) db[rb] = bfrag_from_acc(D[w][rb], qp);
             // O^* = conj(Q)G S + tril(A) Delta ; o = conj(O^*)   (not needed for the record)
 #pragma unroll
-            for (int rb = 0; rb < (MODE == 0 ? NRB : 0); ++rb) {
+            for (int rb = 0; rb < (MODE == 0 || MODE == 3 ? NRB : 0); ++rb) {
                 f32x4 acc = zero4();
                 const int row = rb * 16 + c;
 #pragma unroll
@@ -533,6 +577,18 @@ __device__ __forceinline__ void chunk_scan(ChunkSmem<C>& sm, const ChunkArgs& ar
                         a.v[2 * r + 1] = x.y;
                     }
                     mma<P>(acc, a, db[jb]);
+                    if constexpr (MODE == 3) {            // + A_qr Delta_r
+                        Frag8 a3;
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const int jt = jb * 16 + 4 * g + r;
+                            const float2 lo_p = pin(sm.g3[jt * LDG + row]), dg_p = pin(sm.g3[row * LDG + row]);
+                            const float2 x = masked(jt <= row, jt < row ? lo_p : dg_p);
+                            a3.v[2 * r] = x.x;
+                            a3.v[2 * r + 1] = x.y;
+                        }
+                        mma<P>(acc, a3, bvr[w][jb]);
+                    }
                 }
                 if (j < n && go != nullptr) {     // o == NULL: no output
 #pragma unroll
@@ -566,6 +622,16 @@ __device__ __forceinline__ void chunk_scan(ChunkSmem<C>& sm, const ChunkArgs& ar
                         a.v[2 * r + 1] = x.x * gcr.y + x.y * gcr.x;
                     }
                     mma<P>(Sacc[w][kb], a, db[tb]);
+                    if constexpr (MODE == 3) {            // + diag(g_C) (R/G)^T Delta_r
+                        Frag8 a3;
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const float2 x = sm.ri[(tb * 16 + 4 * g + r) * LDX + irow];
+                            a3.v[2 * r] = x.x * gcr.x - x.y * gcr.y;
+                            a3.v[2 * r + 1] = x.x * gcr.y + x.y * gcr.x;
+                        }
+                        mma<P>(Sacc[w][kb], a3, bvr[w][tb]);
+                    }
                 }
             }
         }
@@ -593,8 +659,9 @@ __device__ __forceinline__ void chunk_scan(ChunkSmem<C>& sm, const ChunkArgs& ar
 template <int P, typename TIN, typename TOUT, int C, bool GATED, int MODE>
 __global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
 {
-    __shared__ ChunkSmem<C> sm;
-    chunk_scan<P, TIN, TOUT, C, GATED, MODE>(sm, args, blockIdx.x);
+    using SM = std::conditional_t<MODE == 3, ChunkSmemDec<C>, ChunkSmem<C>>;
+    __shared__ SM sm;
+    chunk_scan<P, TIN, TOUT, C, GATED, MODE, SM>(sm, args, blockIdx.x);
 }
 
 // The backward's two scans in one launch: the first nfwd workgroups run the recording
@@ -619,6 +686,7 @@ static ChunkArgs make_args(const ChunkLaunch& L)
     a.n_slices = (L.n + L.slice - 1) / L.slice;
     a.amin = L.alpha_min; a.aspan = L.alpha_max - L.alpha_min; a.tmax = L.theta_max; a.eps = L.eps;
     a.ck_state = L.ck_state; a.ck_rows = L.ck_rows; a.dO = L.dO; a.dv = L.dv;
+    a.r = L.r; a.wbeta = L.wbeta;
     return a;
 }
 
@@ -645,6 +713,28 @@ hipError_t launch_chunk(const ChunkLaunch& L, hipStream_t st)
     if (L.in_bf16) return launch_chunk_bf16(L, st);
     return L.out_bf16 ? launch_chunk_t<PREC_F32, float, uint16_t>(L, st)
                       : launch_chunk_t<PREC_F32, float, float>(L, st);
+}
+
+template <int P, typename TIN, typename TOUT>
+static hipError_t launch_dec_t(const ChunkLaunch& L, hipStream_t st)
+{
+    const ChunkArgs a = make_args(L);
+    const dim3 grid(static_cast<unsigned>(static_cast<long>(L.B) * L.H * a.n_slices));
+    switch (L.C) {
+        case 16: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 16, false, 3>), grid, dim3(NTHR), 0, st, a); break;
+        case 32: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 32, false, 3>), grid, dim3(NTHR), 0, st, a); break;
+        default: return hipErrorInvalidValue;       // C = 64 needs more LDS than a CU has
+    }
+    return hipGetLastError();
+}
+
+// the write-decoupled forward; bf16 inputs take bf16 matrix-core operands
+hipError_t launch_chunk_decoupled(const ChunkLaunch& L, hipStream_t st)
+{
+    if (L.in_bf16)
+        return L.out_bf16 ? launch_dec_t<PREC_BF16, uint16_t, uint16_t>(L, st)
+                          : launch_dec_t<PREC_BF16, uint16_t, float>(L, st);
+    return L.out_bf16 ? launch_dec_t<PREC_F32, float, uint16_t>(L, st) : launch_dec_t<PREC_F32, float, float>(L, st);
 }
 
 // bf16 inputs take bf16 matrix-core operands (fp32 accumulation, fp32 state and records)

@@ -34,6 +34,10 @@ struct ChunkArgs {
     float* ck_rows;
     const void* dO;      // adjoint scan: dL/do, o's dtype
     void* dv;            // adjoint scan: dL/dv, the inputs' dtype
+    // write-decoupled forward: write directions r [B,H,T,m] complex and write strengths
+    // [B,H,T] (beta then holds the erase strengths eta)
+    const void* r;
+    const void* wbeta;
 };
 
 __device__ __forceinline__ float sigmoid_acc(float x) { return 1.f / (1.f + expf(-x)); }
@@ -51,13 +55,23 @@ struct ChunkSmem {
     float segp[4][MP];
 };
 
+// the write-decoupled forward also keeps R / G, the k-r and q-r Gram blocks and the write
+// strengths
+template <int C>
+struct ChunkSmemDec : ChunkSmem<C> {
+    float2 ri[C * LDX];                      // r_t / g_t
+    float2 g3[C * ChunkSmem<C>::LDG];        // packed: L'_kr (strict lower), A_qr^T (strict upper), A_qr diag
+    float wb[C];                             // write strengths beta_t
+};
+
 // ----------------------------------------------------------------- load stage
 // Thread (channel i = tid % 64, segment tid / 64) walks C / 4 consecutive tokens of the
 // chunk starting at t0: running sums of log alpha and theta give g_t; the decay-scaled
 // operands go to LDS.  Padding past T (and channels past m) are identity tokens.  With
-// KEEP, g_t of the thread's tokens is returned in gkeep.
-template <typename TIN, int C, bool GATED, bool KEEP = false>
-__device__ __forceinline__ void stage_load(ChunkSmem<C>& sm, const ChunkArgs& args, long bh,
+// KEEP, g_t of the thread's tokens is returned in gkeep; with DEC (SM = ChunkSmemDec) the
+// write directions become R / G and the write strengths are loaded too.
+template <typename TIN, int C, bool GATED, bool KEEP = false, bool DEC = false, typename SM = ChunkSmem<C>>
+__device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long bh,
                                            int t0, int tid, float2 (&gkeep)[C / 4])
 {
     constexpr int SEG = C / 4;
@@ -97,6 +111,10 @@ __device__ __forceinline__ void stage_load(ChunkSmem<C>& sm, const ChunkArgs& ar
         float bv = Elem<TIN>::load(gb, bh * static_cast<long>(T) + min(tb, T - 1));
         if constexpr (GATED) bv = sigmoid_acc(bv);
         if (tid < C) sm.beta[tid] = masked(tb < T, bv);
+        if constexpr (DEC) {
+            const float wv = Elem<TIN>::load(static_cast<const TIN*>(args.wbeta), bh * static_cast<long>(T) + min(tb, T - 1));
+            if (tid < C) sm.wb[tid] = masked(tb < T, wv);
+        }
     }
     __syncthreads();
     float oa = 0.f, op = 0.f;
@@ -135,6 +153,10 @@ __device__ __forceinline__ void stage_load(ChunkSmem<C>& sm, const ChunkArgs& ar
         sm.qg[tl * LDX + i] = make_float2(qq.x * gr + qq.y * gi, qq.x * gi - qq.y * gr);
         sm.kg[tl * LDX + i] = make_float2(kk.x * gr + kk.y * gi, kk.x * gi - kk.y * gr);
         sm.ki[tl * LDX + i] = make_float2(kk.x * hr - kk.y * hi, kk.x * hi + kk.y * hr);
+        if constexpr (DEC) {
+            const float2 rr = masked(ok, Elem<TIN>::load2(static_cast<const TIN*>(args.r), e2));
+            sm.ri[tl * LDX + i] = make_float2(rr.x * hr - rr.y * hi, rr.x * hi + rr.y * hr);
+        }
         if (tl == C - 1) sm.gc[i] = make_float2(gr, gi);
     }
 }
@@ -142,8 +164,10 @@ __device__ __forceinline__ void stage_load(ChunkSmem<C>& sm, const ChunkArgs& ar
 // ----------------------------------------------------------------- gram stage
 // L' (strict lower, at g2[t][j]) and, with WANT_A, A (A[r][j] for j < r at g2[j][r], the
 // diagonal at g2[r][r]).  Reads qg, kg, ki; the caller synchronises before and after.
-template <int P, int C, bool WANT_A>
-__device__ __forceinline__ void stage_gram(ChunkSmem<C>& sm, int tid)
+// With ROP (SM = ChunkSmemDec) the right operand is R / G instead of K / G and the blocks
+// (L'_kr, A_qr) go to g3.
+template <int P, int C, bool WANT_A, bool ROP = false, typename SM = ChunkSmem<C>>
+__device__ __forceinline__ void stage_gram(SM& sm, int tid)
 {
     constexpr int NRB = C / 16;
     constexpr int LDG = ChunkSmem<C>::LDG;
@@ -151,7 +175,15 @@ __device__ __forceinline__ void stage_gram(ChunkSmem<C>& sm, int tid)
     constexpr int NT1 = NRB * (NRB + 1);             // causal tiles per matrix
     const int lane = tid & 63, wave = tid >> 6;
     const int c = lane & 15, g = lane >> 4, qp = lane & 1;
-    float* g2f = reinterpret_cast<float*>(sm.g2);
+    float* g2f;
+    const float2* Yop;
+    if constexpr (ROP) {
+        g2f = reinterpret_cast<float*>(sm.g3);
+        Yop = sm.ri;
+    } else {
+        g2f = reinterpret_cast<float*>(sm.g2);
+        Yop = sm.ki;
+    }
     for (int tile = wave; tile < (WANT_A ? 2 : 1) * NT1; tile += 4) {
         const int mat = tile / NT1;                  // 0: L' from conj(K)G, 1: A from conj(Q)G
         int rem = tile - mat * NT1, rb = 0;
@@ -170,7 +202,7 @@ __device__ __forceinline__ void stage_gram(ChunkSmem<C>& sm, int tid)
                 const float2 x = X[row * LDX + i];
                 a.v[2 * r] = x.x;
                 a.v[2 * r + 1] = x.y;
-                const float2 y = sm.ki[jcol * LDX + i];   // B(i, j) = (K/G)^T
+                const float2 y = Yop[jcol * LDX + i];     // B(i, j) = (K/G)^T (or (R/G)^T)
                 bpair(b, r, y.x, y.y, qp);
             }
             mma<P>(acc, a, b);

@@ -35,6 +35,10 @@ struct ChunkLaunch {
     float* ck_rows = nullptr;
     const void* dO = nullptr;
     void* dv = nullptr;
+    // write-decoupled forward (launch_chunk_decoupled): write directions r and write
+    // strengths wbeta; beta holds the erase strengths
+    const void* r = nullptr;
+    const void* wbeta = nullptr;
 };
 
 // per-chunk gradient pass of the backward (one workgroup per head and chunk)
@@ -56,6 +60,7 @@ struct GateParams {
 hipError_t launch_step(const StepLaunch& L, hipStream_t st);
 hipError_t launch_chunk(const ChunkLaunch& L, hipStream_t st);
 hipError_t launch_chunk_bf16(const ChunkLaunch& L, hipStream_t st);   // bf16 inputs
+hipError_t launch_chunk_decoupled(const ChunkLaunch& L, hipStream_t st);   // C = 16 or 32
 // backward: the forward scan recording states and Delta (F; none when F.T == 0) and the
 // reverse adjoint scan (A) in one launch, then the per-chunk gradient pass
 hipError_t launch_bwd_scans(const ChunkLaunch& F, const ChunkLaunch& A, hipStream_t st);

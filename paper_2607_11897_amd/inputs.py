@@ -294,6 +294,73 @@ def make_chunk_inputs(w: Workload, T: Optional[int] = None, B: Optional[int] = N
                        stack(6, "f32"), w.dtype)
 
 
+@dataclasses.dataclass
+class DecoupledInputs:
+    """Stored inputs of one write-decoupled forward call, as exact float64/complex128
+    values.  q, k, r: [B,H,T,m] complex; v: [B,H,T,n] complex; alpha, theta: [B,H,T,m];
+    eta, beta: [B,H,T]; S0: [B,H,m,n] complex or None."""
+    q: np.ndarray
+    k: np.ndarray
+    r: np.ndarray
+    v: np.ndarray
+    alpha: np.ndarray
+    theta: np.ndarray
+    eta: np.ndarray
+    beta: np.ndarray
+    S0: Optional[np.ndarray]
+    dtype: str
+
+    @property
+    def shape(self):
+        B, H, T, m = self.q.shape
+        return B, H, T, m, self.v.shape[-1]
+
+    def storage(self) -> dict:
+        d = {name: to_storage(getattr(self, name), self.dtype)
+             for name in ("q", "k", "r", "v", "alpha", "theta", "eta", "beta")}
+        d["S0"] = None if self.S0 is None else to_storage(self.S0, "f32")
+        return d
+
+    def head(self, b: int, h: int) -> "DecoupledInputs":
+        sl = (slice(b, b + 1), slice(h, h + 1))
+        return DecoupledInputs(self.q[sl], self.k[sl], self.r[sl], self.v[sl], self.alpha[sl],
+                               self.theta[sl], self.eta[sl], self.beta[sl],
+                               None if self.S0 is None else self.S0[sl], self.dtype)
+
+
+def make_decoupled_inputs(B: int, H: int, T: int, m: int, n: int, dtype: str, seed: int,
+                          laws: Laws = None, heads: Optional[Sequence] = None) -> DecoupledInputs:
+    """Seeded write-decoupled inputs with the laws of the main workloads (default: those of
+    the benchmarked shape): q, v ~ CN(0, 1), k and r ~ CN(0, 1) normalised, alpha and theta
+    by the laws, eta ~ U(0, 1) (erase strengths), beta by the law (write strengths), S0 by
+    the law; per head from PCG64 streams seeded (seed, b, h, 2), drawn in the order q, k,
+    r, v, alpha, theta, eta, beta, S0; rounded to the storage dtype."""
+    laws = LAWS_MAIN if laws is None else laws
+    pairs = [(b, h) for b in range(B) for h in range(H)] if heads is None else list(heads)
+    shape_bh = (B, H) if heads is None else (1, len(pairs))
+    cols = {name: [] for name in ("q", "k", "r", "v", "alpha", "theta", "eta", "beta", "S0")}
+    for (b, h) in pairs:
+        rng = np.random.Generator(np.random.PCG64([seed, b, h, 2]))
+        cols["q"].append(_cn(rng, (T, m)))
+        cols["k"].append(_normalise_keys(_cn(rng, (T, m))))
+        cols["r"].append(_normalise_keys(_cn(rng, (T, m))))
+        cols["v"].append(_cn(rng, (T, n)))
+        cols["alpha"].append(_alpha(rng, laws.alpha, (T, m)))
+        cols["theta"].append(_theta(rng, laws.theta, (T, m)))
+        cols["eta"].append(rng.uniform(0.0, 1.0, (T,)))
+        cols["beta"].append(rng.uniform(laws.beta[1], laws.beta[2], (T,)))
+        cols["S0"].append(None if laws.s0_scale is None else laws.s0_scale * _cn(rng, (m, n)))
+
+    def stack(name, dtype):
+        if cols[name][0] is None:
+            return None
+        a = np.stack(cols[name])
+        return round_to_storage(a.reshape(shape_bh + a.shape[1:]), dtype)
+
+    return DecoupledInputs(*(stack(nm, dtype) for nm in ("q", "k", "r", "v", "alpha", "theta", "eta", "beta")),
+                           stack("S0", "f32"), dtype)
+
+
 def make_cotangents(B: int, H: int, T: int, m: int, n: int, out_dtype: str, seed: int,
                     dS_scale: Optional[float] = 1.0, heads: Optional[Sequence] = None):
     """Seeded upstream gradients for the backward: dO = dL/do [B,H,T,n] ~ CN(0, 1) rounded

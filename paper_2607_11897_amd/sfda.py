@@ -17,7 +17,8 @@ LIB_PATH = os.path.join(HERE, "libsfda.so")
 SFDA_F32, SFDA_BF16 = 0, 1
 STATUS = {0: "SFDA_OK", 1: "SFDA_ERR_NULL", 2: "SFDA_ERR_SHAPE", 3: "SFDA_ERR_CHUNK",
           4: "SFDA_ERR_DTYPE", 5: "SFDA_ERR_ALIGN", 6: "SFDA_ERR_ALIAS", 7: "SFDA_ERR_HIP"}
-EXPORTS = ("sfda_chunk_fwd", "sfda_chunk_fwd_sliced", "sfda_chunk_fwd_gated", "sfda_chunk_fwd_segmented",
+EXPORTS = ("sfda_chunk_fwd", "sfda_chunk_fwd_sliced", "sfda_chunk_fwd_gated", "sfda_chunk_fwd_decoupled",
+           "sfda_chunk_fwd_segmented",
            "sfda_chunk_fwd_segmented_workspace_bytes", "sfda_chunk_bwd", "sfda_chunk_bwd_workspace_bytes",
            "sfda_step", "sfda_status_string", "sfda_abi_version")
 
@@ -48,6 +49,8 @@ def load_library(path: str = LIB_PATH):
     f = ctypes.c_float
     lib.sfda_chunk_fwd_gated.argtypes = [vp] * 9 + [i] * 6 + [f] * 4 + [i, i, vp]
     lib.sfda_chunk_fwd_gated.restype = i
+    lib.sfda_chunk_fwd_decoupled.argtypes = [vp] * 11 + [i] * 6 + [i, i, vp]
+    lib.sfda_chunk_fwd_decoupled.restype = i
     lib.sfda_chunk_fwd_segmented.argtypes = [vp] * 9 + [i] * 7 + [i, i, vp, ctypes.c_size_t, vp]
     lib.sfda_chunk_fwd_segmented.restype = i
     lib.sfda_chunk_fwd_segmented_workspace_bytes.argtypes = [i] * 5
@@ -160,6 +163,34 @@ def chunk_fwd_gated(q, k_raw, v, a, b, c, S0=None, C: int = 64, *, alpha_min: fl
                                   _dtype_code(o), _stream(stream))
     if st != 0:
         raise SfdaError(st, "sfda_chunk_fwd_gated")
+    return o, S_T
+
+
+def chunk_fwd_decoupled(q, k, r, v, alpha, theta, eta, beta, S0=None, C: int = 32, *, o=None,
+                        S_T=None, out_dtype=None, want_state: bool = True, stream=None) -> Tuple:
+    """Write-decoupled forward (sfda_chunk_fwd_decoupled): erase along k with strengths eta
+    [B,H,T], write along r [B,H,T,m,2] with strengths beta [B,H,T]; C 16 or 32.  Shapes and
+    results otherwise as chunk_fwd."""
+    import torch
+    lib = load_library()
+    B, H, T, m, _ = q.shape
+    n = v.shape[3]
+    in_code = _dtype_code(q)
+    for t in (k, r, v, alpha, theta, eta, beta):
+        if t.dtype != q.dtype:
+            raise TypeError("q, k, r, v, alpha, theta, eta, beta must share one dtype")
+    out_dtype = q.dtype if out_dtype is None else out_dtype
+    if o is None:
+        o = torch.empty((B, H, T, n, 2), dtype=out_dtype, device=q.device)
+    if S_T is None and want_state:
+        S_T = torch.empty((B, H, m, n, 2), dtype=torch.float32, device=q.device)
+    if S0 is not None and S0.dtype != torch.float32:
+        raise TypeError("S0 must be float32")
+    st = lib.sfda_chunk_fwd_decoupled(_ptr(q), _ptr(k), _ptr(r), _ptr(v), _ptr(alpha), _ptr(theta), _ptr(eta),
+                                      _ptr(beta), _ptr(S0), _ptr(o), _ptr(S_T), B, H, T, m, n, C, in_code,
+                                      _dtype_code(o), _stream(stream))
+    if st != 0:
+        raise SfdaError(st, "sfda_chunk_fwd_decoupled")
     return o, S_T
 
 

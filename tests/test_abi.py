@@ -180,3 +180,19 @@ def test_bwd_argument_errors(lib):
     p = list(PB)
     p[15] = p[8]
     assert bwd(lib, p) == 6                                    # dS0 over dS_T
+
+
+def test_decoupled_argument_errors(lib):
+    def dec(q=P[0], k=P[1], r=A * 20, v=P[2], a=P[3], th=P[4], eta=P[5], b=A * 21, s0=P[6], o=P[7], st=P[8],
+            B=1, H=1, T=4, m=8, n=8, C=16, din=0, dout=0):
+        return lib.sfda_chunk_fwd_decoupled(q, k, r, v, a, th, eta, b, s0, o, st, B, H, T, m, n, C, din, dout, None)
+    assert dec(B=0) == 0
+    assert dec(C=64) == 3
+    assert dec(C=48) == 3
+    assert dec(r=0) == 1
+    assert dec(b=0) == 1
+    assert dec(eta=0) == 1
+    assert dec(b=A * 21 + 4) == 5
+    assert dec(o=A * 20) == 6          # o over r
+    assert dec(st=A * 21) == 6         # S_T over beta
+    assert dec(m=65) == 2
