@@ -51,10 +51,9 @@ namespace sfda {
 // and dL/dv = conj(G_E).  G_F is recorded per token (ck_rows) for the gradient pass; the
 // caller records G itself before the chunk.  A^* is read from A^T in g2's upper part, N^*
 // from N in its strict lower part.
-template <int P, typename TIN, int C>
+template <int P, typename TIN, typename TOUT, int C>
 __device__ __forceinline__ void adjoint_chunk(ChunkSmem<C>& sm, const ChunkArgs& args,
-                                              f32x4 (&Sacc)[2][MP / 16],
-                                              const float2 (&vf)[2][C / 16][4], long bh, int t0,
+                                              f32x4 (&Sacc)[2][MP / 16], long bh, int t0,
                                               int nchunks, int n0, int ncb, int tid)
 {
     constexpr int NRB = C / 16;
@@ -73,7 +72,13 @@ __device__ __forceinline__ void adjoint_chunk(ChunkSmem<C>& sm, const ChunkArgs&
 #pragma unroll
         for (int kb = 0; kb < NRB; ++kb)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) bpair(br[kb], r, vf[w][kb][r].x, -vf[w][kb][r].y, qp);
+            for (int r = 0; r < 4; ++r) {
+                const int t = t0 + kb * 16 + 4 * g + r;
+                const bool ok = j < n && t < T;
+                const float2 x = masked(ok, Elem<TOUT>::load2(static_cast<const TOUT*>(args.dO),
+                                                              base_tn + static_cast<long>(min(t, T - 1)) * n + min(j, n - 1)));
+                bpair(br[kb], r, x.x, -x.y, qp);
+            }
         Frag8 sb[MP / 16];
 #pragma unroll
         for (int kb = 0; kb < MP / 16; ++kb) sb[kb] = bfrag_from_acc(Sacc[w][kb], qp);
@@ -261,26 +266,25 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
 
         // ============================================================ L: load, g, operands
         // this wave's conj(V) B-fragments for U = T conj(V): v[t0 + kb*16 + 4g + r][col]
-        // (MODE 2: dL/do, whose conjugate is the adjoint of O^*)
+        // (the adjoint scan loads its dL/do fragments itself, where they are used)
         float2 vf[CBW][NRB][4];
+        if constexpr (MODE != 2) {
 #pragma unroll
-        for (int w = 0; w < CBW; ++w) {
-            const int cb = wave + 4 * w;
-            const int j = n0 + cb * 8 + (c >> 1);
+            for (int w = 0; w < CBW; ++w) {
+                const int cb = wave + 4 * w;
+                const int j = n0 + cb * 8 + (c >> 1);
 #pragma unroll
-            for (int kb = 0; kb < NRB; ++kb)
+                for (int kb = 0; kb < NRB; ++kb)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int t = t0 + kb * 16 + 4 * g + r;
-                    const bool ok = cb < ncb && j < n && t < T;
-                    float2 x = make_float2(0.f, 0.f);
-                    const long e = base_tn + static_cast<long>(min(t, T - 1)) * n + min(j, n - 1);
-                    if constexpr (MODE == 2)
-                        x = Elem<TOUT>::load2(static_cast<const TOUT*>(args.dO), e);
-                    else if (gv != nullptr)      // v == NULL reads as zeros (uniform branch)
-                        x = Elem<TIN>::load2(gv, e);
-                    vf[w][kb][r] = masked(ok, x);
-                }
+                    for (int r = 0; r < 4; ++r) {
+                        const int t = t0 + kb * 16 + 4 * g + r;
+                        const bool ok = cb < ncb && j < n && t < T;
+                        float2 x = make_float2(0.f, 0.f);
+                        if (gv != nullptr)      // v == NULL reads as zeros (uniform branch)
+                            x = Elem<TIN>::load2(gv, base_tn + static_cast<long>(min(t, T - 1)) * n + min(j, n - 1));
+                        vf[w][kb][r] = masked(ok, x);
+                    }
+            }
         }
         {
             float2 gkeep[SEG];
@@ -381,7 +385,7 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
 
 
         if constexpr (MODE == 2) {
-            adjoint_chunk<P, TIN, C>(sm, args, Sacc, vf, bh, t0, nchunks, n0, ncb, tid);
+            adjoint_chunk<P, TIN, TOUT, C>(sm, args, Sacc, bh, t0, nchunks, n0, ncb, tid);
             __syncthreads();
             continue;
         }
