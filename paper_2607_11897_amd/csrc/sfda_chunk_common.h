@@ -69,11 +69,14 @@ struct ChunkSmemDec : ChunkSmem<C> {
 // chunk starting at t0: running sums of log alpha and theta give g_t; the decay-scaled
 // operands go to LDS.  Padding past T (and channels past m) are identity tokens.  With
 // KEEP, g_t of the thread's tokens is returned in gkeep; with DEC (SM = ChunkSmemDec) the
-// write directions become R / G and the write strengths are loaded too.
-template <typename TIN, int C, bool GATED, bool KEEP = false, bool DEC = false, typename SM = ChunkSmem<C>>
+// write directions become R / G and the write strengths are loaded too.  In a block wider
+// than 256 threads (WIDE) only the first 256 work; every thread passes the barrier.
+template <typename TIN, int C, bool GATED, bool KEEP = false, bool DEC = false, typename SM = ChunkSmem<C>,
+          bool WIDE = false>
 __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long bh,
                                            int t0, int tid, float2 (&gkeep)[C / 4])
 {
+    const bool worker = !WIDE || tid < NTHR;
     constexpr int SEG = C / 4;
     const TIN* __restrict__ gq = static_cast<const TIN*>(args.q);
     const TIN* __restrict__ gk = static_cast<const TIN*>(args.k);
@@ -84,9 +87,10 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
     const long base_tm = bh * static_cast<long>(T) * m;
 
     const int i = tid & 63;
-    const int seg = tid >> 6;
+    const int seg = (tid >> 6) & 3;
     float la[SEG], ph[SEG];
     float sa = 0.f, sp = 0.f;
+    if (worker) {
 #pragma unroll
     for (int u = 0; u < SEG; ++u) {
         const int t = t0 + seg * SEG + u;
@@ -106,7 +110,8 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
     }
     sm.sega[seg][i] = sa;
     sm.segp[seg][i] = sp;
-    {
+    }
+    if (worker) {
         const int tb = t0 + (tid & (C - 1));
         float bv = Elem<TIN>::load(gb, bh * static_cast<long>(T) + min(tb, T - 1));
         if constexpr (GATED) bv = sigmoid_acc(bv);
@@ -117,6 +122,7 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
         }
     }
     __syncthreads();
+    if (!worker) return;
     float oa = 0.f, op = 0.f;
     for (int s2 = 0; s2 < seg; ++s2) {
         oa += sm.sega[s2][i];
@@ -166,7 +172,7 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
 // diagonal at g2[r][r]).  Reads qg, kg, ki; the caller synchronises before and after.
 // With ROP (SM = ChunkSmemDec) the right operand is R / G instead of K / G and the blocks
 // (L'_kr, A_qr) go to g3.
-template <int P, int C, bool WANT_A, bool ROP = false, typename SM = ChunkSmem<C>>
+template <int P, int C, bool WANT_A, bool ROP = false, typename SM = ChunkSmem<C>, int NW = 4>
 __device__ __forceinline__ void stage_gram(SM& sm, int tid)
 {
     constexpr int NRB = C / 16;
@@ -184,7 +190,7 @@ __device__ __forceinline__ void stage_gram(SM& sm, int tid)
         g2f = reinterpret_cast<float*>(sm.g2);
         Yop = sm.ki;
     }
-    for (int tile = wave; tile < (WANT_A ? 2 : 1) * NT1; tile += 4) {
+    for (int tile = wave; tile < (WANT_A ? 2 : 1) * NT1; tile += NW) {
         const int mat = tile / NT1;                  // 0: L' from conj(K)G, 1: A from conj(Q)G
         int rem = tile - mat * NT1, rb = 0;
         while (rem >= min(NCB, 2 * rb + 2)) { rem -= min(NCB, 2 * rb + 2); ++rb; }

@@ -31,6 +31,8 @@
 
 namespace sfda {
 
+constexpr int GW = 8;        // waves per workgroup: two per SIMD, to hide the record loads' latency
+
 struct GradArgs {
     ChunkArgs in;                          // q, k, v, alpha, theta, beta, T, m, n
     const void* dO;
@@ -39,7 +41,7 @@ struct GradArgs {
 };
 
 template <int P, typename TIN, typename TOUT, int C>
-__global__ __launch_bounds__(NTHR, 1) void grad_kernel(GradArgs A)
+__global__ __launch_bounds__(GW * 64, 1) void grad_kernel(GradArgs A)
 {
     constexpr int NRB = C / 16;
     constexpr int SEG = C / 4;
@@ -47,7 +49,7 @@ __global__ __launch_bounds__(NTHR, 1) void grad_kernel(GradArgs A)
     constexpr int NCT = NRB * (2 * MP / 16);        // C x m output tiles (16 tokens x 8 channels)
     constexpr int NT1 = NRB * (NRB + 1);            // causal tiles of a C x C matrix
     __shared__ ChunkSmem<C> sm;
-    __shared__ float dbeta_part[4][C];              // per-wave shares of dbeta
+    __shared__ float dbeta_part[GW][C];             // per-wave shares of dbeta
     __shared__ float ggc[2 * MP];                   // dL/dg_C (complex)
 
     const ChunkArgs& args = A.in;
@@ -131,47 +133,52 @@ __global__ __launch_bounds__(NTHR, 1) void grad_kernel(GradArgs A)
         }
     };
 
-    float2 gkeep[SEG];
-    stage_load<TIN, C, false, true>(sm, args, bh, t0, tid, gkeep);
-    // dL/dg_C, first part: sum over columns of G * conj(S), one state row per 4 threads
+    // (the load stage and the elementwise stage work on the first 256 threads; the latter
+    // forms g again rather than holding it in registers through the whole kernel)
     {
-        const int i = tid >> 2, part = tid & 3;
+        float2 gkeep[SEG];
+        stage_load<TIN, C, false, false, false, ChunkSmem<C>, true>(sm, args, bh, t0, tid, gkeep);
+    }
+    // dL/dg_C, first part: sum over columns of G * conj(S), one state row per 8 threads
+    {
+        const int i = tid >> 3, part = tid & 7;
         float2 acc = make_float2(0.f, 0.f);
         for (int c0 = 0; c0 < n; c0 += 64) {
-            float2 gs[16], sv[16];
+            float2 gs[8], sv[8];
 #pragma unroll
-            for (int u = 0; u < 16; ++u) {
-                gs[u] = rec(Grec, i, m, c0 + part + 4 * u);
-                sv[u] = rec(Srec, i, m, c0 + part + 4 * u);
+            for (int u = 0; u < 8; ++u) {
+                gs[u] = rec(Grec, i, m, c0 + part + 8 * u);
+                sv[u] = rec(Srec, i, m, c0 + part + 8 * u);
             }
 #pragma unroll
-            for (int u = 0; u < 16; ++u) {
+            for (int u = 0; u < 8; ++u) {
                 acc.x += gs[u].x * sv[u].x + gs[u].y * sv[u].y;
                 acc.y += gs[u].y * sv[u].x - gs[u].x * sv[u].y;
             }
         }
-        acc.x += __shfl_xor(acc.x, 1);
-        acc.y += __shfl_xor(acc.y, 1);
-        acc.x += __shfl_xor(acc.x, 2);
-        acc.y += __shfl_xor(acc.y, 2);
+#pragma unroll
+        for (int sh = 1; sh < 8; sh <<= 1) {
+            acc.x += __shfl_xor(acc.x, sh);
+            acc.y += __shfl_xor(acc.y, sh);
+        }
         if (part == 0) {
             ggc[2 * i] = acc.x;
             ggc[2 * i + 1] = acc.y;
         }
     }
     __syncthreads();
-    stage_gram<P, C, false>(sm, tid);                 // L'
+    stage_gram<P, C, false, false, ChunkSmem<C>, GW>(sm, tid);   // L'
     __syncthreads();
 
     // ================================================================ H = E - L' Delta, dbeta
-    // (each wave sums its column blocks in registers; the four shares are added in a fixed
-    // order at the end, so no atomics are needed)
+    // (each wave sums its column blocks in registers; the per-wave shares are added in a
+    // fixed order at the end, so no atomics are needed)
     float dacc[NRB][4];
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) dacc[rb][r] = 0.f;
-    for (int cb = wave; cb < ncbn; cb += 4) {
+    for (int cb = wave; cb < ncbn; cb += GW) {
         const int j = cb * 8 + (c >> 1);
         Frag8 sbf[MP / 16];                            // S, K = state row
 #pragma unroll
@@ -255,7 +262,7 @@ __global__ __launch_bounds__(NTHR, 1) void grad_kernel(GradArgs A)
     // ================================================================ G_A, G_L' (into g2)
     {
         float* g2f = reinterpret_cast<float*>(sm.g2);
-        for (int tile = wave; tile < 2 * NT1; tile += 4) {
+        for (int tile = wave; tile < 2 * NT1; tile += GW) {
             const int mat = tile / NT1;                // 0: G_N from G_F, 1: G_A from G_R
             int rem = tile - mat * NT1, rb = 0;
             while (rem >= min(C / 8, 2 * rb + 2)) { rem -= min(C / 8, 2 * rb + 2); ++rb; }
@@ -296,14 +303,14 @@ __global__ __launch_bounds__(NTHR, 1) void grad_kernel(GradArgs A)
     __syncthreads();
 
     // ================================================================ G_Ki, G_Qg, G_Kg
-    // Tile it of wave w covers channel block (w + 4 it) % 8 = w + 4 (it % 2), so the two
-    // channel blocks of a wave collect their dL/dg_C shares in gsum[0], gsum[1].
-    constexpr int PER = (NCT + 3) / 4;
+    // Tile it of wave w covers channel block (w + 8 it) % 8 = w, so each wave collects the
+    // dL/dg_C shares of its channel block in gsum.
+    constexpr int PER = (NCT + GW - 1) / GW;
     f32x4 gki[PER], gqg[PER], gkg[PER];
-    float gsum[2] = {0.f, 0.f};
+    float gsum = 0.f;
 #pragma unroll
     for (int it = 0; it < PER; ++it) {
-        const int tile = wave + 4 * it;
+        const int tile = wave + GW * it;
         gki[it] = zero4(); gqg[it] = zero4(); gkg[it] = zero4();
         if (tile >= NCT) continue;
         const int rb = tile / (2 * MP / 16);
@@ -311,10 +318,10 @@ __global__ __launch_bounds__(NTHR, 1) void grad_kernel(GradArgs A)
         const int row = rb * 16 + c;
         const float btr = sm.beta[row];
         // value-dimension products: conj(Delta) G^T, G_R S^*, -G_E S^*
-        for (int k0 = 0; k0 < nkb; k0 += 4) {             // all loads of four K-blocks first
-            Frag8 ad[4], ar[4], af[4], bg[4], bs[4];
+        for (int k0 = 0; k0 < nkb; k0 += 2) {             // all loads of two K-blocks first
+            Frag8 ad[2], ar[2], af[2], bg[2], bs[2];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < 2; ++u) {
                 const int c0 = (k0 + u) * 16 + 4 * g;
                 float2 d[4], x[4], f[4], y[4], sv[4];
                 rec4(Drow, row, C, c0, d);
@@ -335,7 +342,7 @@ __global__ __launch_bounds__(NTHR, 1) void grad_kernel(GradArgs A)
                 }
             }
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
+            for (int u = 0; u < 2; ++u)
                 if (k0 + u < nkb) {
                     mma<P>(gki[it], ad[u], bg[u]);
                     mma<P>(gqg[it], ar[u], bs[u]);
@@ -353,7 +360,7 @@ __global__ __launch_bounds__(NTHR, 1) void grad_kernel(GradArgs A)
             }
             part += __shfl_xor(part, 16);
             part += __shfl_xor(part, 32);
-            gsum[it & 1] += part;
+            gsum += part;
         }
         // G_Yp diag(conj(g_C))
         {
@@ -395,11 +402,8 @@ __global__ __launch_bounds__(NTHR, 1) void grad_kernel(GradArgs A)
         }
     }
     if (g == 0) {                                      // one owner lane per element of ggc
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
-            const int icol = (wave + 4 * s2) * 8 + (c >> 1);
-            if (icol < m) ggc[2 * icol + qp] += gsum[s2];
-        }
+        const int icol = wave * 8 + (c >> 1);
+        if (icol < m) ggc[2 * icol + qp] += gsum;
     }
     __syncthreads();                                   // every read of qg, kg, ki done
     {
@@ -408,7 +412,7 @@ __global__ __launch_bounds__(NTHR, 1) void grad_kernel(GradArgs A)
         float* kif = reinterpret_cast<float*>(sm.ki);
 #pragma unroll
         for (int it = 0; it < PER; ++it) {
-            const int tile = wave + 4 * it;
+            const int tile = wave + GW * it;
             if (tile >= NCT) continue;
             const int rb = tile / (2 * MP / 16);
             const int icol = (tile - rb * (2 * MP / 16)) * 8 + (c >> 1);
@@ -432,11 +436,51 @@ __global__ __launch_bounds__(NTHR, 1) void grad_kernel(GradArgs A)
         TIN* dk = static_cast<TIN*>(A.dk);
         TIN* dal = static_cast<TIN*>(A.dalpha);
         TIN* dth = static_cast<TIN*>(A.dtheta);
-        const int i = tid & 63, seg = tid >> 6;
+        const int i = tid & 63, seg = (tid >> 6) & 3;
+        const bool worker = tid < NTHR;                // the load stage's thread mapping
+        // g of this thread's tokens: running sums of log alpha and theta over its segment,
+        // offset by the segments before it
+        float2 gkeep[SEG];
+        {
+            const TIN* gth = static_cast<const TIN*>(args.theta);
+            float la[SEG], ph[SEG];
+            float sa = 0.f, sp2 = 0.f;
+#pragma unroll
+            for (int u = 0; u < SEG; ++u) {
+                const int t = t0 + seg * SEG + u;
+                const bool ok = t < T && i < m;
+                const long e = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
+                const float a_ld = pin(Elem<TIN>::load(ga, e));
+                const float th = masked(ok, Elem<TIN>::load(gth, e));
+                sa += __logf(ok ? a_ld : 1.f);
+                sp2 += th;
+                la[u] = sa;
+                ph[u] = sp2;
+            }
+            if (worker) {
+                sm.sega[seg][i] = sa;
+                sm.segp[seg][i] = sp2;
+            }
+            __syncthreads();
+            float oa = 0.f, op2 = 0.f;
+            for (int s2 = 0; s2 < seg; ++s2) {
+                oa += sm.sega[s2][i];
+                op2 += sm.segp[s2][i];
+            }
+#pragma unroll
+            for (int u = 0; u < SEG; ++u) {
+                const float e = __expf(la[u] + oa);
+                float sn, cs;
+                __sincosf(ph[u] + op2, &sn, &cs);
+                gkeep[u] = make_float2(e * cs, e * sn);
+            }
+            __syncthreads();                           // before sega / segp are reused below
+        }
         float gl[SEG], gp[SEG];
         float sl = 0.f, sp = 0.f;
 #pragma unroll
         for (int u = SEG - 1; u >= 0; --u) {
+            if (!worker) break;
             const int tl = seg * SEG + u;
             const int t = t0 + tl;
             const bool ok = t < T && i < m;
@@ -451,7 +495,7 @@ __global__ __launch_bounds__(NTHR, 1) void grad_kernel(GradArgs A)
             const float2 vq = make_float2(gg.x * gqv.x + gg.y * gqv.y, gg.y * gqv.x - gg.x * gqv.y);
             const float2 vk = make_float2(gg.x * gkv.x + gg.y * gkv.y + gi.x * gkiv.x + gi.y * gkiv.y,
                                           gg.y * gkv.x - gg.x * gkv.y + gi.x * gkiv.y - gi.y * gkiv.x);
-            if (ok) {
+            if (ok) {          // (a worker thread)
                 Elem<TIN>::store2(dq, e, vq.x, vq.y);
                 Elem<TIN>::store2(dk, e, vk.x, vk.y);
             }
@@ -472,9 +516,12 @@ __global__ __launch_bounds__(NTHR, 1) void grad_kernel(GradArgs A)
             gl[u] = sl;
             gp[u] = sp;
         }
-        sm.sega[seg][i] = sl;
-        sm.segp[seg][i] = sp;
+        if (worker) {
+            sm.sega[seg][i] = sl;
+            sm.segp[seg][i] = sp;
+        }
         __syncthreads();
+        if (!worker) return;
         float ol = 0.f, op = 0.f;
         for (int s2 = seg + 1; s2 < 4; ++s2) {
             ol += sm.sega[s2][i];
@@ -489,9 +536,12 @@ __global__ __launch_bounds__(NTHR, 1) void grad_kernel(GradArgs A)
                 Elem<TIN>::store(dth, e, gp[u] + op);
             }
         }
-        if (tid < C && t0 + tid < T)
-            Elem<TIN>::store(static_cast<TIN*>(A.dbeta), bh * static_cast<long>(T) + t0 + tid,
-                             ((dbeta_part[0][tid] + dbeta_part[1][tid]) + dbeta_part[2][tid]) + dbeta_part[3][tid]);
+        if (tid < C && t0 + tid < T) {
+            float db = 0.f;
+#pragma unroll
+            for (int w = 0; w < GW; ++w) db += dbeta_part[w][tid];
+            Elem<TIN>::store(static_cast<TIN*>(A.dbeta), bh * static_cast<long>(T) + t0 + tid, db);
+        }
     }
 }
 
@@ -509,9 +559,9 @@ static hipError_t launch_grad_t(const GradLaunch& L, hipStream_t st)
     const long nchunks = (L.T + L.C - 1) / L.C;
     const dim3 grid(static_cast<unsigned>(static_cast<long>(L.B) * L.H * nchunks));
     switch (L.C) {
-        case 16: hipLaunchKernelGGL((grad_kernel<P, TIN, TOUT, 16>), grid, dim3(NTHR), 0, st, a); break;
-        case 32: hipLaunchKernelGGL((grad_kernel<P, TIN, TOUT, 32>), grid, dim3(NTHR), 0, st, a); break;
-        case 64: hipLaunchKernelGGL((grad_kernel<P, TIN, TOUT, 64>), grid, dim3(NTHR), 0, st, a); break;
+        case 16: hipLaunchKernelGGL((grad_kernel<P, TIN, TOUT, 16>), grid, dim3(GW * 64), 0, st, a); break;
+        case 32: hipLaunchKernelGGL((grad_kernel<P, TIN, TOUT, 32>), grid, dim3(GW * 64), 0, st, a); break;
+        case 64: hipLaunchKernelGGL((grad_kernel<P, TIN, TOUT, 64>), grid, dim3(GW * 64), 0, st, a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
