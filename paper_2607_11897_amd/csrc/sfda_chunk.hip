@@ -51,9 +51,9 @@ namespace sfda {
 // and dL/dv = conj(G_E).  G_F is recorded per token (ck_rows) for the gradient pass; the
 // caller records G itself before the chunk.  A^* is read from A^T in g2's upper part, N^*
 // from N in its strict lower part.
-template <int P, typename TIN, typename TOUT, int C>
+template <int P, typename TIN, typename TOUT, int C, int NW>
 __device__ __forceinline__ void adjoint_chunk(ChunkSmem<C>& sm, const ChunkArgs& args,
-                                              f32x4 (&Sacc)[2][MP / 16], long bh, int t0,
+                                              f32x4 (&Sacc)[8 / NW][MP / 16], long bh, int t0,
                                               int nchunks, int n0, int ncb, int tid)
 {
     constexpr int NRB = C / 16;
@@ -64,8 +64,8 @@ __device__ __forceinline__ void adjoint_chunk(ChunkSmem<C>& sm, const ChunkArgs&
     const long base_tn = bh * static_cast<long>(T) * n;
     TIN* __restrict__ gdv = static_cast<TIN*>(args.dv);
 #pragma unroll
-    for (int w = 0; w < 2; ++w) {
-        const int cb = wave + 4 * w;
+    for (int w = 0; w < 8 / NW; ++w) {
+        const int cb = wave + NW * w;
         if (cb >= ncb) continue;
         const int j = n0 + cb * 8 + (c >> 1);
         Frag8 br[NRB];                   // G_R = conj(dL/do), K = token
@@ -189,13 +189,14 @@ __device__ __forceinline__ void adjoint_chunk(ChunkSmem<C>& sm, const ChunkArgs&
 // recording, per chunk, the state entering it (ck_state) and Delta (ck_rows), for the
 // backward.  MODE 2: the adjoint scan of the
 // backward, chunks in reverse order (below).
-template <int P, typename TIN, typename TOUT, int C, bool GATED, int MODE, typename SM = ChunkSmem<C>>
+template <int P, typename TIN, typename TOUT, int C, bool GATED, int MODE, typename SM = ChunkSmem<C>,
+          int NW = 4>
 __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsigned block)
 {
     constexpr int NRB = C / 16;          // 16-token blocks per chunk
     constexpr int SEG = C / 4;           // tokens per thread in the cumulative sums
     constexpr int LDG = ChunkSmem<C>::LDG;
-    constexpr int CBW = 2;               // value column blocks (8 complex columns) per wave
+    constexpr int CBW = 8 / NW;          // value column blocks (8 complex columns) per wave of NW
 
     const TIN* __restrict__ gv = static_cast<const TIN*>(args.v);
     TOUT* __restrict__ go = static_cast<TOUT*>(args.o);
@@ -225,7 +226,7 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
     f32x4 Sacc[CBW][MP / 16];
 #pragma unroll
     for (int w = 0; w < CBW; ++w) {
-        const int cb = wave + 4 * w;
+        const int cb = wave + NW * w;
         const int j = n0 + cb * 8 + (c >> 1);
 #pragma unroll
         for (int kb = 0; kb < MP / 16; ++kb) {
@@ -251,7 +252,7 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
             const long base = (bh * nchunks + ch) * static_cast<long>(m) * n;
 #pragma unroll
             for (int w = 0; w < CBW; ++w) {
-                const int cb = wave + 4 * w;
+                const int cb = wave + NW * w;
                 const int j = n0 + cb * 8 + (c >> 1);
                 if (cb >= ncb || j >= n) continue;
 #pragma unroll
@@ -271,7 +272,7 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
         if constexpr (MODE != 2) {
 #pragma unroll
             for (int w = 0; w < CBW; ++w) {
-                const int cb = wave + 4 * w;
+                const int cb = wave + NW * w;
                 const int j = n0 + cb * 8 + (c >> 1);
 #pragma unroll
                 for (int kb = 0; kb < NRB; ++kb)
@@ -288,13 +289,13 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
         }
         {
             float2 gkeep[SEG];
-            stage_load<TIN, C, GATED, false, MODE == 3>(sm, args, bh, t0, tid, gkeep);
+            stage_load<TIN, C, GATED, false, MODE == 3, SM, (NW > 4)>(sm, args, bh, t0, tid, gkeep);
         }
         __syncthreads();
 
         // ============================================================ G: L' and A
-        stage_gram<P, C, true>(sm, tid);
-        if constexpr (MODE == 3) stage_gram<P, C, true, true>(sm, tid);   // L'_kr, A_qr
+        stage_gram<P, C, true, false, SM, NW>(sm, tid);
+        if constexpr (MODE == 3) stage_gram<P, C, true, true, SM, NW>(sm, tid);   // L'_kr, A_qr
         __syncthreads();
 
         // ============================================================ S: N = (I + D_beta L')^{-1}
@@ -328,11 +329,12 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
         //   N_ps = -N_pp sum_{qb = s}^{p-1} (D_beta L')_{p qb} N_{qb s}
 #pragma unroll
         for (int p = 1; p < NRB; ++p) {
-            f32x4 res[2];
+            constexpr int NIT = (8 + NW - 1) / NW;   // tasks per wave (at most 2 (NRB - 1) = 6)
+            f32x4 res[NIT];
             const int ntask = 2 * p;
 #pragma unroll
-            for (int it = 0; it < 2; ++it) {
-                const int task = wave + 4 * it;
+            for (int it = 0; it < NIT; ++it) {
+                const int task = wave + NW * it;
                 if (task < ntask) {
                     const int s = task >> 1, h = task & 1;
                     const int row = p * 16 + c;
@@ -370,8 +372,8 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
             }
             __syncthreads();
 #pragma unroll
-            for (int it = 0; it < 2; ++it) {
-                const int task = wave + 4 * it;
+            for (int it = 0; it < NIT; ++it) {
+                const int task = wave + NW * it;
                 if (task < ntask) {
                     const int s = task >> 1, h = task & 1;
                     const int jcol = s * 16 + h * 8 + (c >> 1);
@@ -385,7 +387,7 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
 
 
         if constexpr (MODE == 2) {
-            adjoint_chunk<P, TIN, TOUT, C>(sm, args, Sacc, bh, t0, nchunks, n0, ncb, tid);
+            adjoint_chunk<P, TIN, TOUT, C, NW>(sm, args, Sacc, bh, t0, nchunks, n0, ncb, tid);
             __syncthreads();
             continue;
         }
@@ -448,7 +450,7 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
                         }
 #pragma unroll
                         for (int w = 0; w < CBW; ++w)
-                            if (wave + 4 * w < ncb) mma<P>(yacc[w][rb], a, bvr[w][kb]);
+                            if (wave + NW * w < ncb) mma<P>(yacc[w][rb], a, bvr[w][kb]);
                     }
 #pragma unroll
                 for (int w = 0; w < CBW; ++w)
@@ -466,16 +468,16 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
                     const Frag8 a = tfrag(rb, kb);
 #pragma unroll
                     for (int w = 0; w < CBW; ++w)
-                        if (wave + 4 * w < ncb) mma<P>(D[w][rb], a, bv[w][kb]);
+                        if (wave + NW * w < ncb) mma<P>(D[w][rb], a, bv[w][kb]);
                 }
         }
         {
             constexpr int NWT = NRB * (2 * MP / 16);         // Wt tiles
-            constexpr int PER = (NWT + 3) / 4;
+            constexpr int PER = (NWT + NW - 1) / NW;
             f32x4 wres[PER];
 #pragma unroll
             for (int it = 0; it < PER; ++it) {
-                const int tile = wave + 4 * it;
+                const int tile = wave + NW * it;
                 wres[it] = zero4();
                 if (tile < NWT) {
                     const int rb = tile / (2 * MP / 16);
@@ -496,7 +498,7 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
             __syncthreads();
 #pragma unroll
             for (int it = 0; it < PER; ++it) {
-                const int tile = wave + 4 * it;
+                const int tile = wave + NW * it;
                 if (tile < NWT) {
                     const int rb = tile / (2 * MP / 16);
                     const int ib = tile - rb * (2 * MP / 16);
@@ -512,7 +514,7 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
         // ============================================================ D: Delta, O, S update
 #pragma unroll
         for (int w = 0; w < CBW; ++w) {
-            const int cb = wave + 4 * w;
+            const int cb = wave + NW * w;
             if (cb >= ncb) continue;
             const int jl = cb * 8 + (c >> 1);
             const int j = n0 + jl;
@@ -646,7 +648,7 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
     if (args.S_T != nullptr) {
 #pragma unroll
         for (int w = 0; w < CBW; ++w) {
-            const int cb = wave + 4 * w;
+            const int cb = wave + NW * w;
             const int j = n0 + cb * 8 + (c >> 1);
             if (cb >= ncb || j >= n) continue;
 #pragma unroll
@@ -660,25 +662,29 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
     }
 }
 
+// waves per workgroup: two per SIMD where the registers allow it (at C = 64 a second wave
+// per SIMD spills heavily), one otherwise
+template <int C> constexpr int scan_waves() { return C == 64 ? 4 : 8; }
+
 template <int P, typename TIN, typename TOUT, int C, bool GATED, int MODE>
-__global__ __launch_bounds__(NTHR, 1) void chunk_kernel(ChunkArgs args)
+__global__ __launch_bounds__(scan_waves<C>() * 64, 1) void chunk_kernel(ChunkArgs args)
 {
     using SM = std::conditional_t<MODE == 3, ChunkSmemDec<C>, ChunkSmem<C>>;
     __shared__ SM sm;
-    chunk_scan<P, TIN, TOUT, C, GATED, MODE, SM>(sm, args, blockIdx.x);
+    chunk_scan<P, TIN, TOUT, C, GATED, MODE, SM, scan_waves<C>()>(sm, args, blockIdx.x);
 }
 
 // The backward's two scans in one launch: the first nfwd workgroups run the recording
 // forward scan, the rest the adjoint scan (they read the same inputs and write disjoint
 // records), so both fill the GPU together.
 template <int P, typename TIN, typename TOUT, int C>
-__global__ __launch_bounds__(NTHR, 1) void scan_pair_kernel(ChunkArgs fwd, ChunkArgs adj, unsigned nfwd)
+__global__ __launch_bounds__(scan_waves<C>() * 64, 1) void scan_pair_kernel(ChunkArgs fwd, ChunkArgs adj, unsigned nfwd)
 {
     __shared__ ChunkSmem<C> sm;
     if (blockIdx.x < nfwd)
-        chunk_scan<P, TIN, float, C, false, 1>(sm, fwd, blockIdx.x);
+        chunk_scan<P, TIN, float, C, false, 1, ChunkSmem<C>, scan_waves<C>()>(sm, fwd, blockIdx.x);
     else
-        chunk_scan<P, TIN, TOUT, C, false, 2>(sm, adj, blockIdx.x - nfwd);
+        chunk_scan<P, TIN, TOUT, C, false, 2, ChunkSmem<C>, scan_waves<C>()>(sm, adj, blockIdx.x - nfwd);
 }
 
 static ChunkArgs make_args(const ChunkLaunch& L)
@@ -702,9 +708,9 @@ static hipError_t launch_chunk_t(const ChunkLaunch& L, hipStream_t st)
     auto go = [&](auto gated) {
         constexpr bool G = decltype(gated)::value;
         switch (L.C) {
-            case 16: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 16, G, 0>), grid, dim3(NTHR), 0, st, a); break;
-            case 32: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 32, G, 0>), grid, dim3(NTHR), 0, st, a); break;
-            case 64: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 64, G, 0>), grid, dim3(NTHR), 0, st, a); break;
+            case 16: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 16, G, 0>), grid, dim3(scan_waves<16>() * 64), 0, st, a); break;
+            case 32: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 32, G, 0>), grid, dim3(scan_waves<32>() * 64), 0, st, a); break;
+            case 64: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 64, G, 0>), grid, dim3(scan_waves<64>() * 64), 0, st, a); break;
             default: return hipErrorInvalidValue;
         }
         return hipGetLastError();
@@ -725,8 +731,8 @@ static hipError_t launch_dec_t(const ChunkLaunch& L, hipStream_t st)
     const ChunkArgs a = make_args(L);
     const dim3 grid(static_cast<unsigned>(static_cast<long>(L.B) * L.H * a.n_slices));
     switch (L.C) {
-        case 16: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 16, false, 3>), grid, dim3(NTHR), 0, st, a); break;
-        case 32: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 32, false, 3>), grid, dim3(NTHR), 0, st, a); break;
+        case 16: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 16, false, 3>), grid, dim3(scan_waves<16>() * 64), 0, st, a); break;
+        case 32: hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 32, false, 3>), grid, dim3(scan_waves<32>() * 64), 0, st, a); break;
         default: return hipErrorInvalidValue;       // C = 64 needs more LDS than a CU has
     }
     return hipGetLastError();
@@ -750,9 +756,9 @@ static hipError_t launch_scans_t(const ChunkLaunch& F, const ChunkLaunch& A, hip
     const unsigned nfwd = static_cast<unsigned>(nf);
     const dim3 grid(static_cast<unsigned>(nf + static_cast<long>(A.B) * A.H * aa.n_slices));
     switch (F.C) {
-        case 16: hipLaunchKernelGGL((scan_pair_kernel<P, TIN, TOUT, 16>), grid, dim3(NTHR), 0, st, af, aa, nfwd); break;
-        case 32: hipLaunchKernelGGL((scan_pair_kernel<P, TIN, TOUT, 32>), grid, dim3(NTHR), 0, st, af, aa, nfwd); break;
-        case 64: hipLaunchKernelGGL((scan_pair_kernel<P, TIN, TOUT, 64>), grid, dim3(NTHR), 0, st, af, aa, nfwd); break;
+        case 16: hipLaunchKernelGGL((scan_pair_kernel<P, TIN, TOUT, 16>), grid, dim3(scan_waves<16>() * 64), 0, st, af, aa, nfwd); break;
+        case 32: hipLaunchKernelGGL((scan_pair_kernel<P, TIN, TOUT, 32>), grid, dim3(scan_waves<32>() * 64), 0, st, af, aa, nfwd); break;
+        case 64: hipLaunchKernelGGL((scan_pair_kernel<P, TIN, TOUT, 64>), grid, dim3(scan_waves<64>() * 64), 0, st, af, aa, nfwd); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
