@@ -207,6 +207,29 @@ def cpu_baseline(x, budget_s=12.0):
                       f"(complex128 recurrence), {el:.1f} s"}
 
 
+def cpu_baseline_backward(x, dO, dS, budget_s=10.0):
+    """The oracle's reverse-mode sweep (oracle.backward, complex128 numpy) on whole heads of
+    the workload, one after another, until about budget_s seconds have been spent; the
+    rate counts a token as one position through all H heads, like the GPU figure."""
+    from oracle import backward as BW
+    B, H, T, m, n = x.shape
+    done = 0
+    t0 = time.perf_counter()
+    while True:
+        b, h = divmod(done % (B * H), H)
+        BW.recurrence_backward(x.q[b:b + 1, h:h + 1], x.k[b:b + 1, h:h + 1], x.v[b:b + 1, h:h + 1],
+                               x.alpha[b:b + 1, h:h + 1], x.theta[b:b + 1, h:h + 1], x.beta[b:b + 1, h:h + 1],
+                               None if x.S0 is None else x.S0[b:b + 1, h:h + 1], dO[b:b + 1, h:h + 1],
+                               dS[b:b + 1, h:h + 1])
+        done += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    el = time.perf_counter() - t0
+    return {"value": round(done * T / H / el, 1), "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"{done} heads of {B * H} (taken in turn) x {T} tokens (complex128 reverse sweep, "
+                      f"numpy in one process), {el:.1f} s"}
+
+
 def long_context(args):
     """The long-context float32 workload (B=1, H=16, T=65536, m=n=64, C=64): one
     sfda_chunk_fwd launch (one workgroup per head) against sfda_chunk_fwd_segmented with
@@ -348,14 +371,24 @@ def backward(args):
         flops = bwd_flops_per_chunk_head(C_BWD, m, n) * chunks
         eb = 2 if w.dtype == "bf16" else 4
         nbytes = bwd_bytes_per_token_head(m, n, eb, eb) * B * H * T
-        res["runs"].append({
+        tflops = flops / (ms / 1e3) / 1e12
+        peak = BF16_MFMA_PEAK_TFLOPS if w.dtype == "bf16" else FP32_MFMA_PEAK_TFLOPS
+        run = {
             "workload": w.name, "B": B, "H": H, "T": T, "m": m, "n": n, "C_fwd": w.C, "C_bwd": C_BWD, "dtype": w.dtype,
             "ms_bwd": round(ms, 4), "ms_fwd": round(ms_f, 4), "bwd_over_fwd": round(ms / ms_f, 2),
             "tokens_per_s_bwd": round(B * T / (ms / 1e3), 1),
-            "useful_tflops": round(flops / (ms / 1e3) / 1e12, 2),
-            "frac_fp32_mfma_peak": round(flops / (ms / 1e3) / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4),
-            "algorithmic_GBps": round(nbytes / (ms / 1e3) / 1e9, 1),
-            "workspace_bytes": int(ws.numel())})
+            # the whole pass against the matrix cores of the operand type it runs on, and its
+            # algorithmic bytes against HBM
+            "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": peak, "unit": "TFLOP/s",
+                         "frac": round(tflops / peak, 4), "traffic": None,
+                         "flops_per_chunk_head": bwd_flops_per_chunk_head(C_BWD, m, n)},
+            "hbm": {"achieved_GBps": round(nbytes / (ms / 1e3) / 1e9, 1), "peak_GBps": HBM_PEAK_GBS,
+                    "bytes_per_token_head": bwd_bytes_per_token_head(m, n, eb, eb)},
+            "workspace_bytes": int(ws.numel())}
+        if not args.no_cpu_baseline:
+            print(f"# oracle backward on the CPU ({w.name})", file=sys.stderr, flush=True)
+            run["cpu_baseline"] = cpu_baseline_backward(x, dO, dS)
+        res["runs"].append(run)
         del d, dO_t, dS_t, ws
         torch.cuda.empty_cache()
     print(json.dumps(res), flush=True)
@@ -398,12 +431,29 @@ def decoupled(args):
     ms_d = timed(run_dec, max(5, args.steps // 5), max(2, args.warmup // 5), stream)
     ms_t = timed(run_tied, max(5, args.steps // 5), max(2, args.warmup // 5), stream)
     flops = dec_flops_per_chunk_head(C, m, n) * B * H * (T // C)
+    tflops = flops / (ms_d / 1e3) / 1e12
     out = {"mode": "dec", "workload": "decoupled_bf16_b8h16_t4k_c32", "B": B, "H": H, "T": T, "m": m, "n": n,
            "C": C, "ms_decoupled": round(ms_d, 4), "ms_tied_same_C": round(ms_t, 4),
            "tokens_per_s_decoupled": round(B * T / (ms_d / 1e3), 1),
-           "useful_tflops": round(flops / (ms_d / 1e3) / 1e12, 2),
-           "frac_bf16_mfma_peak": round(flops / (ms_d / 1e3) / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
+           "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": BF16_MFMA_PEAK_TFLOPS,
+                        "unit": "TFLOP/s", "frac": round(tflops / BF16_MFMA_PEAK_TFLOPS, 4), "traffic": None,
+                        "flops_per_chunk_head": dec_flops_per_chunk_head(C, m, n)},
            "kernel_hash_fp32_path": bwd_hash()}
+    if not args.no_cpu_baseline:
+        from oracle import decoupled as Dd
+        print("# oracle (write-decoupled recurrence) on the CPU", file=sys.stderr, flush=True)
+        done, t0 = 0, time.perf_counter()
+        while True:
+            b = done % B
+            Dd.decoupled_recurrence(*(getattr(x, nm)[b:b + 1] for nm in ("q", "k", "r", "v", "alpha", "theta", "eta", "beta")),
+                                    x.S0[b:b + 1])
+            done += 1
+            if time.perf_counter() - t0 >= 10.0:
+                break
+        el = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round(done * T / el, 1), "unit": "tokens/s", "cores": 1, "kind": "oracle",
+                               "sample": f"{done} batch elements of {B} (taken in turn) x {H} heads x {T} tokens "
+                                         f"(complex128 numpy recurrence in one process), {el:.1f} s"}
     print(json.dumps(out), flush=True)
 
 
