@@ -41,7 +41,7 @@ struct GradArgs {
 };
 
 template <int P, typename TIN, typename TOUT, int C>
-__global__ __launch_bounds__(GW * 64, 1) void grad_kernel(GradArgs A)
+__global__ __launch_bounds__(GW * 64, C <= 32 ? 4 : 2) void grad_kernel(GradArgs A)
 {
     constexpr int NRB = C / 16;
     constexpr int SEG = C / 4;
@@ -304,51 +304,74 @@ __global__ __launch_bounds__(GW * 64, 1) void grad_kernel(GradArgs A)
 
     // ================================================================ G_Ki, G_Qg, G_Kg
     // Tile it of wave w covers channel block (w + 8 it) % 8 = w, so each wave collects the
-    // dL/dg_C shares of its channel block in gsum.
+    // dL/dg_C shares of its channel block in gsum.  The three products run one after another,
+    // each holding only its own operands in registers.
     constexpr int PER = (NCT + GW - 1) / GW;
     f32x4 gki[PER], gqg[PER], gkg[PER];
     float gsum = 0.f;
+    // left operand rows (K = value column): 0 conj(Delta), 1 G_R, 2 -G_E = -beta G_F
+    auto left4 = [&](int kind, int row, int c0, Frag8& a) {
+        float2 x[4];
+        if (kind == 0) rec4(Drow, row, C, c0, x);
+        else if (kind == 1) grad_out4(row, c0, x);
+        else rec4(Frow, row, C, c0, x);
+        const float sc = kind == 2 ? -sm.beta[min(row, C - 1)] : 1.f;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            a.v[2 * r] = sc * x[r].x;
+            a.v[2 * r + 1] = kind == 0 ? -x[r].y : sc * x[r].y;
+        }
+    };
+    // right operand (K = value column, output column icol): 0 G^T, 1 S^*
+    auto right4 = [&](int kind, int icol, int c0, Frag8& b) {
+        float2 y[4];
+        rec4(kind == 0 ? Grec : Srec, icol, m, c0, y);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) bpair(b, r, y[r].x, kind == 0 ? y[r].y : -y[r].y, qp);
+    };
+    // acc += (left kind lk) (right kind rk) over the value columns, two K-blocks of loads at a time
+    auto value_product = [&](f32x4& acc, int lk, int rk, int row, int icol) {
+        for (int k0 = 0; k0 < nkb; k0 += 2) {
+            Frag8 a[2], b[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                left4(lk, row, (k0 + u) * 16 + 4 * g, a[u]);
+                right4(rk, icol, (k0 + u) * 16 + 4 * g, b[u]);
+            }
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+                if (k0 + u < nkb) mma<P>(acc, a[u], b[u]);
+        }
+    };
+    // a C x C operand fragment from g2: G_L' (strict lower at g2[t][j]) or G_A (lower, at g2[j][t])
+    auto cc_frag = [&](bool transposed_store, int row, int kb, int lo, Frag8& a) {
+        // lo: 0 -> jt < row, 1 -> jt <= row, 2 -> jt > row, 3 -> jt >= row
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int jt = kb * 16 + 4 * g + r;
+            const bool ok = lo == 0 ? jt < row : lo == 1 ? jt <= row : lo == 2 ? jt > row : jt >= row;
+            const float2 x = masked(ok, pin(transposed_store ? sm.g2[jt * LDG + row] : sm.g2[row * LDG + jt]));
+            a.v[2 * r] = x.x;
+            a.v[2 * r + 1] = x.y;
+        }
+    };
+    auto lds_right = [&](const float2* X, int kb, int icol, Frag8& b) {   // conj(X[jt][icol])
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const float2 y = X[(kb * 16 + 4 * g + r) * LDX + icol];
+            bpair(b, r, y.x, -y.y, qp);
+        }
+    };
+    // G_Ki = conj(Delta) G^T diag(conj(g_C)) + G_L'^T conj(conj(K)G) + G_A^T conj(conj(Q)G)
 #pragma unroll
     for (int it = 0; it < PER; ++it) {
         const int tile = wave + GW * it;
-        gki[it] = zero4(); gqg[it] = zero4(); gkg[it] = zero4();
+        gki[it] = zero4();
         if (tile >= NCT) continue;
         const int rb = tile / (2 * MP / 16);
         const int icol = (tile - rb * (2 * MP / 16)) * 8 + (c >> 1);
         const int row = rb * 16 + c;
-        const float btr = sm.beta[row];
-        // value-dimension products: conj(Delta) G^T, G_R S^*, -G_E S^*
-        for (int k0 = 0; k0 < nkb; k0 += 2) {             // all loads of two K-blocks first
-            Frag8 ad[2], ar[2], af[2], bg[2], bs[2];
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                const int c0 = (k0 + u) * 16 + 4 * g;
-                float2 d[4], x[4], f[4], y[4], sv[4];
-                rec4(Drow, row, C, c0, d);
-                grad_out4(row, c0, x);
-                rec4(Frow, row, C, c0, f);
-                rec4(Grec, icol, m, c0, y);                        // G^T[cc][icol]
-                rec4(Srec, icol, m, c0, sv);                       // S^*[cc][icol]
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    ad[u].v[2 * r] = d[r].x;
-                    ad[u].v[2 * r + 1] = -d[r].y;
-                    ar[u].v[2 * r] = x[r].x;
-                    ar[u].v[2 * r + 1] = x[r].y;
-                    af[u].v[2 * r] = -btr * f[r].x;
-                    af[u].v[2 * r + 1] = -btr * f[r].y;
-                    bpair(bg[u], r, y[r].x, y[r].y, qp);
-                    bpair(bs[u], r, sv[r].x, -sv[r].y, qp);
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < 2; ++u)
-                if (k0 + u < nkb) {
-                    mma<P>(gki[it], ad[u], bg[u]);
-                    mma<P>(gqg[it], ar[u], bs[u]);
-                    mma<P>(gkg[it], af[u], bs[u]);
-                }
-        }
+        value_product(gki[it], 0, 0, row, icol);
         // dL/dg_C, second part: column sums of G_Yp * conj(K/G)
         {
             float part = 0.f;
@@ -371,33 +394,37 @@ __global__ __launch_bounds__(GW * 64, 1) void grad_kernel(GradArgs A)
                 gki[it][r] = qp ? (gg.x * own - gg.y * oth) : (gg.x * own + gg.y * oth);
             }
         }
-        // token-dimension products from LDS
 #pragma unroll
-        for (int kb = 0; kb < NRB; ++kb) {
-            Frag8 alt, aat, aa, al, bkg, bqg, bki;
+        for (int kb = rb; kb < NRB; ++kb) {
+            Frag8 a, b;
+            cc_frag(true, row, kb, 2, a);              // G_L'^T[row][jt] = G_L'[jt][row], jt > row
+            lds_right(sm.kg, kb, icol, b);
+            mma<P>(gki[it], a, b);
+            cc_frag(false, row, kb, 3, a);             // G_A^T[row][jt] = G_A[jt][row], jt >= row
+            lds_right(sm.qg, kb, icol, b);
+            mma<P>(gki[it], a, b);
+        }
+    }
+    // G_Qg = G_R S^* + G_A conj(K/G),  G_Kg = -G_E S^* + G_L' conj(K/G)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int jt = kb * 16 + 4 * g + r;
-                const float2 lt = masked(jt > row, pin(sm.g2[jt * LDG + row]));   // G_L'^T[row][jt]
-                const float2 at = masked(jt >= row, pin(sm.g2[row * LDG + jt]));  // G_A^T[row][jt]
-                const float2 a1 = masked(jt <= row, pin(sm.g2[jt * LDG + row]));  // G_A[row][jt]
-                const float2 l1 = masked(jt < row, pin(sm.g2[row * LDG + jt]));   // G_L'[row][jt]
-                alt.v[2 * r] = lt.x; alt.v[2 * r + 1] = lt.y;
-                aat.v[2 * r] = at.x; aat.v[2 * r + 1] = at.y;
-                aa.v[2 * r] = a1.x;  aa.v[2 * r + 1] = a1.y;
-                al.v[2 * r] = l1.x;  al.v[2 * r + 1] = l1.y;
-                const float2 y1 = sm.kg[jt * LDX + icol], y2 = sm.qg[jt * LDX + icol], y3 = sm.ki[jt * LDX + icol];
-                bpair(bkg, r, y1.x, -y1.y, qp);
-                bpair(bqg, r, y2.x, -y2.y, qp);
-                bpair(bki, r, y3.x, -y3.y, qp);
-            }
-            if (kb >= rb) {
-                mma<P>(gki[it], alt, bkg);
-                mma<P>(gki[it], aat, bqg);
-            }
-            if (kb <= rb) {
-                mma<P>(gqg[it], aa, bki);
-                mma<P>(gkg[it], al, bki);
+    for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+        for (int it = 0; it < PER; ++it) {
+            const int tile = wave + GW * it;
+            f32x4& acc = pass == 0 ? gqg[it] : gkg[it];
+            acc = zero4();
+            if (tile >= NCT) continue;
+            const int rb = tile / (2 * MP / 16);
+            const int icol = (tile - rb * (2 * MP / 16)) * 8 + (c >> 1);
+            const int row = rb * 16 + c;
+            value_product(acc, pass == 0 ? 1 : 2, 1, row, icol);
+#pragma unroll
+            for (int kb = 0; kb <= rb; ++kb) {
+                Frag8 a, b;
+                if (pass == 0) cc_frag(true, row, kb, 1, a);    // G_A[row][jt], jt <= row
+                else cc_frag(false, row, kb, 0, a);             // G_L'[row][jt], jt < row
+                lds_right(sm.ki, kb, icol, b);
+                mma<P>(acc, a, b);
             }
         }
     }
