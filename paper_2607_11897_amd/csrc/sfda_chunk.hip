@@ -243,6 +243,11 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
         }
     }
 
+    // eight-wave scans fetch alpha, theta and beta a chunk ahead (their registers fit there)
+    constexpr bool PRE = NW > 4;
+    InPre<C> pf;
+    if constexpr (PRE)
+        if (nchunks > 0) prefetch_inputs<TIN, C, true>(args, bh, (MODE == 2 ? nchunks - 1 : 0) * C, tid, pf);
     for (int it_ch = 0; it_ch < nchunks; ++it_ch) {
         const int ch = MODE == 2 ? nchunks - 1 - it_ch : it_ch;
         const int t0 = ch * C;
@@ -289,8 +294,11 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
         }
         {
             float2 gkeep[SEG];
-            stage_load<TIN, C, GATED, false, MODE == 3, SM, (NW > 4)>(sm, args, bh, t0, tid, gkeep);
+            stage_load<TIN, C, GATED, false, MODE == 3, SM, (NW > 4), PRE>(sm, args, bh, t0, tid, gkeep, &pf);
         }
+        if constexpr (PRE)
+            if (it_ch + 1 < nchunks)
+                prefetch_inputs<TIN, C, true>(args, bh, (MODE == 2 ? ch - 1 : ch + 1) * C, tid, pf);
         __syncthreads();
 
         // ============================================================ G: L' and A

@@ -64,17 +64,44 @@ struct ChunkSmemDec : ChunkSmem<C> {
     float wb[C];                             // write strengths beta_t
 };
 
+// raw alpha, theta and beta of one thread's tokens, fetched a chunk ahead by a scan
+template <int C>
+struct InPre {
+    float a[C / 4], th[C / 4], b;
+};
+
+template <typename TIN, int C, bool WIDE>
+__device__ __forceinline__ void prefetch_inputs(const ChunkArgs& args, long bh, int t0, int tid, InPre<C>& pf)
+{
+    constexpr int SEG = C / 4;
+    if (WIDE && tid >= NTHR) return;
+    const int T = args.T, m = args.m;
+    const long base_tm = bh * static_cast<long>(T) * m;
+    const int i = tid & 63, seg = (tid >> 6) & 3;
+#pragma unroll
+    for (int u = 0; u < SEG; ++u) {
+        const int t = t0 + seg * SEG + u;
+        const long e = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
+        pf.a[u] = Elem<TIN>::load(static_cast<const TIN*>(args.alpha), e);
+        pf.th[u] = Elem<TIN>::load(static_cast<const TIN*>(args.theta), e);
+    }
+    pf.b = Elem<TIN>::load(static_cast<const TIN*>(args.beta), bh * static_cast<long>(T) + min(t0 + (tid & (C - 1)), T - 1));
+}
+
 // ----------------------------------------------------------------- load stage
 // Thread (channel i = tid % 64, segment tid / 64) walks C / 4 consecutive tokens of the
 // chunk starting at t0: running sums of log alpha and theta give g_t; the decay-scaled
 // operands go to LDS.  Padding past T (and channels past m) are identity tokens.  With
 // KEEP, g_t of the thread's tokens is returned in gkeep; with DEC (SM = ChunkSmemDec) the
 // write directions become R / G and the write strengths are loaded too.  In a block wider
-// than 256 threads (WIDE) only the first 256 work; every thread passes the barrier.
+// than 256 threads (WIDE) only the first 256 work; every thread passes the barrier.  With
+// PRE, alpha, theta and beta come from *pre (fetched a chunk ahead) and q, k are requested
+// before the running sums, so their latency overlaps the sums and the barrier.
 template <typename TIN, int C, bool GATED, bool KEEP = false, bool DEC = false, typename SM = ChunkSmem<C>,
-          bool WIDE = false>
+          bool WIDE = false, bool PRE = false>
 __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long bh,
-                                           int t0, int tid, float2 (&gkeep)[C / 4])
+                                           int t0, int tid, float2 (&gkeep)[C / 4],
+                                           const InPre<C>* pre = nullptr)
 {
     const bool worker = !WIDE || tid < NTHR;
     constexpr int SEG = C / 4;
@@ -90,14 +117,32 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
     const int seg = (tid >> 6) & 3;
     float la[SEG], ph[SEG];
     float sa = 0.f, sp = 0.f;
+    float2 qpre[PRE ? SEG : 1], kpre[PRE ? SEG : 1];
+    if constexpr (PRE) {
+        if (worker) {
+#pragma unroll
+            for (int u = 0; u < SEG; ++u) {
+                const int t = t0 + seg * SEG + u;
+                const long e2 = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
+                qpre[u] = Elem<TIN>::load2(gq, e2);
+                kpre[u] = Elem<TIN>::load2(gk, e2);
+            }
+        }
+    }
     if (worker) {
 #pragma unroll
     for (int u = 0; u < SEG; ++u) {
         const int t = t0 + seg * SEG + u;
         const bool ok = t < T && i < m;
         const long e = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
-        const float a_ld = pin(Elem<TIN>::load(ga, e));
-        float th = masked(ok, Elem<TIN>::load(gth, e));
+        float a_ld, th;
+        if constexpr (PRE) {
+            a_ld = pin(pre->a[u]);
+            th = masked(ok, pre->th[u]);
+        } else {
+            a_ld = pin(Elem<TIN>::load(ga, e));
+            th = masked(ok, Elem<TIN>::load(gth, e));
+        }
         float a = ok ? a_ld : 1.f;
         if constexpr (GATED) {      // padding stays the identity token (alpha = 1, theta = 0)
             a = ok ? args.amin + args.aspan * sigmoid_acc(a_ld) : 1.f;
@@ -113,7 +158,9 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
     }
     if (worker) {
         const int tb = t0 + (tid & (C - 1));
-        float bv = Elem<TIN>::load(gb, bh * static_cast<long>(T) + min(tb, T - 1));
+        float bv;
+        if constexpr (PRE) bv = pre->b;
+        else bv = Elem<TIN>::load(gb, bh * static_cast<long>(T) + min(tb, T - 1));
         if constexpr (GATED) bv = sigmoid_acc(bv);
         if (tid < C) sm.beta[tid] = masked(tb < T, bv);
         if constexpr (DEC) {
@@ -143,7 +190,14 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
         if constexpr (KEEP) gkeep[u] = make_float2(gr, gi);
         const bool ok = t < T && i < m;
         const long e2 = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
-        float2 qq = Elem<TIN>::load2(gq, e2), kk = Elem<TIN>::load2(gk, e2);
+        float2 qq, kk;
+        if constexpr (PRE) {
+            qq = qpre[u];
+            kk = kpre[u];
+        } else {
+            qq = Elem<TIN>::load2(gq, e2);
+            kk = Elem<TIN>::load2(gk, e2);
+        }
         qq = masked(ok, qq);
         kk = masked(ok, kk);
         if constexpr (GATED) {
