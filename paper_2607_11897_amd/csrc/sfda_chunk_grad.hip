@@ -136,8 +136,11 @@ __global__ __launch_bounds__(GW * 64, C <= 32 ? 4 : 2) void grad_kernel(GradArgs
     // (the load stage and the elementwise stage work on the first 256 threads; the latter
     // forms g again rather than holding it in registers through the whole kernel)
     {
+        // every input load of the stage in flight at once: alpha, theta, beta, then q, k
+        InPre<C> pf;
+        prefetch_inputs<TIN, C, true>(args, bh, t0, tid, pf);
         float2 gkeep[SEG];
-        stage_load<TIN, C, false, false, false, ChunkSmem<C>, true>(sm, args, bh, t0, tid, gkeep);
+        stage_load<TIN, C, false, false, false, ChunkSmem<C>, true, true>(sm, args, bh, t0, tid, gkeep, &pf);
     }
     // dL/dg_C, first part: sum over columns of G * conj(S), one state row per 8 threads
     {
