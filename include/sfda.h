@@ -202,7 +202,11 @@ sfda_status_t sfda_chunk_fwd_segmented(const void* q, const void* k, const void*
  *          bytes (SFDA_ERR_SHAPE if smaller, SFDA_ERR_NULL if NULL and needed), 16-byte
  *          aligned, no initial contents; holds per chunk the state entering it and dL/dS
  *          leaving it (m x n) and two C x n blocks, complex float32.
- *   Sizes, C and dtypes as sfda_chunk_fwd; T == 0 writes dS0 = dS_T (or zeros).
+ *   Sizes, C and dtypes as sfda_chunk_fwd; T == 0 writes dS0 = dS_T (or zeros).  The
+ *   chunk length only fixes how the work is blocked (every C gives the same gradients up
+ *   to rounding): C = 64 runs at chunk length 32, the largest whose gradient pass keeps a
+ *   chunk's operands and a staged block of value columns in one CU's LDS, and the
+ *   workspace function sizes for that.
  *   alpha must be nonzero wherever T > 0 (dalpha divides by it).
  */
 size_t sfda_chunk_bwd_workspace_bytes(int B, int H, int T, int m, int n, int C);

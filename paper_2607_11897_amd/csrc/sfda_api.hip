@@ -253,10 +253,16 @@ sfda_status_t sfda_chunk_fwd_segmented(const void* q, const void* k, const void*
     return SFDA_OK;
 }
 
+// the backward's chunk length: C = 64 runs at 32 (the gradient pass stages a block of
+// value columns beside the chunk's operands in LDS; every C gives the same gradients up to
+// rounding)
+static int bwd_chunk(int C) { return C > 32 ? 32 : C; }
+
 size_t sfda_chunk_bwd_workspace_bytes(int B, int H, int T, int m, int n, int C)
 {
     if (B <= 0 || H <= 0 || T < 0 || m < 1 || m > 64 || n < 1) return 0;
     if (C != 16 && C != 32 && C != 64) return 0;
+    C = bwd_chunk(C);
     const size_t chunks = static_cast<size_t>(B) * H * ((static_cast<size_t>(T) + C - 1) / C);
     // per chunk: S entering and dL/dS leaving (m x n each), Delta and G_F (C x n each)
     return chunks * (2 * static_cast<size_t>(m) * n + 2 * static_cast<size_t>(C) * n) * 8;
@@ -273,6 +279,8 @@ sfda_status_t sfda_chunk_bwd(const void* q, const void* k, const void* v, const 
     if (!dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return SFDA_ERR_DTYPE;
     if (B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1) return SFDA_ERR_SHAPE;
     if (C != 16 && C != 32 && C != 64) return SFDA_ERR_CHUNK;
+    const size_t need = sfda_chunk_bwd_workspace_bytes(B, H, T, m, n, C);
+    C = bwd_chunk(C);
     const long BH = static_cast<long>(B) * H;
     const int slice = n <= 64 ? ((n + 7) / 8) * 8 : 64;
     const long nchunks = (static_cast<long>(T) + C - 1) / C;
@@ -282,7 +290,6 @@ sfda_status_t sfda_chunk_bwd(const void* q, const void* k, const void* v, const 
     if (need_inputs && (!q || !k || !v || !alpha || !theta || !beta || !dO || !dq || !dk || !dv ||
                         !dalpha || !dtheta || !dbeta))
         return SFDA_ERR_NULL;
-    const size_t need = sfda_chunk_bwd_workspace_bytes(B, H, T, m, n, C);
     if (need > 0 && !workspace) return SFDA_ERR_NULL;
     const void* ptrs[] = {q, k, v, alpha, theta, beta, S0, dO, dS_T, dq, dk, dv, dalpha, dtheta,
                           dbeta, dS0, workspace};

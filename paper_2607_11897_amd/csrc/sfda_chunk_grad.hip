@@ -23,15 +23,20 @@
 //   into suffix sums over the chunk: dalpha = suffix(Re dL/dz) / alpha, dtheta = suffix(Im).
 // Gradients of a complex variable are dL/dRe + i dL/dIm.
 //
-// Products over the value dimension read their operands straight from the records (global
-// memory, one 32-byte row piece per lane and K-block); products over tokens read the
-// decay-scaled operands from LDS.  The C x C gradients G_L' and G_A share one LDS block
-// (G_L' strict lower, G_A^T upper with the diagonal).
+// Products over the value dimension take their operands from LDS: the records are staged
+// a block of value columns at a time (every load of a block in flight together) and each
+// product accumulates over the blocks in registers, so the pass waits on global memory
+// once per block instead of once per product; products over tokens read the decay-scaled
+// operands from LDS.  The C x C gradients G_L' and G_A share one LDS block (G_L' strict
+// lower, G_A^T upper with the diagonal).  C = 16 and 32 (the chunk's LDS and the staged
+// block together stay within one CU's 160 KB).
+#include <type_traits>
+
 #include "sfda_chunk_common.h"
 
 namespace sfda {
 
-constexpr int GW = 8;        // waves per workgroup: two per SIMD, to hide the record loads' latency
+constexpr int GW = 8;        // waves per workgroup
 
 struct GradArgs {
     ChunkArgs in;                          // q, k, v, alpha, theta, beta, T, m, n
@@ -40,17 +45,160 @@ struct GradArgs {
     void *dq, *dk, *dalpha, *dtheta, *dbeta;
 };
 
+// ---------------------------------------------------------------- staged record blocks
+// The products over the value dimension read a block of NB value columns of S, G (state
+// rows x NB) and of Delta, G_F, G_R (tokens x NB) from LDS, staged once per block with every
+// load of the block in flight together.  The bf16 path keeps them as bf16 pairs (its matrix
+// cores round the operands to bf16 anyway; the fp32 records stay the source of the
+// elementwise sums), the fp32 path as fp32.  Rows are 272 bytes: a 16-byte fragment read by
+// 16 lanes of different rows touches every bank once.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+struct FragW { u32x4 w; };   // a lane's 8 bf16 operand values as 4 packed pairs
+
+// Global reads of the stage go through buffer resources: a read past the resource's size
+// returns zero, so padding rows need no mask, and a lane outside the valid columns passes an
+// offset past every resource.  No select follows a load, so the loads of a stage issue back
+// to back and are waited on once.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t OOR = 0x80000000u;
+__device__ __forceinline__ rsrc_t buf(const void* base, long bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes), 0x00020000);
+}
+__device__ __forceinline__ float2 ld_c64(rsrc_t r, uint32_t off) {      // complex float32
+    return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+}
+template <typename T> __device__ __forceinline__ float2 ld_cplx(rsrc_t r, uint32_t off);
+template <> __device__ __forceinline__ float2 ld_cplx<float>(rsrc_t r, uint32_t off) { return ld_c64(r, off); }
+template <> __device__ __forceinline__ float2 ld_cplx<uint16_t>(rsrc_t r, uint32_t off) {
+    const uint32_t w = __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+    return make_float2(__uint_as_float(w << 16), __uint_as_float(w & 0xFFFF0000u));
+}
+template <typename T> __device__ __forceinline__ float ld_real(rsrc_t r, uint32_t off);
+template <> __device__ __forceinline__ float ld_real<float>(rsrc_t r, uint32_t off) {
+    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+template <> __device__ __forceinline__ float ld_real<uint16_t>(rsrc_t r, uint32_t off) {
+    return __uint_as_float(static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0)) << 16);
+}
+
+template <int P> struct Rec;
+
+template <> struct Rec<PREC_BF16> {
+    using E = uint32_t;      // (re, im) bf16 pair, re in the low half
+    using Op = FragW;
+    static constexpr int NB = 64, LD = 68;
+    static __device__ __forceinline__ E pack(float2 x) {
+        const f32x2 v = {x.x, x.y};
+        return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+    }
+    static __device__ __forceinline__ float re(E w) { return __uint_as_float(w << 16); }
+    static __device__ __forceinline__ float im(E w) { return __uint_as_float(w & 0xFFFF0000u); }
+    // the B pair of bpair for y (cj: for conj(y)) and output column part q, on the packed
+    // word: part 1 swaps the halves (a byte permute), the sign flips are one xor
+    static __device__ __forceinline__ uint32_t bword(E w, bool cj, int q) {
+        const uint32_t sel = q ? 0x01000302u : 0x03020100u;
+        const uint32_t flip = q ? (cj ? 0x8000u : 0u) : (cj ? 0u : 0x80000000u);
+        return __builtin_amdgcn_perm(w, w, sel) ^ flip;
+    }
+    // A fragment: four consecutive entries of one row (16-byte aligned), cj conjugates
+    static __device__ __forceinline__ Op left(const E* p, bool cj) {
+        u32x4 x = *reinterpret_cast<const u32x4*>(p);
+        if (cj) x ^= 0x80000000u;
+        return Op{x};
+    }
+    static __device__ __forceinline__ Op right(E y0, E y1, E y2, E y3, bool cj, int q) {
+        const u32x4 x = {bword(y0, cj, q), bword(y1, cj, q), bword(y2, cj, q), bword(y3, cj, q)};
+        return Op{x};
+    }
+    static __device__ __forceinline__ Op right4(const E* p, bool cj, int q) {
+        const u32x4 x = *reinterpret_cast<const u32x4*>(p);
+        return right(x[0], x[1], x[2], x[3], cj, q);
+    }
+    static __device__ __forceinline__ Op conv(const Frag8& f) {
+        u32x4 x;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) x[r] = pack(make_float2(f.v[2 * r], f.v[2 * r + 1]));
+        return Op{x};
+    }
+    static __device__ __forceinline__ void mma(f32x4& acc, const Op& a, const Op& b) {
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a.w),
+                                                       __builtin_bit_cast(bf16x8, b.w), acc, 0, 0, 0);
+    }
+};
+
+template <> struct Rec<PREC_F32> {
+    using E = float2;
+    using Op = Frag8;
+    static constexpr int NB = 32, LD = 34;
+    static __device__ __forceinline__ E pack(float2 x) { return x; }
+    static __device__ __forceinline__ float re(E w) { return w.x; }
+    static __device__ __forceinline__ float im(E w) { return w.y; }
+    static __device__ __forceinline__ Op left(const E* p, bool cj) {
+        const float4 a = *reinterpret_cast<const float4*>(p);
+        const float4 b = *reinterpret_cast<const float4*>(p + 2);
+        const float s = cj ? -1.f : 1.f;
+        Op f;
+        f.v[0] = a.x; f.v[1] = s * a.y; f.v[2] = a.z; f.v[3] = s * a.w;
+        f.v[4] = b.x; f.v[5] = s * b.y; f.v[6] = b.z; f.v[7] = s * b.w;
+        return f;
+    }
+    static __device__ __forceinline__ Op right(E y0, E y1, E y2, E y3, bool cj, int q) {
+        const float s = cj ? -1.f : 1.f;
+        Op f;
+        bpair(f, 0, y0.x, s * y0.y, q);
+        bpair(f, 1, y1.x, s * y1.y, q);
+        bpair(f, 2, y2.x, s * y2.y, q);
+        bpair(f, 3, y3.x, s * y3.y, q);
+        return f;
+    }
+    static __device__ __forceinline__ Op right4(const E* p, bool cj, int q) {
+        const float4 a = *reinterpret_cast<const float4*>(p);
+        const float4 b = *reinterpret_cast<const float4*>(p + 2);
+        return right(make_float2(a.x, a.y), make_float2(a.z, a.w), make_float2(b.x, b.y),
+                     make_float2(b.z, b.w), cj, q);
+    }
+    static __device__ __forceinline__ Op conv(const Frag8& f) { return f; }
+    static __device__ __forceinline__ void mma(f32x4& acc, const Op& a, const Op& b) {
+        sfda::mma<PREC_F32>(acc, a, b);
+    }
+};
+
+template <int P, int C>
+struct GradSmem {
+    using E = typename Rec<P>::E;
+    static constexpr int LD = Rec<P>::LD;
+    ChunkSmem<C> ch;
+    alignas(16) E S[MP * LD];          // state entering the chunk
+    alignas(16) E G[MP * LD];          // dL/dS of the state leaving it
+    alignas(16) E D[C * LD];           // Delta
+    alignas(16) E F[C * LD];           // G_F
+    alignas(16) E R[C * LD];           // G_R = conj(dL/do)
+    float dbeta_part[GW][C];           // per-wave shares of dbeta
+    float ggc[2 * MP];                 // dL/dg_C (complex)
+};
+
 template <int P, typename TIN, typename TOUT, int C>
-__global__ __launch_bounds__(GW * 64, C <= 32 ? 4 : 2) void grad_kernel(GradArgs A)
+__global__ __launch_bounds__(GW * 64, C <= 16 ? 4 : 2) void grad_kernel(GradArgs A)
 {
+    using RC = Rec<P>;
+    using Op = typename RC::Op;
+    constexpr int NB = RC::NB, LD = RC::LD;
     constexpr int NRB = C / 16;
     constexpr int SEG = C / 4;
     constexpr int LDG = ChunkSmem<C>::LDG;
     constexpr int NCT = NRB * (2 * MP / 16);        // C x m output tiles (16 tokens x 8 channels)
     constexpr int NT1 = NRB * (NRB + 1);            // causal tiles of a C x C matrix
-    __shared__ ChunkSmem<C> sm;
-    __shared__ float dbeta_part[GW][C];             // per-wave shares of dbeta
-    __shared__ float ggc[2 * MP];                   // dL/dg_C (complex)
+    constexpr int PER = (NCT + GW - 1) / GW;        // C x m tiles per wave
+    constexpr int NGA = (2 * NT1 + GW - 1) / GW;    // G_A / G_L' tiles per wave
+    constexpr int RPI = GW * 64 / NB;               // record rows per staging step
+    constexpr int NS = MP / RPI;                    // staged S, G entries per thread
+    constexpr int NR = C / RPI;                     // staged Delta, G_F, G_R entries per thread
+    static_assert(NR >= 1 && NB % 16 == 0 && NB / 8 <= GW, "staging shape");
+    __shared__ GradSmem<P, C> gs;
+    ChunkSmem<C>& sm = gs.ch;
 
     const ChunkArgs& args = A.in;
     const int T = args.T, m = args.m, n = args.n;
@@ -61,8 +209,6 @@ __global__ __launch_bounds__(GW * 64, C <= 32 ? 4 : 2) void grad_kernel(GradArgs
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int c = lane & 15, g = lane >> 4, qp = lane & 1;
-    const int nkb = (n + 15) / 16;                  // K-blocks over the value columns
-    const int ncbn = (n + 7) / 8;                   // 8-column blocks of the value columns
 
     const float2* Srec = reinterpret_cast<const float2*>(A.S_rec) + (bh * nchunks + ch) * static_cast<long>(m) * n;
     const float2* Grec = reinterpret_cast<const float2*>(A.G_rec) + (bh * nchunks + ch) * static_cast<long>(m) * n;
@@ -73,282 +219,256 @@ __global__ __launch_bounds__(GW * 64, C <= 32 ? 4 : 2) void grad_kernel(GradArgs
     const long base_tn = bh * static_cast<long>(T) * n;
     const long base_tm = bh * static_cast<long>(T) * m;
 
-    // record element (row, column) of a [rows][n] block, zero outside
-    auto rec = [&](const float2* p, int row, int rows, int col) {
-        const bool ok = row < rows && col < n;
-        return masked(ok, p[static_cast<long>(min(row, rows - 1)) * n + min(col, n - 1)]);
+    // ------------------------------------------------------------ staging
+    // thread tid covers column tid % NB of rows tid / NB + RPI u (consecutive lanes read
+    // consecutive columns); the H stage's conj(V) parts go straight to registers
+    struct Raw {
+        float2 s[NS], g[NS], d[NR], f[NR], r[NR];
+        typename RC::E v[NRB][4];                   // raw v entries (parts taken in the H stage)
     };
-    // G_R = conj(dL/do) at chunk row tl, column col
-    auto grad_out = [&](int tl, int col) {
-        const int t = t0 + tl;
-        const bool ok = t < T && col < n;
-        float2 x = masked(ok, Elem<TOUT>::load2(gdO, base_tn + static_cast<long>(min(t, T - 1)) * n + min(col, n - 1)));
-        return make_float2(x.x, -x.y);
-    };
-    // Four consecutive columns col0 .. col0 + 3 (col0 a multiple of 4) of one row: with n a
-    // multiple of 4 the group is wholly inside or outside the row and 32-byte aligned, and a
-    // lane fetches it with 16-byte loads (a wave touches 16 rows x 64 bytes per load instead
-    // of 64 scattered 8-byte pieces); otherwise element by element.
-    const bool vec4 = (n & 3) == 0;
-    auto rec4 = [&](const float2* p, int row, int rows, int col0, float2 (&x)[4]) {
-        if (vec4) {
-            const bool ok = row < rows && col0 < n;
-            const float4* q4 = reinterpret_cast<const float4*>(p + static_cast<long>(min(row, rows - 1)) * n + min(col0, n - 4));
-            const float4 a = q4[0], b = q4[1];
-            x[0] = masked(ok, make_float2(a.x, a.y));
-            x[1] = masked(ok, make_float2(a.z, a.w));
-            x[2] = masked(ok, make_float2(b.x, b.y));
-            x[3] = masked(ok, make_float2(b.z, b.w));
-        } else {
+    const int scol = tid % NB, srow = tid / NB;
+    const int rows_in = min(C, T - t0);             // tokens of this chunk inside the sequence
+    const rsrc_t rS = buf(Srec, static_cast<long>(m) * n * 8), rG = buf(Grec, static_cast<long>(m) * n * 8);
+    const rsrc_t rD = buf(Drow, static_cast<long>(C) * n * 8), rF = buf(Frow, static_cast<long>(C) * n * 8);
+    const rsrc_t rO = buf(gdO + 2 * (base_tn + static_cast<long>(t0) * n), static_cast<long>(rows_in) * n * 2 * sizeof(TOUT));
+    const rsrc_t rV = buf(gv + 2 * (base_tn + static_cast<long>(t0) * n), static_cast<long>(rows_in) * n * 2 * sizeof(TIN));
+    auto fetch = [&](int n0, Raw& x) {
+        const int j = n0 + scol;
+        const bool jok = j < n;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) x[r] = rec(p, row, rows, col0 + r);
+        for (int u = 0; u < NS; ++u) {              // rows past m lie past the resource
+            const uint32_t off = jok ? static_cast<uint32_t>(((srow + RPI * u) * n + j) * 8) : OOR;
+            x.s[u] = ld_c64(rS, off);
+            x.g[u] = ld_c64(rG, off);
         }
-    };
-    auto grad_out4 = [&](int tl, int col0, float2 (&x)[4]) {
-        if (vec4) {
-            const int t = t0 + tl;
-            const bool ok = t < T && col0 < n;
-            const long e = base_tn + static_cast<long>(min(t, T - 1)) * n + min(col0, n - 4);
-            float2 y[4];
-            if constexpr (sizeof(TOUT) == 4) {
-                const float4* q4 = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(gdO) + 2 * e);
-                const float4 a = q4[0], b = q4[1];
-                y[0] = make_float2(a.x, a.y); y[1] = make_float2(a.z, a.w);
-                y[2] = make_float2(b.x, b.y); y[3] = make_float2(b.z, b.w);
-            } else {
-                const uint4 w = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(gdO) + 2 * e);
-                const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    y[r] = make_float2(__uint_as_float(ws[r] << 16), __uint_as_float(ws[r] & 0xFFFF0000u));
-            }
+        for (int u = 0; u < NR; ++u) {              // tokens past T lie past rO
+            const uint32_t e = static_cast<uint32_t>((srow + RPI * u) * n + j);
+            x.d[u] = ld_c64(rD, jok ? e * 8 : OOR);
+            x.f[u] = ld_c64(rF, jok ? e * 8 : OOR);
+            x.r[u] = ld_cplx<TOUT>(rO, jok ? e * 2 * static_cast<uint32_t>(sizeof(TOUT)) : OOR);
+        }
+        const int jv = n0 + wave * 8 + (c >> 1);
+        const bool vok = wave < NB / 8 && jv < n;
+#pragma unroll
+        for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const float2 z = masked(ok, y[r]);
-                x[r] = make_float2(z.x, -z.y);
+                const uint32_t e = static_cast<uint32_t>((rb * 16 + 4 * g + r) * n + jv);
+                const uint32_t off = vok ? e * 2 * static_cast<uint32_t>(sizeof(TIN)) : OOR;
+                if constexpr (P == PREC_BF16) x.v[rb][r] = __builtin_amdgcn_raw_buffer_load_b32(rV, off, 0, 0);
+                else x.v[rb][r] = ld_c64(rV, off);
             }
-        } else {
+    };
+    // put also adds the block's share of dL/dg_C's first part, rowsum(G * conj(S)) from the
+    // fp32 records (one row per NB lanes; lane scol == 0 owns the row's entry of ggc)
+    auto put = [&](const Raw& x, bool first) {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) x[r] = grad_out(tl, col0 + r);
+        for (int u = 0; u < NS; ++u) {
+            const int i = srow + RPI * u;
+            gs.S[i * LD + scol] = RC::pack(x.s[u]);
+            gs.G[i * LD + scol] = RC::pack(x.g[u]);
+            float px = x.g[u].x * x.s[u].x + x.g[u].y * x.s[u].y;
+            float py = x.g[u].y * x.s[u].x - x.g[u].x * x.s[u].y;
+#pragma unroll
+            for (int sh = 1; sh < NB; sh <<= 1) {
+                px += __shfl_xor(px, sh);
+                py += __shfl_xor(py, sh);
+            }
+            if (scol == 0) {
+                gs.ggc[2 * i] = first ? px : gs.ggc[2 * i] + px;
+                gs.ggc[2 * i + 1] = first ? py : gs.ggc[2 * i + 1] + py;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < NR; ++u) {
+            const int tl = srow + RPI * u;
+            gs.D[tl * LD + scol] = RC::pack(x.d[u]);
+            gs.F[tl * LD + scol] = RC::pack(x.f[u]);
+            gs.R[tl * LD + scol] = RC::pack(make_float2(x.r[u].x, -x.r[u].y));
         }
     };
 
+    // ------------------------------------------------------------ load stage, L'
     // (the load stage and the elementwise stage work on the first 256 threads; the latter
     // forms g again rather than holding it in registers through the whole kernel)
+    Raw raw;
     {
-        // every input load of the stage in flight at once: alpha, theta, beta, then q, k
+        // the first record block, then alpha, theta, beta, then q, k
+        fetch(0, raw);
         InPre<C> pf;
         prefetch_inputs<TIN, C, true>(args, bh, t0, tid, pf);
         float2 gkeep[SEG];
         stage_load<TIN, C, false, false, false, ChunkSmem<C>, true, true>(sm, args, bh, t0, tid, gkeep, &pf);
     }
-    // dL/dg_C, first part: sum over columns of G * conj(S), one state row per 8 threads
-    {
-        const int i = tid >> 3, part = tid & 7;
-        float2 acc = make_float2(0.f, 0.f);
-        for (int c0 = 0; c0 < n; c0 += 64) {
-            float2 gs[8], sv[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                gs[u] = rec(Grec, i, m, c0 + part + 8 * u);
-                sv[u] = rec(Srec, i, m, c0 + part + 8 * u);
-            }
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                acc.x += gs[u].x * sv[u].x + gs[u].y * sv[u].y;
-                acc.y += gs[u].y * sv[u].x - gs[u].x * sv[u].y;
-            }
-        }
-#pragma unroll
-        for (int sh = 1; sh < 8; sh <<= 1) {
-            acc.x += __shfl_xor(acc.x, sh);
-            acc.y += __shfl_xor(acc.y, sh);
-        }
-        if (part == 0) {
-            ggc[2 * i] = acc.x;
-            ggc[2 * i + 1] = acc.y;
-        }
-    }
+    put(raw, true);
     __syncthreads();
     stage_gram<P, C, false, false, ChunkSmem<C>, GW>(sm, tid);   // L'
     __syncthreads();
 
-    // ================================================================ H = E - L' Delta, dbeta
-    // (each wave sums its column blocks in registers; the per-wave shares are added in a
-    // fixed order at the end, so no atomics are needed)
+    // ------------------------------------------------------------ value-column blocks
     float dacc[NRB][4];
+    f32x4 gacc[NGA], gki[PER], gqg[PER], gkg[PER];
 #pragma unroll
     for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) dacc[rb][r] = 0.f;
-    for (int cb = wave; cb < ncbn; cb += GW) {
-        const int j = cb * 8 + (c >> 1);
-        Frag8 sbf[MP / 16];                            // S, K = state row
 #pragma unroll
-        for (int kb = 0; kb < MP / 16; ++kb)
+    for (int s = 0; s < NGA; ++s) gacc[s] = zero4();
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float2 y = rec(Srec, kb * 16 + 4 * g + r, m, j);
-                bpair(sbf[kb], r, y.x, y.y, qp);
-            }
-        Frag8 dbf[NRB];                                // Delta, K = token
-#pragma unroll
-        for (int kb = 0; kb < NRB; ++kb)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float2 y = rec(Drow, kb * 16 + 4 * g + r, C, j);
-                bpair(dbf[kb], r, y.x, y.y, qp);
-            }
-        float vpart[NRB][4], fpart[NRB][4];            // this lane's parts of conj(V) and G_F
-#pragma unroll
-        for (int rb = 0; rb < NRB; ++rb)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int tl = rb * 16 + 4 * g + r;
-                const int t = t0 + tl;
-                const bool ok = t < T && j < n;
-                float2 vv = make_float2(0.f, 0.f);
-                if (gv != nullptr)
-                    vv = Elem<TIN>::load2(gv, base_tn + static_cast<long>(min(t, T - 1)) * n + min(j, n - 1));
-                vv = masked(ok, vv);
-                vpart[rb][r] = qp ? -vv.y : vv.x;
-                const float2 f = rec(Frow, tl, C, j);
-                fpart[rb][r] = qp ? f.y : f.x;
-            }
-#pragma unroll
-        for (int rb = 0; rb < NRB; ++rb) {
-            const int row = rb * 16 + c;
-            f32x4 pw = zero4();                        // (conj(K) G) S + L' Delta
+    for (int it = 0; it < PER; ++it) {
+        gki[it] = zero4();
+        gqg[it] = zero4();
+        gkg[it] = zero4();
+    }
+    // causal C x C tile -> (matrix, row block, column block)
+    auto ga_tile = [&](int tile, int& mat, int& rb, int& cb) {
+        mat = tile / NT1;
+        int rem = tile - mat * NT1;
+        rb = 0;
+        while (rem >= min(C / 8, 2 * rb + 2)) { rem -= min(C / 8, 2 * rb + 2); ++rb; }
+        cb = rem;
+    };
+    const int nblk = (n + NB - 1) / NB;
+    for (int blk = 0; blk < nblk; ++blk) {
+        if (blk > 0) {
+            __syncthreads();                           // every read of the previous block done
+            fetch(blk * NB, raw);
+            put(raw, false);
+            __syncthreads();
+        }
+        // H = E - L' Delta and the dbeta shares (Re conj(G_F) H), column block `wave`; each
+        // wave sums in registers, the per-wave shares are added in a fixed order at the end
+        if (wave < NB / 8) {
+            const int jl = wave * 8 + (c >> 1);
+            Op sbf[MP / 16], dbf[NRB];
 #pragma unroll
             for (int kb = 0; kb < MP / 16; ++kb) {
-                Frag8 a;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const float2 x = sm.kg[row * LDX + kb * 16 + 4 * g + r];
-                    a.v[2 * r] = x.x;
-                    a.v[2 * r + 1] = x.y;
-                }
-                mma<P>(pw, a, sbf[kb]);
+                const int i0 = kb * 16 + 4 * g;
+                sbf[kb] = RC::right(gs.S[i0 * LD + jl], gs.S[(i0 + 1) * LD + jl], gs.S[(i0 + 2) * LD + jl],
+                                    gs.S[(i0 + 3) * LD + jl], false, qp);
             }
 #pragma unroll
-            for (int kb = 0; kb <= rb; ++kb) {
-                Frag8 a;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int jt = kb * 16 + 4 * g + r;
-                    const float2 x = masked(jt < row, pin(sm.g2[row * LDG + jt]));
-                    a.v[2 * r] = x.x;
-                    a.v[2 * r + 1] = x.y;
-                }
-                mma<P>(pw, a, dbf[kb]);
+            for (int kb = 0; kb < NRB; ++kb) {
+                const int i0 = kb * 16 + 4 * g;
+                dbf[kb] = RC::right(gs.D[i0 * LD + jl], gs.D[(i0 + 1) * LD + jl], gs.D[(i0 + 2) * LD + jl],
+                                    gs.D[(i0 + 3) * LD + jl], false, qp);
             }
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float h = vpart[rb][r] - pw[r];                  // H, this lane's part
-                float prod = fpart[rb][r] * h;                         // Re(conj(G_F) H) share
-                prod += __shfl_xor(prod, 1);
-                prod += __shfl_xor(prod, 2);
-                prod += __shfl_xor(prod, 4);
-                prod += __shfl_xor(prod, 8);
-                dacc[rb][r] += prod;
+            for (int rb = 0; rb < NRB; ++rb) {
+                const int row = rb * 16 + c;
+                f32x4 pw = zero4();                    // (conj(K) G) S + L' Delta
+#pragma unroll
+                for (int kb = 0; kb < MP / 16; ++kb) {
+                    Frag8 a;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const float2 x = sm.kg[row * LDX + kb * 16 + 4 * g + r];
+                        a.v[2 * r] = x.x;
+                        a.v[2 * r + 1] = x.y;
+                    }
+                    RC::mma(pw, RC::conv(a), sbf[kb]);
+                }
+#pragma unroll
+                for (int kb = 0; kb <= rb; ++kb) {
+                    Frag8 a;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int jt = kb * 16 + 4 * g + r;
+                        const float2 x = masked(jt < row, pin(sm.g2[row * LDG + jt]));
+                        a.v[2 * r] = x.x;
+                        a.v[2 * r + 1] = x.y;
+                    }
+                    RC::mma(pw, RC::conv(a), dbf[kb]);
+                }
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const auto f = gs.F[(rb * 16 + 4 * g + r) * LD + jl];
+                    const auto vw = raw.v[rb][r];
+                    const float h = (qp ? -RC::im(vw) : RC::re(vw)) - pw[r];   // H, this lane's part
+                    float prod = (qp ? RC::im(f) : RC::re(f)) * h;  // Re(conj(G_F) H) share
+                    prod += __shfl_xor(prod, 1);
+                    prod += __shfl_xor(prod, 2);
+                    prod += __shfl_xor(prod, 4);
+                    prod += __shfl_xor(prod, 8);
+                    dacc[rb][r] += prod;
+                }
+            }
+        }
+        // G_A = tril(G_R Delta^*) and G_F Delta^* (G_L' after the loop), over this block
+#pragma unroll
+        for (int s = 0; s < NGA; ++s) {
+            const int tile = wave + GW * s;
+            if (tile >= 2 * NT1) continue;
+            int mat, rb, cb;
+            ga_tile(tile, mat, rb, cb);
+            const int row = rb * 16 + c;
+            const int jcol = cb * 8 + (c >> 1);
+#pragma unroll
+            for (int kb = 0; kb < NB / 16; ++kb) {
+                const int c0 = kb * 16 + 4 * g;
+                const Op a = RC::left(mat ? &gs.R[row * LD + c0] : &gs.F[row * LD + c0], false);
+                RC::mma(gacc[s], a, RC::right4(&gs.D[jcol * LD + c0], true, qp));
+            }
+        }
+        // value-column parts of G_Ki (conj(Delta) G^T), G_Qg (G_R S^*) and G_F S^*
+#pragma unroll
+        for (int it = 0; it < PER; ++it) {
+            const int tile = wave + GW * it;
+            if (tile >= NCT) continue;
+            const int rb = tile / (2 * MP / 16);
+            const int icol = (tile - rb * (2 * MP / 16)) * 8 + (c >> 1);
+            const int row = rb * 16 + c;
+#pragma unroll
+            for (int kb = 0; kb < NB / 16; ++kb) {
+                const int c0 = kb * 16 + 4 * g;
+                RC::mma(gki[it], RC::left(&gs.D[row * LD + c0], true), RC::right4(&gs.G[icol * LD + c0], false, qp));
+                const Op bs = RC::right4(&gs.S[icol * LD + c0], true, qp);
+                RC::mma(gqg[it], RC::left(&gs.R[row * LD + c0], false), bs);
+                RC::mma(gkg[it], RC::left(&gs.F[row * LD + c0], false), bs);
             }
         }
     }
+    __syncthreads();                                   // every read of L' and of the records done
+
+    // ------------------------------------------------------------ C x C gradients, dL/dg_C
     if (c == 0) {
 #pragma unroll
         for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) dbeta_part[wave][rb * 16 + 4 * g + r] = dacc[rb][r];
+            for (int r = 0; r < 4; ++r) gs.dbeta_part[wave][rb * 16 + 4 * g + r] = dacc[rb][r];
     }
-    __syncthreads();                                   // every read of L' done
-
-    // ================================================================ G_A, G_L' (into g2)
+    // G_L' = D_beta strict_tril(-G_F Delta^*) at g2[t][j], G_A^T (upper with the diagonal)
     {
         float* g2f = reinterpret_cast<float*>(sm.g2);
-        for (int tile = wave; tile < 2 * NT1; tile += GW) {
-            const int mat = tile / NT1;                // 0: G_N from G_F, 1: G_A from G_R
-            int rem = tile - mat * NT1, rb = 0;
-            while (rem >= min(C / 8, 2 * rb + 2)) { rem -= min(C / 8, 2 * rb + 2); ++rb; }
-            const int row = rb * 16 + c;
-            const int jcol = rem * 8 + (c >> 1);
-            f32x4 acc = zero4();
-            for (int k0 = 0; k0 < nkb; k0 += 4) {         // all loads of four K-blocks first
-                Frag8 a[4], b[4];
 #pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const int c0 = (k0 + u) * 16 + 4 * g;
-                    float2 x[4], y[4];
-                    if (mat) grad_out4(row, c0, x);
-                    else rec4(Frow, row, C, c0, x);
-                    rec4(Drow, jcol, C, c0, y);                    // Delta^*: conj(Delta[jcol][cc])
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        a[u].v[2 * r] = x[r].x;
-                        a[u].v[2 * r + 1] = x[r].y;
-                        bpair(b[u], r, y[r].x, -y[r].y, qp);
-                    }
-                }
-#pragma unroll
-                for (int u = 0; u < 4; ++u)
-                    if (k0 + u < nkb) mma<P>(acc, a[u], b[u]);
-            }
+        for (int s = 0; s < NGA; ++s) {
+            const int tile = wave + GW * s;
+            if (tile >= 2 * NT1) continue;
+            int mat, rb, cb;
+            ga_tile(tile, mat, rb, cb);
+            const int jcol = cb * 8 + (c >> 1);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int t = rb * 16 + 4 * g + r;
                 if (mat == 0) {
-                    if (jcol < t) g2f[2 * (t * LDG + jcol) + qp] = -sm.beta[t] * acc[r];
+                    if (jcol < t) g2f[2 * (t * LDG + jcol) + qp] = -sm.beta[t] * gacc[s][r];
                 } else {
-                    if (jcol <= t) g2f[2 * (jcol * LDG + t) + qp] = acc[r];
+                    if (jcol <= t) g2f[2 * (jcol * LDG + t) + qp] = gacc[s][r];
                 }
             }
         }
     }
     __syncthreads();
 
-    // ================================================================ G_Ki, G_Qg, G_Kg
+    // ------------------------------------------------------------ G_Ki, G_Qg, G_Kg
     // Tile it of wave w covers channel block (w + 8 it) % 8 = w, so each wave collects the
-    // dL/dg_C shares of its channel block in gsum.  The three products run one after another,
-    // each holding only its own operands in registers.
-    constexpr int PER = (NCT + GW - 1) / GW;
-    f32x4 gki[PER], gqg[PER], gkg[PER];
+    // dL/dg_C shares of its channel block in gsum.
     float gsum = 0.f;
-    // left operand rows (K = value column): 0 conj(Delta), 1 G_R, 2 -G_E = -beta G_F
-    auto left4 = [&](int kind, int row, int c0, Frag8& a) {
-        float2 x[4];
-        if (kind == 0) rec4(Drow, row, C, c0, x);
-        else if (kind == 1) grad_out4(row, c0, x);
-        else rec4(Frow, row, C, c0, x);
-        const float sc = kind == 2 ? -sm.beta[min(row, C - 1)] : 1.f;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            a.v[2 * r] = sc * x[r].x;
-            a.v[2 * r + 1] = kind == 0 ? -x[r].y : sc * x[r].y;
-        }
-    };
-    // right operand (K = value column, output column icol): 0 G^T, 1 S^*
-    auto right4 = [&](int kind, int icol, int c0, Frag8& b) {
-        float2 y[4];
-        rec4(kind == 0 ? Grec : Srec, icol, m, c0, y);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) bpair(b, r, y[r].x, kind == 0 ? y[r].y : -y[r].y, qp);
-    };
-    // acc += (left kind lk) (right kind rk) over the value columns, two K-blocks of loads at a time
-    auto value_product = [&](f32x4& acc, int lk, int rk, int row, int icol) {
-        for (int k0 = 0; k0 < nkb; k0 += 2) {
-            Frag8 a[2], b[2];
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                left4(lk, row, (k0 + u) * 16 + 4 * g, a[u]);
-                right4(rk, icol, (k0 + u) * 16 + 4 * g, b[u]);
-            }
-#pragma unroll
-            for (int u = 0; u < 2; ++u)
-                if (k0 + u < nkb) mma<P>(acc, a[u], b[u]);
-        }
-    };
     // a C x C operand fragment from g2: G_L' (strict lower at g2[t][j]) or G_A (lower, at g2[j][t])
-    auto cc_frag = [&](bool transposed_store, int row, int kb, int lo, Frag8& a) {
+    auto cc_frag = [&](bool transposed_store, int row, int kb, int lo) {
         // lo: 0 -> jt < row, 1 -> jt <= row, 2 -> jt > row, 3 -> jt >= row
+        Frag8 a;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int jt = kb * 16 + 4 * g + r;
@@ -357,25 +477,25 @@ __global__ __launch_bounds__(GW * 64, C <= 32 ? 4 : 2) void grad_kernel(GradArgs
             a.v[2 * r] = x.x;
             a.v[2 * r + 1] = x.y;
         }
+        return RC::conv(a);
     };
-    auto lds_right = [&](const float2* X, int kb, int icol, Frag8& b) {   // conj(X[jt][icol])
+    auto lds_right = [&](const float2* X, int kb, int icol) {   // conj(X[jt][icol])
+        Frag8 b;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const float2 y = X[(kb * 16 + 4 * g + r) * LDX + icol];
             bpair(b, r, y.x, -y.y, qp);
         }
+        return RC::conv(b);
     };
-    // G_Ki = conj(Delta) G^T diag(conj(g_C)) + G_L'^T conj(conj(K)G) + G_A^T conj(conj(Q)G)
 #pragma unroll
     for (int it = 0; it < PER; ++it) {
         const int tile = wave + GW * it;
-        gki[it] = zero4();
         if (tile >= NCT) continue;
         const int rb = tile / (2 * MP / 16);
         const int icol = (tile - rb * (2 * MP / 16)) * 8 + (c >> 1);
         const int row = rb * 16 + c;
-        value_product(gki[it], 0, 0, row, icol);
-        // dL/dg_C, second part: column sums of G_Yp * conj(K/G)
+        // dL/dg_C, second part: column sums of G_Yp * conj(K/G) (G_Yp = conj(Delta) G^T)
         {
             float part = 0.f;
 #pragma unroll
@@ -397,43 +517,26 @@ __global__ __launch_bounds__(GW * 64, C <= 32 ? 4 : 2) void grad_kernel(GradArgs
                 gki[it][r] = qp ? (gg.x * own - gg.y * oth) : (gg.x * own + gg.y * oth);
             }
         }
+        // G_Kg's value part is -G_E S^* = -D_beta (G_F S^*)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) gkg[it][r] *= -sm.beta[rb * 16 + 4 * g + r];
+        // + G_L'^T conj(conj(K)G) + G_A^T conj(conj(Q)G)
 #pragma unroll
         for (int kb = rb; kb < NRB; ++kb) {
-            Frag8 a, b;
-            cc_frag(true, row, kb, 2, a);              // G_L'^T[row][jt] = G_L'[jt][row], jt > row
-            lds_right(sm.kg, kb, icol, b);
-            mma<P>(gki[it], a, b);
-            cc_frag(false, row, kb, 3, a);             // G_A^T[row][jt] = G_A[jt][row], jt >= row
-            lds_right(sm.qg, kb, icol, b);
-            mma<P>(gki[it], a, b);
+            RC::mma(gki[it], cc_frag(true, row, kb, 2), lds_right(sm.kg, kb, icol));    // G_L'[jt][row], jt > row
+            RC::mma(gki[it], cc_frag(false, row, kb, 3), lds_right(sm.qg, kb, icol));   // G_A[jt][row], jt >= row
         }
-    }
-    // G_Qg = G_R S^* + G_A conj(K/G),  G_Kg = -G_E S^* + G_L' conj(K/G)
+        // G_Qg += G_A conj(K/G),  G_Kg += G_L' conj(K/G)
 #pragma unroll
-    for (int pass = 0; pass < 2; ++pass) {
-#pragma unroll
-        for (int it = 0; it < PER; ++it) {
-            const int tile = wave + GW * it;
-            f32x4& acc = pass == 0 ? gqg[it] : gkg[it];
-            acc = zero4();
-            if (tile >= NCT) continue;
-            const int rb = tile / (2 * MP / 16);
-            const int icol = (tile - rb * (2 * MP / 16)) * 8 + (c >> 1);
-            const int row = rb * 16 + c;
-            value_product(acc, pass == 0 ? 1 : 2, 1, row, icol);
-#pragma unroll
-            for (int kb = 0; kb <= rb; ++kb) {
-                Frag8 a, b;
-                if (pass == 0) cc_frag(true, row, kb, 1, a);    // G_A[row][jt], jt <= row
-                else cc_frag(false, row, kb, 0, a);             // G_L'[row][jt], jt < row
-                lds_right(sm.ki, kb, icol, b);
-                mma<P>(acc, a, b);
-            }
+        for (int kb = 0; kb <= rb; ++kb) {
+            const Op b = lds_right(sm.ki, kb, icol);
+            RC::mma(gqg[it], cc_frag(true, row, kb, 1), b);                             // G_A[row][jt], jt <= row
+            RC::mma(gkg[it], cc_frag(false, row, kb, 0), b);                            // G_L'[row][jt], jt < row
         }
     }
     if (g == 0) {                                      // one owner lane per element of ggc
         const int icol = wave * 8 + (c >> 1);
-        if (icol < m) ggc[2 * icol + qp] += gsum;
+        if (icol < m) gs.ggc[2 * icol + qp] += gsum;
     }
     __syncthreads();                                   // every read of qg, kg, ki done
     {
@@ -457,33 +560,49 @@ __global__ __launch_bounds__(GW * 64, C <= 32 ? 4 : 2) void grad_kernel(GradArgs
     }
     __syncthreads();
 
-    // ================================================================ elementwise, suffix sums
+    // ------------------------------------------------------------ elementwise, suffix sums
     {
         const TIN* gq = static_cast<const TIN*>(args.q);
         const TIN* gk = static_cast<const TIN*>(args.k);
         const TIN* ga = static_cast<const TIN*>(args.alpha);
+        const TIN* gth = static_cast<const TIN*>(args.theta);
         TIN* dq = static_cast<TIN*>(A.dq);
         TIN* dk = static_cast<TIN*>(A.dk);
         TIN* dal = static_cast<TIN*>(A.dalpha);
         TIN* dth = static_cast<TIN*>(A.dtheta);
         const int i = tid & 63, seg = (tid >> 6) & 3;
         const bool worker = tid < NTHR;                // the load stage's thread mapping
+        // every load of the stage at once: alpha, theta, q, k of this thread's tokens (zero
+        // past T and past m)
+        float av[SEG], la[SEG], ph[SEG];
+        float2 qq[SEG], kk[SEG];
+        {
+            const long e0 = base_tm + static_cast<long>(t0) * m;
+            const long bytes = static_cast<long>(rows_in) * m * sizeof(TIN);
+            const rsrc_t ra = buf(ga + e0, bytes), rt = buf(gth + e0, bytes);
+            const rsrc_t rq = buf(gq + 2 * e0, 2 * bytes), rk = buf(gk + 2 * e0, 2 * bytes);
+#pragma unroll
+            for (int u = 0; u < SEG; ++u) {
+                const uint32_t e = static_cast<uint32_t>((seg * SEG + u) * m + i);
+                const uint32_t o1 = i < m ? e * static_cast<uint32_t>(sizeof(TIN)) : OOR;
+                const uint32_t o2 = i < m ? 2 * e * static_cast<uint32_t>(sizeof(TIN)) : OOR;
+                av[u] = ld_real<TIN>(ra, o1);
+                ph[u] = ld_real<TIN>(rt, o1);
+                qq[u] = ld_cplx<TIN>(rq, o2);
+                kk[u] = ld_cplx<TIN>(rk, o2);
+            }
+        }
         // g of this thread's tokens: running sums of log alpha and theta over its segment,
-        // offset by the segments before it
+        // offset by the segments before it (padding is the identity token: alpha read as 0
+        // there counts as 1)
         float2 gkeep[SEG];
         {
-            const TIN* gth = static_cast<const TIN*>(args.theta);
-            float la[SEG], ph[SEG];
             float sa = 0.f, sp2 = 0.f;
 #pragma unroll
             for (int u = 0; u < SEG; ++u) {
-                const int t = t0 + seg * SEG + u;
-                const bool ok = t < T && i < m;
-                const long e = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
-                const float a_ld = pin(Elem<TIN>::load(ga, e));
-                const float th = masked(ok, Elem<TIN>::load(gth, e));
-                sa += __logf(ok ? a_ld : 1.f);
-                sp2 += th;
+                const bool ok = t0 + seg * SEG + u < T && i < m;
+                sa += __logf(av[u] + (ok ? 0.f : 1.f));
+                sp2 += ph[u];
                 la[u] = sa;
                 ph[u] = sp2;
             }
@@ -515,8 +634,6 @@ __global__ __launch_bounds__(GW * 64, C <= 32 ? 4 : 2) void grad_kernel(GradArgs
             const int t = t0 + tl;
             const bool ok = t < T && i < m;
             const long e = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
-            const float2 qq = masked(ok, Elem<TIN>::load2(gq, e));
-            const float2 kk = masked(ok, Elem<TIN>::load2(gk, e));
             const float2 gqv = sm.kg[tl * LDX + i], gkv = sm.ki[tl * LDX + i], gkiv = sm.qg[tl * LDX + i];
             const float2 gg = gkeep[u];
             const float inv2 = 1.f / (gg.x * gg.x + gg.y * gg.y);
@@ -530,15 +647,16 @@ __global__ __launch_bounds__(GW * 64, C <= 32 ? 4 : 2) void grad_kernel(GradArgs
                 Elem<TIN>::store2(dk, e, vk.x, vk.y);
             }
             // dL/dg = q G_Qg + k G_Kg - conj(k / g^2) G_Ki
-            const float2 kg2 = make_float2(kk.x * gi.x - kk.y * gi.y, kk.x * gi.y + kk.y * gi.x);     // k / g
+            const float2 q1 = qq[u], k1 = kk[u];
+            const float2 kg2 = make_float2(k1.x * gi.x - k1.y * gi.y, k1.x * gi.y + k1.y * gi.x);     // k / g
             const float2 kg3 = make_float2(kg2.x * gi.x - kg2.y * gi.y, kg2.x * gi.y + kg2.y * gi.x); // k / g^2
-            float2 dg = make_float2(qq.x * gqv.x - qq.y * gqv.y + kk.x * gkv.x - kk.y * gkv.y
+            float2 dg = make_float2(q1.x * gqv.x - q1.y * gqv.y + k1.x * gkv.x - k1.y * gkv.y
                                         - (kg3.x * gkiv.x + kg3.y * gkiv.y),
-                                    qq.x * gqv.y + qq.y * gqv.x + kk.x * gkv.y + kk.y * gkv.x
+                                    q1.x * gqv.y + q1.y * gqv.x + k1.x * gkv.y + k1.y * gkv.x
                                         - (kg3.x * gkiv.y - kg3.y * gkiv.x));
             if (tl == C - 1 && i < m) {
-                dg.x += ggc[2 * i];
-                dg.y += ggc[2 * i + 1];
+                dg.x += gs.ggc[2 * i];
+                dg.y += gs.ggc[2 * i + 1];
             }
             // dL/dz = conj(g) dL/dg, suffix sums over the chunk
             sl += gg.x * dg.x + gg.y * dg.y;
@@ -562,14 +680,14 @@ __global__ __launch_bounds__(GW * 64, C <= 32 ? 4 : 2) void grad_kernel(GradArgs
             const int t = t0 + seg * SEG + u;
             if (t < T && i < m) {
                 const long e = base_tm + static_cast<long>(t) * m + i;
-                Elem<TIN>::store(dal, e, (gl[u] + ol) / Elem<TIN>::load(ga, e));
+                Elem<TIN>::store(dal, e, (gl[u] + ol) / av[u]);
                 Elem<TIN>::store(dth, e, gp[u] + op);
             }
         }
         if (tid < C && t0 + tid < T) {
             float db = 0.f;
 #pragma unroll
-            for (int w = 0; w < GW; ++w) db += dbeta_part[w][tid];
+            for (int w = 0; w < GW; ++w) db += gs.dbeta_part[w][tid];
             Elem<TIN>::store(static_cast<TIN*>(A.dbeta), bh * static_cast<long>(T) + t0 + tid, db);
         }
     }
@@ -591,7 +709,6 @@ static hipError_t launch_grad_t(const GradLaunch& L, hipStream_t st)
     switch (L.C) {
         case 16: hipLaunchKernelGGL((grad_kernel<P, TIN, TOUT, 16>), grid, dim3(GW * 64), 0, st, a); break;
         case 32: hipLaunchKernelGGL((grad_kernel<P, TIN, TOUT, 32>), grid, dim3(GW * 64), 0, st, a); break;
-        case 64: hipLaunchKernelGGL((grad_kernel<P, TIN, TOUT, 64>), grid, dim3(GW * 64), 0, st, a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
