@@ -46,6 +46,9 @@ const char* sfda_status_string(sfda_status_t s)
 
 int sfda_abi_version(void) { return SFDA_ABI_VERSION; }
 
+// one head's state (m x n complex float32) is addressed with 32-bit byte offsets
+static bool state_fits(int m, int n) { return static_cast<long>(m) * n * 8 < 0x80000000L; }
+
 static sfda_status_t chunk_fwd_impl(const void* q, const void* k, const void* v,
                                     const void* alpha, const void* theta, const void* beta,
                                     const float* S0, void* o, float* S_T, int B, int H, int T,
@@ -55,7 +58,7 @@ static sfda_status_t chunk_fwd_impl(const void* q, const void* k, const void* v,
                                     const sfda::GateParams* gates = nullptr)
 {
     if (!dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return SFDA_ERR_DTYPE;
-    if (B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1) return SFDA_ERR_SHAPE;
+    if (B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1 || !state_fits(m, n)) return SFDA_ERR_SHAPE;
     if (C != 16 && C != 32 && C != 64) return SFDA_ERR_CHUNK;
     if (slice < 8 || slice > 64 || (slice & 7) != 0) return SFDA_ERR_SHAPE;
     const long BH = static_cast<long>(B) * H;
@@ -200,7 +203,7 @@ sfda_status_t sfda_chunk_fwd_segmented(const void* q, const void* k, const void*
     const int slice_n = n <= 64 ? ((n + 7) / 8) * 8 : 64;
     // the shared checks (and the whole call when there is nothing to split)
     if (T == 0 || static_cast<long>(B) * H == 0 || !dtype_ok(in_dtype) || !dtype_ok(out_dtype) ||
-        B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1 || (C != 16 && C != 32 && C != 64))
+        B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1 || !state_fits(m, n) || (C != 16 && C != 32 && C != 64))
         return chunk_fwd_impl(q, k, v, alpha, theta, beta, S0, o, S_T, B, H, T, m, n, C, in_dtype,
                               out_dtype, stream, slice_n);
     if (T % (static_cast<long>(G) * C) != 0) return SFDA_ERR_SHAPE;
@@ -277,7 +280,7 @@ sfda_status_t sfda_chunk_bwd(const void* q, const void* k, const void* v, const 
                              sfda_stream_t stream)
 {
     if (!dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return SFDA_ERR_DTYPE;
-    if (B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1) return SFDA_ERR_SHAPE;
+    if (B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1 || !state_fits(m, n)) return SFDA_ERR_SHAPE;
     if (C != 16 && C != 32 && C != 64) return SFDA_ERR_CHUNK;
     const size_t need = sfda_chunk_bwd_workspace_bytes(B, H, T, m, n, C);
     C = bwd_chunk(C);
@@ -349,7 +352,7 @@ sfda_status_t sfda_step(const void* q, const void* k, const void* v, const void*
                         sfda_stream_t stream)
 {
     if (!dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return SFDA_ERR_DTYPE;
-    if (B < 0 || H < 0 || m < 1 || m > 64 || n < 1) return SFDA_ERR_SHAPE;
+    if (B < 0 || H < 0 || m < 1 || m > 64 || n < 1 || !state_fits(m, n)) return SFDA_ERR_SHAPE;
     if (n >= (1 << 22)) return SFDA_ERR_SHAPE;   // state rows addressed with 32-bit offsets
     const long BH = static_cast<long>(B) * H;
     int np = 1;

@@ -69,16 +69,19 @@ __device__ __forceinline__ void adjoint_chunk(ChunkSmem<C>& sm, const ChunkArgs&
         if (cb >= ncb) continue;
         const int j = n0 + cb * 8 + (c >> 1);
         Frag8 br[NRB];                   // G_R = conj(dL/do), K = token
+        {
+            // tokens past T lie past the chunk's rows
+            const rsrc_t ro = buf(static_cast<const TOUT*>(args.dO) + 2 * (base_tn + static_cast<long>(t0) * n),
+                                  static_cast<long>(min(C, T - t0)) * n * 2 * sizeof(TOUT));
 #pragma unroll
-        for (int kb = 0; kb < NRB; ++kb)
+            for (int kb = 0; kb < NRB; ++kb)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int t = t0 + kb * 16 + 4 * g + r;
-                const bool ok = j < n && t < T;
-                const float2 x = masked(ok, Elem<TOUT>::load2(static_cast<const TOUT*>(args.dO),
-                                                              base_tn + static_cast<long>(min(t, T - 1)) * n + min(j, n - 1)));
-                bpair(br[kb], r, x.x, -x.y, qp);
-            }
+                for (int r = 0; r < 4; ++r) {
+                    const int tl = kb * 16 + 4 * g + r;
+                    const float2 x = ld_cplx<TOUT>(ro, j < n ? static_cast<uint32_t>((tl * n + j) * 2 * sizeof(TOUT)) : OOR);
+                    bpair(br[kb], r, x.x, -x.y, qp);
+                }
+        }
         Frag8 sb[MP / 16];
 #pragma unroll
         for (int kb = 0; kb < MP / 16; ++kb) sb[kb] = bfrag_from_acc(Sacc[w][kb], qp);
@@ -224,22 +227,21 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
     // ---------------------------------------------------------------- state in registers
     // (MODE 2: the adjoint of the state, starting from dL/dS_T)
     f32x4 Sacc[CBW][MP / 16];
+    {
+        // S0 == NULL: an empty resource, every read is zero; rows past m lie past the head's block
+        const rsrc_t rs = buf(args.S0 ? args.S0 + 2 * base_mn : args.S0, args.S0 ? static_cast<long>(m) * n * 8 : 0);
 #pragma unroll
-    for (int w = 0; w < CBW; ++w) {
-        const int cb = wave + NW * w;
-        const int j = n0 + cb * 8 + (c >> 1);
+        for (int w = 0; w < CBW; ++w) {
+            const int cb = wave + NW * w;
+            const int j = n0 + cb * 8 + (c >> 1);
+            const bool jok = cb < ncb && j < n;
 #pragma unroll
-        for (int kb = 0; kb < MP / 16; ++kb) {
+            for (int kb = 0; kb < MP / 16; ++kb)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int i = kb * 16 + 4 * g + r;
-                float x = 0.f;
-                if (args.S0 != nullptr) {   // uniform branch; the load itself is unconditional
-                    const bool ok = cb < ncb && j < n && i < m;
-                    x = masked(ok, args.S0[2 * (base_mn + static_cast<long>(min(i, m - 1)) * n + min(j, n - 1)) + qp]);
+                for (int r = 0; r < 4; ++r) {
+                    const int i = kb * 16 + 4 * g + r;
+                    Sacc[w][kb][r] = ld_f32(rs, jok ? static_cast<uint32_t>(((i * n + j) * 2 + qp) * 4) : OOR);
                 }
-                Sacc[w][kb][r] = x;
-            }
         }
     }
 
@@ -275,20 +277,20 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
         // (the adjoint scan loads its dL/do fragments itself, where they are used)
         float2 vf[CBW][NRB][4];
         if constexpr (MODE != 2) {
+            // v == NULL: an empty resource (zeros); tokens past T lie past the chunk's rows
+            const long vbytes = gv ? static_cast<long>(min(C, T - t0)) * n * 2 * sizeof(TIN) : 0;
+            const rsrc_t rv = buf(gv ? gv + 2 * (base_tn + static_cast<long>(t0) * n) : gv, vbytes);
 #pragma unroll
             for (int w = 0; w < CBW; ++w) {
                 const int cb = wave + NW * w;
                 const int j = n0 + cb * 8 + (c >> 1);
+                const bool jok = cb < ncb && j < n;
 #pragma unroll
                 for (int kb = 0; kb < NRB; ++kb)
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
-                        const int t = t0 + kb * 16 + 4 * g + r;
-                        const bool ok = cb < ncb && j < n && t < T;
-                        float2 x = make_float2(0.f, 0.f);
-                        if (gv != nullptr)      // v == NULL reads as zeros (uniform branch)
-                            x = Elem<TIN>::load2(gv, base_tn + static_cast<long>(min(t, T - 1)) * n + min(j, n - 1));
-                        vf[w][kb][r] = masked(ok, x);
+                        const int tl = kb * 16 + 4 * g + r;
+                        vf[w][kb][r] = ld_cplx<TIN>(rv, jok ? static_cast<uint32_t>((tl * n + j) * 2 * sizeof(TIN)) : OOR);
                     }
             }
         }

@@ -115,6 +115,12 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
 
     const int i = tid & 63;
     const int seg = (tid >> 6) & 3;
+    // (without PRE: alpha, theta, q, k through resources over this chunk's rows)
+    const long rbytes = static_cast<long>(min(T - t0, C)) * m * sizeof(TIN);
+    const rsrc_t ra = buf(ga + base_tm + static_cast<long>(t0) * m, rbytes);
+    const rsrc_t rt = buf(gth + base_tm + static_cast<long>(t0) * m, rbytes);
+    const rsrc_t rq = buf(gq + 2 * (base_tm + static_cast<long>(t0) * m), 2 * rbytes);
+    const rsrc_t rk = buf(gk + 2 * (base_tm + static_cast<long>(t0) * m), 2 * rbytes);
     float la[SEG], ph[SEG];
     float sa = 0.f, sp = 0.f;
     float2 qpre[PRE ? SEG : 1], kpre[PRE ? SEG : 1];
@@ -136,14 +142,18 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
         const bool ok = t < T && i < m;
         const long e = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
         float a_ld, th;
+        float a;
         if constexpr (PRE) {
             a_ld = pin(pre->a[u]);
             th = masked(ok, pre->th[u]);
+            a = ok ? a_ld : 1.f;
         } else {
-            a_ld = pin(Elem<TIN>::load(ga, e));
-            th = masked(ok, Elem<TIN>::load(gth, e));
+            // buffer reads, zero past T and past m: no pin, so they issue back to back
+            const uint32_t off = i < m ? static_cast<uint32_t>((t - t0) * m + i) * static_cast<uint32_t>(sizeof(TIN)) : OOR;
+            a_ld = ld_real<TIN>(ra, off);
+            th = ld_real<TIN>(rt, off);
+            a = a_ld + (ok ? 0.f : 1.f);          // the identity token's alpha is 1
         }
-        float a = ok ? a_ld : 1.f;
         if constexpr (GATED) {      // padding stays the identity token (alpha = 1, theta = 0)
             a = ok ? args.amin + args.aspan * sigmoid_acc(a_ld) : 1.f;
             th = ok ? args.tmax * tanhf(th) : 0.f;
@@ -192,14 +202,13 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
         const long e2 = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
         float2 qq, kk;
         if constexpr (PRE) {
-            qq = qpre[u];
-            kk = kpre[u];
-        } else {
-            qq = Elem<TIN>::load2(gq, e2);
-            kk = Elem<TIN>::load2(gk, e2);
+            qq = masked(ok, qpre[u]);
+            kk = masked(ok, kpre[u]);
+        } else {                                     // zero past T and past m
+            const uint32_t off = i < m ? static_cast<uint32_t>(tl * m + i) * static_cast<uint32_t>(2 * sizeof(TIN)) : OOR;
+            qq = ld_cplx<TIN>(rq, off);
+            kk = ld_cplx<TIN>(rk, off);
         }
-        qq = masked(ok, qq);
-        kk = masked(ok, kk);
         if constexpr (GATED) {
             // 1 / (||k~_t|| + eps): the wave holds channel i = lane of token t
             float s2 = kk.x * kk.x + kk.y * kk.y;

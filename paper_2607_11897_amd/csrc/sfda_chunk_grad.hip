@@ -58,32 +58,6 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 struct FragW { u32x4 w; };   // a lane's 8 bf16 operand values as 4 packed pairs
 
-// Global reads of the stage go through buffer resources: a read past the resource's size
-// returns zero, so padding rows need no mask, and a lane outside the valid columns passes an
-// offset past every resource.  No select follows a load, so the loads of a stage issue back
-// to back and are waited on once.
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-constexpr uint32_t OOR = 0x80000000u;
-__device__ __forceinline__ rsrc_t buf(const void* base, long bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes), 0x00020000);
-}
-__device__ __forceinline__ float2 ld_c64(rsrc_t r, uint32_t off) {      // complex float32
-    return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
-}
-template <typename T> __device__ __forceinline__ float2 ld_cplx(rsrc_t r, uint32_t off);
-template <> __device__ __forceinline__ float2 ld_cplx<float>(rsrc_t r, uint32_t off) { return ld_c64(r, off); }
-template <> __device__ __forceinline__ float2 ld_cplx<uint16_t>(rsrc_t r, uint32_t off) {
-    const uint32_t w = __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
-    return make_float2(__uint_as_float(w << 16), __uint_as_float(w & 0xFFFF0000u));
-}
-template <typename T> __device__ __forceinline__ float ld_real(rsrc_t r, uint32_t off);
-template <> __device__ __forceinline__ float ld_real<float>(rsrc_t r, uint32_t off) {
-    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
-}
-template <> __device__ __forceinline__ float ld_real<uint16_t>(rsrc_t r, uint32_t off) {
-    return __uint_as_float(static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0)) << 16);
-}
-
 template <int P> struct Rec;
 
 template <> struct Rec<PREC_BF16> {
