@@ -93,36 +93,6 @@ __device__ __forceinline__ float2 masked(bool ok, float2 x) {
     return ok ? x : make_float2(0.f, 0.f);
 }
 
-// ----------------------------------------------------------------- buffer loads
-
-// Reads through a buffer resource: a read past the resource's size returns zero, so rows
-// past the end of a sequence or a block need no mask, and a lane outside the valid columns
-// passes an offset past every resource (OOR).  No select follows such a load, so the loads
-// of a stage issue back to back and are waited on once (a masked load, whose value is
-// pinned before the select, waits right after it is issued).
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-constexpr uint32_t OOR = 0x80000000u;
-__device__ __forceinline__ rsrc_t buf(const void* base, long bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes), 0x00020000);
-}
-__device__ __forceinline__ float2 ld_c64(rsrc_t r, uint32_t off) {      // complex float32
-    return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
-}
-__device__ __forceinline__ float ld_f32(rsrc_t r, uint32_t off) {
-    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
-}
-template <typename T> __device__ __forceinline__ float2 ld_cplx(rsrc_t r, uint32_t off);
-template <> __device__ __forceinline__ float2 ld_cplx<float>(rsrc_t r, uint32_t off) { return ld_c64(r, off); }
-template <> __device__ __forceinline__ float2 ld_cplx<uint16_t>(rsrc_t r, uint32_t off) {
-    const uint32_t w = __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
-    return make_float2(__uint_as_float(w << 16), __uint_as_float(w & 0xFFFF0000u));
-}
-template <typename T> __device__ __forceinline__ float ld_real(rsrc_t r, uint32_t off);
-template <> __device__ __forceinline__ float ld_real<float>(rsrc_t r, uint32_t off) { return ld_f32(r, off); }
-template <> __device__ __forceinline__ float ld_real<uint16_t>(rsrc_t r, uint32_t off) {
-    return __uint_as_float(static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0)) << 16);
-}
-
 // ----------------------------------------------------------------- lane exchange
 
 // Value of lane l ^ 1 (DPP quad permutation [1, 0, 3, 2]).
