@@ -35,10 +35,41 @@
 // state entering each chunk and Delta; MODE 2 walks the chunks in reverse carrying dL/dS
 // (the adjoint of the chunk map, adjoint_chunk below) and records it with G_F.
 #include <type_traits>
+#include <utility>
 
 #include "sfda_chunk_common.h"
 
 namespace sfda {
+
+// ---------------------------------------------------------------- 16 x 16 inverses
+// N = (I - X)^{-1} for X strictly lower triangular (X = -(D_beta L') on a diagonal block),
+// i.e. N = I + X N, by forward substitution over the pivots s = 0 .. 14.  Lane (i, cg) --
+// i = lane % 16, cg = lane / 16 -- holds row i of X and row i, columns cg, cg + 4, cg + 8,
+// cg + 12 of N (slot k holds column 4k + cg); the pivot row N(s, .) is lane s of the lane's
+// own 16-lane row (a DPP row broadcast).  N is lower triangular, so the pivot row is zero
+// past column s and slot k takes part only in the steps s >= 4k.
+template <int K>
+__device__ __forceinline__ float row_bcast(float x) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x150 + K, 0xF, 0xF, false));
+}
+template <int S>
+__device__ __forceinline__ void subst_step(float (&nr)[4], float (&ni)[4], const float2 (&xrow)[16])
+{
+    const float xr = xrow[S].x, xi = xrow[S].y;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        if (4 * k > S) continue;
+        const float pr = row_bcast<S>(nr[k]), pi = row_bcast<S>(ni[k]);
+        nr[k] = __builtin_fmaf(xr, pr, __builtin_fmaf(-xi, pi, nr[k]));
+        ni[k] = __builtin_fmaf(xr, pi, __builtin_fmaf(xi, pr, ni[k]));
+    }
+}
+template <int... S>
+__device__ __forceinline__ void subst_steps(float (&nr)[4], float (&ni)[4], const float2 (&xrow)[16],
+                                            std::integer_sequence<int, S...>)
+{
+    (subst_step<S>(nr, ni, xrow), ...);
+}
 
 // ---------------------------------------------------------------- adjoint scan (MODE 2)
 // The reverse-mode sweep over the chunks for dL/dS (the backward of the chunk map): with
@@ -310,29 +341,23 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
 
         // ============================================================ S: N = (I + D_beta L')^{-1}
         if (wave < NRB) {
-            // diagonal block p = wave; lane jj owns column jj of N_pp
-            const int p = wave;
-            const int jj = lane & 15;
-            float2 nv[16];
+            // diagonal block p = wave (the substitution above): lane (i, cg) reads row i of
+            // L' and writes row i of N over it (one wave's LDS accesses run in order)
+            const int p = wave, i = lane & 15, cg = lane >> 4;
+            const float bi = sm.beta[p * 16 + i];
+            float2 xrow[16];
 #pragma unroll
-            for (int r = 0; r < 16; ++r) nv[r] = make_float2(r == jj ? 1.f : 0.f, 0.f);
-#pragma unroll
-            for (int r = 1; r < 16; ++r) {
-                float2 s = make_float2(0.f, 0.f);
-#pragma unroll
-                for (int s2 = 0; s2 < r; ++s2) {
-                    const float2 l = sm.g2[(p * 16 + r) * LDG + p * 16 + s2];
-                    s.x += l.x * nv[s2].x - l.y * nv[s2].y;
-                    s.y += l.x * nv[s2].y + l.y * nv[s2].x;
-                }
-                const float bt = sm.beta[p * 16 + r];
-                if (r > jj) nv[r] = make_float2(-bt * s.x, -bt * s.y);
+            for (int s2 = 0; s2 < 16; ++s2) {
+                const float2 l = sm.g2[(p * 16 + i) * LDG + p * 16 + s2];
+                xrow[s2] = s2 < i ? make_float2(-bi * l.x, -bi * l.y) : make_float2(0.f, 0.f);
             }
-            if (lane < 16) {
+            float nr[4], ni[4];
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    if (r > jj) sm.g2[(p * 16 + r) * LDG + p * 16 + jj] = nv[r];
-            }
+            for (int k = 0; k < 4; ++k) { nr[k] = i == 4 * k + cg ? 1.f : 0.f; ni[k] = 0.f; }
+            subst_steps(nr, ni, xrow, std::make_integer_sequence<int, 15>{});
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                if (4 * k + cg < i) sm.g2[(p * 16 + i) * LDG + p * 16 + 4 * k + cg] = make_float2(nr[k], ni[k]);
         }
         __syncthreads();
         // off-diagonal blocks, block row by block row:
