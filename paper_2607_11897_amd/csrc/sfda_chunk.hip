@@ -71,6 +71,19 @@ __device__ __forceinline__ void subst_steps(float (&nr)[4], float (&ni)[4], cons
     (subst_step<S>(nr, ni, xrow), ...);
 }
 
+// a complex element as loaded (bf16 pair word or fp32 pair), converted where it is used
+template <typename T> struct RawC;
+template <> struct RawC<uint16_t> {
+    using W = uint32_t;
+    static __device__ __forceinline__ W load(rsrc_t r, uint32_t off) { return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0); }
+    static __device__ __forceinline__ float2 get(W w) { return make_float2(__uint_as_float(w << 16), __uint_as_float(w & 0xFFFF0000u)); }
+};
+template <> struct RawC<float> {
+    using W = float2;
+    static __device__ __forceinline__ W load(rsrc_t r, uint32_t off) { return ld_c64(r, off); }
+    static __device__ __forceinline__ float2 get(W w) { return w; }
+};
+
 // ---------------------------------------------------------------- adjoint scan (MODE 2)
 // The reverse-mode sweep over the chunks for dL/dS (the backward of the chunk map): with
 // G = dL/dS_out of this chunk and G_R = conj(dL/do) the adjoint of O^*, the chunk relations
@@ -85,7 +98,8 @@ __device__ __forceinline__ void subst_steps(float (&nr)[4], float (&ni)[4], cons
 template <int P, typename TIN, typename TOUT, int C, int NW>
 __device__ __forceinline__ void adjoint_chunk(ChunkSmem<C>& sm, const ChunkArgs& args,
                                               f32x4 (&Sacc)[8 / NW][MP / 16], long bh, int t0,
-                                              int nchunks, int n0, int ncb, int tid)
+                                              int nchunks, int n0, int ncb, int tid,
+                                              const typename RawC<TOUT>::W (&dor)[8 / NW][C / 16][4])
 {
     constexpr int NRB = C / 16;
     constexpr int LDG = ChunkSmem<C>::LDG;
@@ -99,20 +113,14 @@ __device__ __forceinline__ void adjoint_chunk(ChunkSmem<C>& sm, const ChunkArgs&
         const int cb = wave + NW * w;
         if (cb >= ncb) continue;
         const int j = n0 + cb * 8 + (c >> 1);
-        Frag8 br[NRB];                   // G_R = conj(dL/do), K = token
-        {
-            // tokens past T lie past the chunk's rows
-            const rsrc_t ro = buf(static_cast<const TOUT*>(args.dO) + 2 * (base_tn + static_cast<long>(t0) * n),
-                                  static_cast<long>(min(C, T - t0)) * n * 2 * sizeof(TOUT));
+        Frag8 br[NRB];                   // G_R = conj(dL/do), K = token (loaded at the chunk's start)
 #pragma unroll
-            for (int kb = 0; kb < NRB; ++kb)
+        for (int kb = 0; kb < NRB; ++kb)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int tl = kb * 16 + 4 * g + r;
-                    const float2 x = ld_cplx<TOUT>(ro, j < n ? static_cast<uint32_t>((tl * n + j) * 2 * sizeof(TOUT)) : OOR);
-                    bpair(br[kb], r, x.x, -x.y, qp);
-                }
-        }
+            for (int r = 0; r < 4; ++r) {
+                const float2 x = RawC<TOUT>::get(dor[w][kb][r]);
+                bpair(br[kb], r, x.x, -x.y, qp);
+            }
         Frag8 sb[MP / 16];
 #pragma unroll
         for (int kb = 0; kb < MP / 16; ++kb) sb[kb] = bfrag_from_acc(Sacc[w][kb], qp);
@@ -284,6 +292,24 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
     for (int it_ch = 0; it_ch < nchunks; ++it_ch) {
         const int ch = MODE == 2 ? nchunks - 1 - it_ch : it_ch;
         const int t0 = ch * C;
+        // MODE 2: this wave's dL/do entries of the chunk, requested first so that they arrive
+        // during the load, Gram and inverse stages (tokens past T lie past the chunk's rows)
+        typename RawC<TOUT>::W dor[CBW][NRB][4];
+        if constexpr (MODE == 2) {
+            const rsrc_t ro = buf(static_cast<const TOUT*>(args.dO) + 2 * (base_tn + static_cast<long>(t0) * n),
+                                  static_cast<long>(min(C, T - t0)) * n * 2 * sizeof(TOUT));
+#pragma unroll
+            for (int w = 0; w < CBW; ++w) {
+                const int j = n0 + (wave + NW * w) * 8 + (c >> 1);
+#pragma unroll
+                for (int kb = 0; kb < NRB; ++kb)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int tl = kb * 16 + 4 * g + r;
+                        dor[w][kb][r] = RawC<TOUT>::load(ro, j < n ? static_cast<uint32_t>((tl * n + j) * 2 * sizeof(TOUT)) : OOR);
+                    }
+            }
+        }
         if constexpr (MODE == 1 || MODE == 2) {
             // this wave's share of the chunk's [m][n] record: the state entering it (MODE 1)
             // or the adjoint of the state leaving it (MODE 2)
@@ -422,7 +448,7 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
 
 
         if constexpr (MODE == 2) {
-            adjoint_chunk<P, TIN, TOUT, C, NW>(sm, args, Sacc, bh, t0, nchunks, n0, ncb, tid);
+            adjoint_chunk<P, TIN, TOUT, C, NW>(sm, args, Sacc, bh, t0, nchunks, n0, ncb, tid, dor);
             __syncthreads();
             continue;
         }
@@ -793,7 +819,6 @@ static hipError_t launch_scans_t(const ChunkLaunch& F, const ChunkLaunch& A, hip
     switch (F.C) {
         case 16: hipLaunchKernelGGL((scan_pair_kernel<P, TIN, TOUT, 16>), grid, dim3(scan_waves<16>() * 64), 0, st, af, aa, nfwd); break;
         case 32: hipLaunchKernelGGL((scan_pair_kernel<P, TIN, TOUT, 32>), grid, dim3(scan_waves<32>() * 64), 0, st, af, aa, nfwd); break;
-        case 64: hipLaunchKernelGGL((scan_pair_kernel<P, TIN, TOUT, 64>), grid, dim3(scan_waves<64>() * 64), 0, st, af, aa, nfwd); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
