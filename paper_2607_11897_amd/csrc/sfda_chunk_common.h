@@ -95,11 +95,20 @@ struct ChunkSmemDec : ChunkSmem<C> {
     float wb[C];                             // write strengths beta_t
 };
 
-// raw alpha, theta and beta of one thread's tokens, fetched a chunk ahead by a scan
+// alpha, theta and beta of one thread's tokens, fetched a chunk ahead by a scan, as the
+// loaded words (a bf16 value is converted where it is used, so the fetch is not waited on
+// where it is issued)
 template <int C>
 struct InPre {
-    float a[C / 4], th[C / 4], b;
+    uint32_t a[C / 4], th[C / 4], b;
 };
+template <typename TIN> __device__ __forceinline__ uint32_t raw_word(const void* p, long e) {
+    if constexpr (sizeof(TIN) == 2) return static_cast<const uint16_t*>(p)[e];
+    else return __float_as_uint(static_cast<const float*>(p)[e]);
+}
+template <typename TIN> __device__ __forceinline__ float word_f(uint32_t w) {
+    return __uint_as_float(sizeof(TIN) == 2 ? w << 16 : w);
+}
 
 template <typename TIN, int C, bool WIDE>
 __device__ __forceinline__ void prefetch_inputs(const ChunkArgs& args, long bh, int t0, int tid, InPre<C>& pf)
@@ -113,10 +122,10 @@ __device__ __forceinline__ void prefetch_inputs(const ChunkArgs& args, long bh, 
     for (int u = 0; u < SEG; ++u) {
         const int t = t0 + seg * SEG + u;
         const long e = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
-        pf.a[u] = Elem<TIN>::load(static_cast<const TIN*>(args.alpha), e);
-        pf.th[u] = Elem<TIN>::load(static_cast<const TIN*>(args.theta), e);
+        pf.a[u] = raw_word<TIN>(args.alpha, e);
+        pf.th[u] = raw_word<TIN>(args.theta, e);
     }
-    pf.b = Elem<TIN>::load(static_cast<const TIN*>(args.beta), bh * static_cast<long>(T) + min(t0 + (tid & (C - 1)), T - 1));
+    pf.b = raw_word<TIN>(args.beta, bh * static_cast<long>(T) + min(t0 + (tid & (C - 1)), T - 1));
 }
 
 // ----------------------------------------------------------------- load stage
@@ -175,8 +184,8 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
         float a_ld, th;
         float a;
         if constexpr (PRE) {
-            a_ld = pin(pre->a[u]);
-            th = masked(ok, pre->th[u]);
+            a_ld = pin(word_f<TIN>(pre->a[u]));
+            th = masked(ok, word_f<TIN>(pre->th[u]));
             a = ok ? a_ld : 1.f;
         } else {
             // buffer reads, zero past T and past m: no pin, so they issue back to back
@@ -200,7 +209,7 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
     if (worker) {
         const int tb = t0 + (tid & (C - 1));
         float bv;
-        if constexpr (PRE) bv = pre->b;
+        if constexpr (PRE) bv = word_f<TIN>(pre->b);
         else bv = Elem<TIN>::load(gb, bh * static_cast<long>(T) + min(tb, T - 1));
         if constexpr (GATED) bv = sigmoid_acc(bv);
         if (tid < C) sm.beta[tid] = masked(tb < T, bv);
