@@ -8,7 +8,8 @@ B*T tokens (every token through all H heads) per second.
 
 Also reported on the same JSON line:
   roofline      the chunk kernel against HBM bandwidth (algorithmic bytes / launch time),
-                with achieved MFMA rates (useful causal flops and dense-tile flops) beside it
+                with achieved MFMA rates (useful causal flops, dense-tile flops and the
+                executed matrix-core flops counted by SQ_INSTS_VALU_MFMA_MOPS_BF16) beside it
   decode        the sfda_step kernel on the state [512, 32, 64, 64] complex fp32 (HBM-bound)
   cpu_baseline  the CPU oracle (complex128 recurrence) on a bounded sample of the workload
 
@@ -88,6 +89,19 @@ def load_traffic(kernel: str, workload: str):
     return d.get("bytes_per_launch")
 
 
+def load_mfma_counters(kernel: str, workload: str):
+    """Executed matrix-core flops per launch, from a committed counter summary
+    (SQ_INSTS_VALU_MFMA_MOPS_BF16) for the current kernel source, or None."""
+    path = os.path.join(PROFILES, f"{kernel}_{workload}_mfma.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("kernel_hash") != kernel_hash():
+        return None
+    return d.get("mfma_flops_per_launch")
+
+
 def timed(fn, steps, warmup, stream):
     import torch
     for _ in range(warmup):
@@ -138,6 +152,7 @@ def bench_chunk(args, stream):
     sec = ms / 1e3
     achieved = bytes_alg / sec / 1e9
     traffic = load_traffic("chunk_fwd", w.name)
+    exec_flops = load_mfma_counters("chunk_fwd", w.name)
     return dict(
         w=w, ms=ms, tokens_per_s=B * T / sec, x=x,
         roofline={"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
@@ -151,7 +166,12 @@ def bench_chunk(args, stream):
                            "useful_frac": round(useful * nchunk / sec / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
                            "tile_tflops": round(tile * nchunk / sec / 1e12, 2),
                            "tile_frac": round(tile * nchunk / sec / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
-                           "flops_per_chunk_head": {"useful": useful, "tile": tile}}},
+                           "exec_tflops": None if exec_flops is None else round(exec_flops / sec / 1e12, 2),
+                           "exec_frac": None if exec_flops is None
+                           else round(exec_flops / sec / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
+                           "flops_per_chunk_head": {"useful": useful, "tile": tile,
+                                                    "exec": None if exec_flops is None
+                                                    else exec_flops / nchunk}}},
     )
 
 
