@@ -14,12 +14,14 @@ Also reported on the same JSON line:
   cpu_baseline  the CPU oracle (complex128 recurrence) on a bounded sample of the workload
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--only chunk|decode]
-       [--no-cpu-baseline] [--mode copy|rmw|long]   (copy: a plain device copy, for counter
+       [--no-cpu-baseline] [--mode copy|rmw|long|gated|bwd|dec|f32]   (copy: a plain device copy, for counter
        scaling; rmw: an in-place pass over 1 GiB, the decode step's access pattern; long:
        the long-context workload, one workgroup per head against the segment-parallel scan;
        gated: the benchmarked shape through sfda_chunk_fwd_gated; bwd: sfda_chunk_bwd on the
        benchmarked shape and on the float32 workload B=4, H=8, T=2048; dec: the write-decoupled
-       variant on the benchmarked batch, heads and length with C=32)
+       variant on the benchmarked batch, heads and length with C=32; f32: the float32
+       workload B=4, H=8, T=2048 against the fp32 matrix-core peak, one workgroup per head at
+       C = 16, 32, 64 and segment-parallel)
 """
 from __future__ import annotations
 
@@ -291,6 +293,61 @@ def long_context(args):
     print(json.dumps(out), flush=True)
 
 
+def fp32_forward(args):
+    """The float32 workload (B=4, H=8, T=2048, m=n=64, C=64) through the fp32 chunk kernel,
+    against the fp32 matrix-core peak (its roofline bound: 72 flop per byte against an fp32
+    ridge of 20): one workgroup per head at the workload's C = 64 and at C = 16 and 32 (the
+    same result to rounding), and sfda_chunk_fwd_segmented with G segments per head (32
+    heads leave most of the 256 CUs idle).  Useful flops are the method's (causal halves,
+    solve included) for the whole result, whatever the path; the oracle is timed beside it."""
+    import numpy as np
+    import torch
+    from paper_2607_11897_amd import inputs as I
+    from paper_2607_11897_amd import sfda
+    w = I.WORKLOADS["fwd_f32_b4h8_t2k"]
+    print(f"# generating inputs for {w.name}", file=sys.stderr, flush=True)
+    x = I.make_chunk_inputs(w)
+    st = x.storage()
+    d = {k: torch.from_numpy(np.ascontiguousarray(st[k], dtype=np.float32)).cuda()
+         for k in ("q", "k", "v", "alpha", "theta", "beta")}
+    S0 = torch.from_numpy(np.ascontiguousarray(st["S0"], dtype=np.float32)).cuda()
+    B, H, T, m, n = x.shape
+    o = torch.empty((B, H, T, n, 2), dtype=torch.float32, device="cuda")
+    S_T = torch.empty((B, H, m, n, 2), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    useful, tile = chunk_flops_per_chunk_head(w.C, m, n)
+    nchunk = B * H * (T // w.C)
+    bytes_alg = chunk_bytes_per_token_head(m, n, T, 4, 4) * B * H * T
+    runs = []
+    for C, G in ((64, None), (32, None), (16, None), (64, 4), (64, 8), (16, 8)):
+        ws = None if G is None else torch.empty(sfda.segmented_workspace_bytes(B, H, m, n, G),
+                                                dtype=torch.uint8, device="cuda")
+
+        def run():
+            sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], S0, C=C,
+                           o=o, S_T=S_T, segments=G, workspace=ws, stream=stream)
+
+        print(f"# timing C={C} G={G}", file=sys.stderr, flush=True)
+        ms = timed(run, args.steps, min(args.warmup, 10), stream)
+        sec = ms / 1e3
+        tf = useful * nchunk / sec / 1e12
+        runs.append({"C": C, "segments": G, "ms": round(ms, 4), "tokens_per_s": round(B * T / sec, 1),
+                     "roofline": {"bound": "mfma", "achieved": round(tf, 2), "peak": FP32_MFMA_PEAK_TFLOPS,
+                                  "unit": "TFLOP/s", "frac": round(tf / FP32_MFMA_PEAK_TFLOPS, 4),
+                                  "traffic": None,
+                                  "tile_tflops": round(tile * nchunk / sec / 1e12, 2)},
+                     "hbm_GBps_algorithmic": round(bytes_alg / sec / 1e9, 1)})
+        del ws
+    out = {"mode": "f32", "workload": w.name, "B": B, "H": H, "T": T, "m": m, "n": n, "C": w.C,
+           "dtype": "f32", "flops_per_chunk_head": {"useful": useful, "tile": tile},
+           "bytes_per_token_head": chunk_bytes_per_token_head(m, n, T, 4, 4), "runs": runs,
+           "kernel_hash_fp32_path": bwd_hash()}
+    if not args.no_cpu_baseline:
+        print("# timing the CPU oracle", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(x)
+    print(json.dumps(out), flush=True)
+
+
 def gated(args):
     """The benchmarked shape (bf16, B=8, H=16, T=4096, m=n=64, C=64) on pre-activations:
     sfda_chunk_fwd_gated, alpha, theta, beta and the key normalisation formed inside the
@@ -515,7 +572,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--only", choices=["chunk", "decode"], default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=["bench", "copy", "rmw", "long", "gated", "bwd", "dec"], default="bench")
+    ap.add_argument("--mode", choices=["bench", "copy", "rmw", "long", "gated", "bwd", "dec", "f32"],
+                    default="bench")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported. The (batch, head) "
@@ -546,6 +604,9 @@ def main():
         return
     if args.mode == "dec":
         decoupled(args)
+        return
+    if args.mode == "f32":
+        fp32_forward(args)
         return
     stream = torch.cuda.current_stream()
     out = {}
