@@ -70,6 +70,12 @@ def test_chunk_argument_errors(lib):
     assert chunk(lib, st=P[6] + 16) == 6              # S_T partly overlapping S0
     assert lib.sfda_chunk_fwd_sliced(*P, 1, 1, 4, 8, 8, 16, 12, 0, 0, None) == 2   # slice % 8
     assert lib.sfda_chunk_fwd_sliced(*P, 1, 1, 4, 8, 8, 16, 72, 0, 0, None) == 2
+    # bf16 inputs: each head's share of q, k, v and o below 2 GiB (32-bit buffer ranges);
+    # with m = n = 64 and bf16 o the longest head is (2^31 - 1) // 256 = 8388607 tokens
+    Pf = [1 << 44 + i for i in range(9)]      # addresses far enough apart for 2 GiB buffers
+    big = dict(zip(("q", "k", "v", "a", "th", "b", "s0", "o", "st"), Pf))
+    assert chunk(lib, T=8388608, m=64, n=64, din=1, dout=1, **big) == 2
+    assert chunk(lib, T=4194304, m=64, n=64, din=1, dout=0, **big) == 2    # fp32 o
     # B*H == 0 is a no-op and never touches the pointers
     assert chunk(lib, B=0, q=None, o=None) == 0
 

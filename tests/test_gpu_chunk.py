@@ -312,3 +312,46 @@ def test_bf16_guard_bands_untouched():
         assert torch.all(buf[:pad] == canary) and torch.all(buf[-pad:] == canary)
     o_ref, S_ref = run_oracle(x)
     assert rel_err(to_complex(o), o_ref) <= 2e-2 and rel_err(to_complex(S), S_ref) <= 2e-2
+
+
+def test_bf16_largest_head():
+    """One head of the longest sequence the bf16 path accepts with m = n = 64 and bf16 o
+    (each head's q, k, v and o below 2 GiB: T = (2^31 - 1) // 256 = 8388607 tokens, a ragged
+    last chunk).  Identity tokens (k = q = v = 0, beta = 0, alpha = 1, theta = 0) up to the
+    last 1000 tokens, which follow the benchmark laws: the bulk's outputs are exactly zero,
+    the state reaches the tail unchanged (S0), and the tail's outputs and S_T match the
+    oracle run on the tail from S0.  Exercises the buffer ranges and offsets at the top of
+    the allowed sizes."""
+    import torch
+    from paper_2607_11897_amd import sfda
+    m = n = 64
+    T = (2 ** 31 - 1) // (n * 2 * 2)
+    tail = 1000
+    w = I.Workload("largest", 1, 1, tail, m, n, 64, "bf16", I.LAWS_MAIN, 77, 2e-2)
+    xt = I.make_chunk_inputs(w)
+    st = xt.storage()
+    say("bf16 largest head: T", T, "building inputs")
+    dev = torch.device("cuda")
+
+    def full(name, fill_bits, shape_tail):
+        a = torch.full((T,) + shape_tail, fill_bits, dtype=torch.int16)
+        a[T - tail:] = torch.from_numpy(np.ascontiguousarray(st[name][0, 0]).view(np.int16))
+        return a.to(dev).view(torch.bfloat16).view((1, 1, T) + shape_tail)
+
+    one = int(np.array([1.0], dtype=np.float32).view(np.uint32)[0] >> 16)   # bf16 bits of 1.0
+    q = full("q", 0, (m, 2))
+    k = full("k", 0, (m, 2))
+    v = full("v", 0, (n, 2))
+    alpha = full("alpha", one, (m,))
+    theta = full("theta", 0, (m,))
+    beta = full("beta", 0, ())
+    S0 = torch.from_numpy(np.ascontiguousarray(st["S0"], dtype=np.float32)).to(dev)
+    say("bf16 largest head: running")
+    o, S = sfda.chunk_fwd(q, k, v, alpha, theta, beta, S0, C=64)
+    torch.cuda.synchronize()
+    assert int(torch.count_nonzero(o[0, 0, :T - tail])) == 0     # value test: -0.0 counts as zero
+    o_ref, S_ref = run_oracle(xt)
+    eo = rel_err(to_complex(o[:, :, T - tail:]), o_ref)
+    es = rel_err(to_complex(S), S_ref)
+    say("bf16 largest head: err(o tail)", eo, "err(S_T)", es)
+    assert eo <= 2e-2 and es <= 2e-2
