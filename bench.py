@@ -21,7 +21,7 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--only chunk|decode]
        benchmarked shape and on the float32 workload B=4, H=8, T=2048; dec: the write-decoupled
        variant on the benchmarked batch, heads and length with C=32; f32: the float32
        workload B=4, H=8, T=2048 against the fp32 matrix-core peak, one workgroup per head at
-       C = 16, 32, 64 and segment-parallel)
+       C = 16, 32, 64, value-column slices and segment-parallel)
 """
 from __future__ import annotations
 
@@ -299,7 +299,9 @@ def fp32_forward(args):
     ridge of 20): one workgroup per head at the workload's C = 64 and at C = 16 and 32 (the
     same result to rounding), and sfda_chunk_fwd_segmented with G segments per head (32
     heads leave most of the 256 CUs idle).  Useful flops are the method's (causal halves,
-    solve included) for the whole result, whatever the path; the oracle is timed beside it."""
+    solve included) for the whole result, whatever the path; the oracle is timed beside it.
+    slice: value columns per workgroup (sfda_chunk_fwd_sliced: 64 / slice workgroups per
+    head, each repeating the head's chunk factors)."""
     import numpy as np
     import torch
     from paper_2607_11897_amd import inputs as I
@@ -319,19 +321,21 @@ def fp32_forward(args):
     nchunk = B * H * (T // w.C)
     bytes_alg = chunk_bytes_per_token_head(m, n, T, 4, 4) * B * H * T
     runs = []
-    for C, G in ((64, None), (32, None), (16, None), (64, 4), (64, 8), (16, 8)):
+    for C, G, sl in ((64, None, None), (32, None, None), (16, None, None), (64, None, 16),
+                     (16, None, 16), (64, 4, None), (64, 8, None), (32, 8, None), (16, 8, None)):
         ws = None if G is None else torch.empty(sfda.segmented_workspace_bytes(B, H, m, n, G),
                                                 dtype=torch.uint8, device="cuda")
 
         def run():
             sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], S0, C=C,
-                           o=o, S_T=S_T, segments=G, workspace=ws, stream=stream)
+                           o=o, S_T=S_T, slice=sl, segments=G, workspace=ws, stream=stream)
 
-        print(f"# timing C={C} G={G}", file=sys.stderr, flush=True)
+        print(f"# timing C={C} G={G} slice={sl}", file=sys.stderr, flush=True)
         ms = timed(run, args.steps, min(args.warmup, 10), stream)
         sec = ms / 1e3
         tf = useful * nchunk / sec / 1e12
-        runs.append({"C": C, "segments": G, "ms": round(ms, 4), "tokens_per_s": round(B * T / sec, 1),
+        runs.append({"C": C, "segments": G, "slice": sl, "ms": round(ms, 4),
+                     "tokens_per_s": round(B * T / sec, 1),
                      "roofline": {"bound": "mfma", "achieved": round(tf, 2), "peak": FP32_MFMA_PEAK_TFLOPS,
                                   "unit": "TFLOP/s", "frac": round(tf / FP32_MFMA_PEAK_TFLOPS, 4),
                                   "traffic": None,
