@@ -77,6 +77,34 @@ def _dtype_code(t) -> int:
     raise TypeError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
 
 
+def _check(named: dict) -> None:
+    """Every given tensor has its expected shape and sits on the first tensor's GPU: the
+    library receives bare pointers and sizes, so a short buffer or a host pointer would
+    only show up as a fault inside a kernel.  `named` maps a name to (tensor or None,
+    expected shape)."""
+    dev = None
+    for name, (t, shape) in named.items():
+        if t is None:
+            continue
+        if tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    for name, (t, _) in named.items():
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a GPU tensor (got {t.device})")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise ValueError(f"{name} is on {t.device}, the other tensors on {dev}")
+
+
+def _dims(q, v, nd):
+    if q.dim() != nd or v.dim() != nd:
+        raise ValueError(f"q and v must have {nd} dimensions")
+    return q.shape
+
+
 def _ptr(t) -> Optional[int]:
     if t is None:
         return None
@@ -103,7 +131,7 @@ def chunk_fwd(q, k, v, alpha, theta, beta, S0=None, C: int = 64, *, o=None, S_T=
     least segmented_workspace_bytes(...) bytes, allocated here when not given)."""
     import torch
     lib = load_library()
-    B, H, T, m, _ = q.shape
+    B, H, T, m, _ = _dims(q, v, 5)
     n = v.shape[3]
     in_code = _dtype_code(q)
     for t in (k, v, alpha, theta, beta):
@@ -116,6 +144,10 @@ def chunk_fwd(q, k, v, alpha, theta, beta, S0=None, C: int = 64, *, o=None, S_T=
         S_T = torch.empty((B, H, m, n, 2), dtype=torch.float32, device=q.device)
     if S0 is not None and S0.dtype != torch.float32:
         raise TypeError("S0 must be float32")
+    _check(dict(q=(q, (B, H, T, m, 2)), k=(k, (B, H, T, m, 2)), v=(v, (B, H, T, n, 2)),
+                alpha=(alpha, (B, H, T, m)), theta=(theta, (B, H, T, m)), beta=(beta, (B, H, T)),
+                S0=(S0, (B, H, m, n, 2)), o=(o, (B, H, T, n, 2)), S_T=(S_T, (B, H, m, n, 2)),
+                workspace=(workspace, tuple(workspace.shape) if workspace is not None else ())))
     args = [_ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(theta), _ptr(beta), _ptr(S0),
             _ptr(o), _ptr(S_T), B, H, T, m, n, C]
     if segments is not None:
@@ -123,7 +155,7 @@ def chunk_fwd(q, k, v, alpha, theta, beta, S0=None, C: int = 64, *, o=None, S_T=
         if workspace is None:
             workspace = torch.empty(max(nws, 1), dtype=torch.uint8, device=q.device)
         st = lib.sfda_chunk_fwd_segmented(*args, segments, in_code, _dtype_code(o), _ptr(workspace),
-                                          workspace.numel(), _stream(stream))
+                                          workspace.numel() * workspace.element_size(), _stream(stream))
         if st != 0:
             raise SfdaError(st, "sfda_chunk_fwd_segmented")
         return o, S_T
@@ -144,7 +176,7 @@ def chunk_fwd_gated(q, k_raw, v, a, b, c, S0=None, C: int = 64, *, alpha_min: fl
     keys k_raw [B,H,T,m,2].  Shapes and results otherwise as chunk_fwd."""
     import torch
     lib = load_library()
-    B, H, T, m, _ = q.shape
+    B, H, T, m, _ = _dims(q, v, 5)
     n = v.shape[3]
     in_code = _dtype_code(q)
     for t in (k_raw, v, a, b, c):
@@ -157,6 +189,9 @@ def chunk_fwd_gated(q, k_raw, v, a, b, c, S0=None, C: int = 64, *, alpha_min: fl
         S_T = torch.empty((B, H, m, n, 2), dtype=torch.float32, device=q.device)
     if S0 is not None and S0.dtype != torch.float32:
         raise TypeError("S0 must be float32")
+    _check(dict(q=(q, (B, H, T, m, 2)), k_raw=(k_raw, (B, H, T, m, 2)), v=(v, (B, H, T, n, 2)),
+                a=(a, (B, H, T, m)), b=(b, (B, H, T, m)), c=(c, (B, H, T)),
+                S0=(S0, (B, H, m, n, 2)), o=(o, (B, H, T, n, 2)), S_T=(S_T, (B, H, m, n, 2))))
     st = lib.sfda_chunk_fwd_gated(_ptr(q), _ptr(k_raw), _ptr(v), _ptr(a), _ptr(b), _ptr(c), _ptr(S0),
                                   _ptr(o), _ptr(S_T), B, H, T, m, n, C, float(alpha_min),
                                   float(alpha_max), float(theta_max), float(eps), in_code,
@@ -173,7 +208,7 @@ def chunk_fwd_decoupled(q, k, r, v, alpha, theta, eta, beta, S0=None, C: int = 3
     results otherwise as chunk_fwd."""
     import torch
     lib = load_library()
-    B, H, T, m, _ = q.shape
+    B, H, T, m, _ = _dims(q, v, 5)
     n = v.shape[3]
     in_code = _dtype_code(q)
     for t in (k, r, v, alpha, theta, eta, beta):
@@ -186,6 +221,10 @@ def chunk_fwd_decoupled(q, k, r, v, alpha, theta, eta, beta, S0=None, C: int = 3
         S_T = torch.empty((B, H, m, n, 2), dtype=torch.float32, device=q.device)
     if S0 is not None and S0.dtype != torch.float32:
         raise TypeError("S0 must be float32")
+    _check(dict(q=(q, (B, H, T, m, 2)), k=(k, (B, H, T, m, 2)), r=(r, (B, H, T, m, 2)),
+                v=(v, (B, H, T, n, 2)), alpha=(alpha, (B, H, T, m)), theta=(theta, (B, H, T, m)),
+                eta=(eta, (B, H, T)), beta=(beta, (B, H, T)), S0=(S0, (B, H, m, n, 2)),
+                o=(o, (B, H, T, n, 2)), S_T=(S_T, (B, H, m, n, 2))))
     st = lib.sfda_chunk_fwd_decoupled(_ptr(q), _ptr(k), _ptr(r), _ptr(v), _ptr(alpha), _ptr(theta), _ptr(eta),
                                       _ptr(beta), _ptr(S0), _ptr(o), _ptr(S_T), B, H, T, m, n, C, in_code,
                                       _dtype_code(o), _stream(stream))
@@ -204,7 +243,7 @@ def chunk_bwd(q, k, v, alpha, theta, beta, S0, dO, dS_T=None, C: int = 64, *,
     here when not given."""
     import torch
     lib = load_library()
-    B, H, T, m, _ = q.shape
+    B, H, T, m, _ = _dims(q, v, 5)
     n = v.shape[3]
     in_code = _dtype_code(q)
     for t in (k, v, alpha, theta, beta):
@@ -213,17 +252,21 @@ def chunk_bwd(q, k, v, alpha, theta, beta, S0, dO, dS_T=None, C: int = 64, *,
     for t in (S0, dS_T):
         if t is not None and t.dtype != torch.float32:
             raise TypeError("S0 and dS_T must be float32")
+    _check(dict(q=(q, (B, H, T, m, 2)), k=(k, (B, H, T, m, 2)), v=(v, (B, H, T, n, 2)),
+                alpha=(alpha, (B, H, T, m)), theta=(theta, (B, H, T, m)), beta=(beta, (B, H, T)),
+                S0=(S0, (B, H, m, n, 2)), dO=(dO, (B, H, T, n, 2)), dS_T=(dS_T, (B, H, m, n, 2))))
     g = dict(dq=torch.empty_like(q), dk=torch.empty_like(k), dv=torch.empty_like(v),
              dalpha=torch.empty_like(alpha), dtheta=torch.empty_like(theta), dbeta=torch.empty_like(beta),
              dS0=torch.empty((B, H, m, n, 2), dtype=torch.float32, device=q.device) if want_dS0 else None)
     nws = lib.sfda_chunk_bwd_workspace_bytes(B, H, T, m, n, C)
     if workspace is None:
         workspace = torch.empty(max(nws, 1), dtype=torch.uint8, device=q.device)
+    _check(dict(q=(q, (B, H, T, m, 2)), workspace=(workspace, tuple(workspace.shape))))
     st = lib.sfda_chunk_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(theta), _ptr(beta), _ptr(S0),
                             _ptr(dO), _ptr(dS_T), _ptr(g["dq"]), _ptr(g["dk"]), _ptr(g["dv"]),
                             _ptr(g["dalpha"]), _ptr(g["dtheta"]), _ptr(g["dbeta"]), _ptr(g["dS0"]),
                             B, H, T, m, n, C, in_code, _dtype_code(dO), _ptr(workspace),
-                            workspace.numel(), _stream(stream))
+                            workspace.numel() * workspace.element_size(), _stream(stream))
     if st != 0:
         raise SfdaError(st, "sfda_chunk_bwd")
     return g
@@ -242,7 +285,7 @@ def step(q, k, v, alpha, theta, beta, S, *, o=None, out_dtype=None, stream=None)
     beta: [B,H]; S: [B,H,m,n,2] float32, updated in place.  Returns o [B,H,n,2]."""
     import torch
     lib = load_library()
-    B, H, m, _ = q.shape
+    B, H, m, _ = _dims(q, v, 4)
     n = v.shape[2]
     in_code = _dtype_code(q)
     for t in (k, v, alpha, theta, beta):
@@ -253,6 +296,8 @@ def step(q, k, v, alpha, theta, beta, S, *, o=None, out_dtype=None, stream=None)
     out_dtype = q.dtype if out_dtype is None else out_dtype
     if o is None:
         o = torch.empty((B, H, n, 2), dtype=out_dtype, device=q.device)
+    _check(dict(q=(q, (B, H, m, 2)), k=(k, (B, H, m, 2)), v=(v, (B, H, n, 2)), alpha=(alpha, (B, H, m)),
+                theta=(theta, (B, H, m)), beta=(beta, (B, H)), S=(S, (B, H, m, n, 2)), o=(o, (B, H, n, 2))))
     st = lib.sfda_step(_ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(theta), _ptr(beta),
                        _ptr(S), _ptr(o), B, H, m, n, in_code, _dtype_code(o), _stream(stream))
     if st != 0:

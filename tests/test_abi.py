@@ -205,3 +205,33 @@ def test_decoupled_argument_errors(lib):
     assert dec(o=A * 20) == 6          # o over r
     assert dec(st=A * 21) == 6         # S_T over beta
     assert dec(m=65) == 2
+
+
+def test_binding_checks_shapes_and_devices(lib):
+    """The ctypes binding refuses tensors whose shapes do not match q's sizes and host
+    tensors before any call reaches the library (CPU only)."""
+    import torch
+    from paper_2607_11897_amd import sfda
+    B, H, T, m, n = 1, 2, 8, 8, 4
+    q = torch.zeros(B, H, T, m, 2)
+    k = torch.zeros(B, H, T, m, 2)
+    v = torch.zeros(B, H, T, n, 2)
+    a = torch.ones(B, H, T, m)
+    th = torch.zeros(B, H, T, m)
+    b = torch.zeros(B, H, T)
+    with pytest.raises(ValueError, match="shape"):
+        sfda.chunk_fwd(q, k[:, :, :4], v, a, th, b, C=16)
+    with pytest.raises(ValueError, match="shape"):
+        sfda.chunk_fwd(q, k, v, a, th, b, torch.zeros(B, H, m, n + 1, 2), C=16)
+    with pytest.raises(ValueError, match="shape"):
+        sfda.chunk_fwd(q, k, v, a, th, b, C=16, o=torch.zeros(B, H, T - 1, n, 2))
+    with pytest.raises(ValueError, match="GPU tensor"):
+        sfda.chunk_fwd(q, k, v, a, th, b, C=16)
+    with pytest.raises(ValueError, match="shape"):
+        sfda.step(q[:, :, 0], k[:, :, 0], v[:, :, 0], a[:, :, 0], th[:, :, 0], b[:, :, 0],
+                  torch.zeros(B, H, m, n, 2), o=torch.zeros(B, H, n + 1, 2))
+    with pytest.raises(ValueError, match="GPU tensor"):
+        sfda.step(q[:, :, 0], k[:, :, 0], v[:, :, 0], a[:, :, 0], th[:, :, 0], b[:, :, 0],
+                  torch.zeros(B, H, m, n, 2))
+    with pytest.raises(ValueError, match="shape"):
+        sfda.chunk_bwd(q, k, v, a, th, b, None, torch.zeros(B, H, T, n + 1, 2), C=16)
