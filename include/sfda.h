@@ -75,8 +75,9 @@ typedef void* sfda_stream_t;
  *          S_T == S0 (same pointer) is allowed and updates the state in place; any other
  *          overlap between S_T and another buffer is SFDA_ERR_ALIAS.
  *   B, H >= 0 (B*H == 0 is a no-op); T >= 0 (T == 0 writes S_T = S0, or zeros);
- *   1 <= m <= 64; n >= 1 with m * n < 2^28 (one head's state is addressed with 32-bit byte
- *   offsets; SFDA_ERR_SHAPE otherwise); C in {16, 32, 64} (SFDA_ERR_CHUNK otherwise).  The
+ *   1 <= m <= 64; n >= 1 with m * n < 2^28 and C * n < 2^28 (one head's state and one
+ *   chunk's rows of v and o are addressed with 32-bit byte offsets; SFDA_ERR_SHAPE
+ *   otherwise); C in {16, 32, 64} (SFDA_ERR_CHUNK otherwise).  The
  *   last chunk may be ragged (T mod C != 0).
  *   Numerical range: the chunk factorisation divides by the in-chunk cumulative decay, so
  *   prod over any C consecutive tokens of alpha_t[i] must stay above about 1e-30 for every

@@ -48,6 +48,9 @@ int sfda_abi_version(void) { return SFDA_ABI_VERSION; }
 
 // one head's state (m x n complex float32) is addressed with 32-bit byte offsets
 static bool state_fits(int m, int n) { return static_cast<long>(m) * n * 8 < 0x80000000L; }
+// the float32 path addresses one chunk's rows of v, o and dL/do (C x n complex, at most 8
+// bytes per element) with 32-bit byte offsets
+static bool chunk_rows_fit(int C, int n) { return static_cast<long>(C) * n * 8 < 0x80000000L; }
 
 static sfda_status_t chunk_fwd_impl(const void* q, const void* k, const void* v,
                                     const void* alpha, const void* theta, const void* beta,
@@ -60,6 +63,7 @@ static sfda_status_t chunk_fwd_impl(const void* q, const void* k, const void* v,
     if (!dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return SFDA_ERR_DTYPE;
     if (B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1 || !state_fits(m, n)) return SFDA_ERR_SHAPE;
     if (C != 16 && C != 32 && C != 64) return SFDA_ERR_CHUNK;
+    if (!chunk_rows_fit(C, n)) return SFDA_ERR_SHAPE;
     if (slice < 8 || slice > 64 || (slice & 7) != 0) return SFDA_ERR_SHAPE;
     const long BH = static_cast<long>(B) * H;
     if (BH * ((n + slice - 1) / slice) > 0x7FFFFFFFL) return SFDA_ERR_SHAPE;
@@ -282,6 +286,7 @@ sfda_status_t sfda_chunk_bwd(const void* q, const void* k, const void* v, const 
     if (!dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return SFDA_ERR_DTYPE;
     if (B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1 || !state_fits(m, n)) return SFDA_ERR_SHAPE;
     if (C != 16 && C != 32 && C != 64) return SFDA_ERR_CHUNK;
+    if (!chunk_rows_fit(C, n)) return SFDA_ERR_SHAPE;
     const size_t need = sfda_chunk_bwd_workspace_bytes(B, H, T, m, n, C);
     C = bwd_chunk(C);
     const long BH = static_cast<long>(B) * H;

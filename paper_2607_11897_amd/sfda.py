@@ -99,6 +99,16 @@ def _check(named: dict) -> None:
             raise ValueError(f"{name} is on {t.device}, the other tensors on {dev}")
 
 
+def _need_f32(**named) -> None:
+    """States (S0, S_T, dS_T, S) are complex float32 whatever the inputs' dtype: the library
+    reads and writes m * n * 8 bytes per head there, so a half-width buffer would be
+    overrun."""
+    import torch
+    for name, t in named.items():
+        if t is not None and t.dtype != torch.float32:
+            raise TypeError(f"{name} must be float32 (got {t.dtype})")
+
+
 def _dims(q, v, nd):
     if q.dim() != nd or v.dim() != nd:
         raise ValueError(f"q and v must have {nd} dimensions")
@@ -142,8 +152,8 @@ def chunk_fwd(q, k, v, alpha, theta, beta, S0=None, C: int = 64, *, o=None, S_T=
         o = torch.empty((B, H, T, n, 2), dtype=out_dtype, device=q.device)
     if S_T is None and want_state:
         S_T = torch.empty((B, H, m, n, 2), dtype=torch.float32, device=q.device)
-    if S0 is not None and S0.dtype != torch.float32:
-        raise TypeError("S0 must be float32")
+    _need_f32(S0=S0, S_T=S_T)
+    _dtype_code(o)
     _check(dict(q=(q, (B, H, T, m, 2)), k=(k, (B, H, T, m, 2)), v=(v, (B, H, T, n, 2)),
                 alpha=(alpha, (B, H, T, m)), theta=(theta, (B, H, T, m)), beta=(beta, (B, H, T)),
                 S0=(S0, (B, H, m, n, 2)), o=(o, (B, H, T, n, 2)), S_T=(S_T, (B, H, m, n, 2)),
@@ -187,8 +197,8 @@ def chunk_fwd_gated(q, k_raw, v, a, b, c, S0=None, C: int = 64, *, alpha_min: fl
         o = torch.empty((B, H, T, n, 2), dtype=out_dtype, device=q.device)
     if S_T is None and want_state:
         S_T = torch.empty((B, H, m, n, 2), dtype=torch.float32, device=q.device)
-    if S0 is not None and S0.dtype != torch.float32:
-        raise TypeError("S0 must be float32")
+    _need_f32(S0=S0, S_T=S_T)
+    _dtype_code(o)
     _check(dict(q=(q, (B, H, T, m, 2)), k_raw=(k_raw, (B, H, T, m, 2)), v=(v, (B, H, T, n, 2)),
                 a=(a, (B, H, T, m)), b=(b, (B, H, T, m)), c=(c, (B, H, T)),
                 S0=(S0, (B, H, m, n, 2)), o=(o, (B, H, T, n, 2)), S_T=(S_T, (B, H, m, n, 2))))
@@ -219,8 +229,8 @@ def chunk_fwd_decoupled(q, k, r, v, alpha, theta, eta, beta, S0=None, C: int = 3
         o = torch.empty((B, H, T, n, 2), dtype=out_dtype, device=q.device)
     if S_T is None and want_state:
         S_T = torch.empty((B, H, m, n, 2), dtype=torch.float32, device=q.device)
-    if S0 is not None and S0.dtype != torch.float32:
-        raise TypeError("S0 must be float32")
+    _need_f32(S0=S0, S_T=S_T)
+    _dtype_code(o)
     _check(dict(q=(q, (B, H, T, m, 2)), k=(k, (B, H, T, m, 2)), r=(r, (B, H, T, m, 2)),
                 v=(v, (B, H, T, n, 2)), alpha=(alpha, (B, H, T, m)), theta=(theta, (B, H, T, m)),
                 eta=(eta, (B, H, T)), beta=(beta, (B, H, T)), S0=(S0, (B, H, m, n, 2)),
@@ -249,9 +259,8 @@ def chunk_bwd(q, k, v, alpha, theta, beta, S0, dO, dS_T=None, C: int = 64, *,
     for t in (k, v, alpha, theta, beta):
         if t.dtype != q.dtype:
             raise TypeError("q, k, v, alpha, theta, beta must share one dtype")
-    for t in (S0, dS_T):
-        if t is not None and t.dtype != torch.float32:
-            raise TypeError("S0 and dS_T must be float32")
+    _need_f32(S0=S0, dS_T=dS_T)
+    _dtype_code(dO)
     _check(dict(q=(q, (B, H, T, m, 2)), k=(k, (B, H, T, m, 2)), v=(v, (B, H, T, n, 2)),
                 alpha=(alpha, (B, H, T, m)), theta=(theta, (B, H, T, m)), beta=(beta, (B, H, T)),
                 S0=(S0, (B, H, m, n, 2)), dO=(dO, (B, H, T, n, 2)), dS_T=(dS_T, (B, H, m, n, 2))))
@@ -291,11 +300,11 @@ def step(q, k, v, alpha, theta, beta, S, *, o=None, out_dtype=None, stream=None)
     for t in (k, v, alpha, theta, beta):
         if t.dtype != q.dtype:
             raise TypeError("q, k, v, alpha, theta, beta must share one dtype")
-    if S.dtype != torch.float32:
-        raise TypeError("S must be float32")
+    _need_f32(S=S)
     out_dtype = q.dtype if out_dtype is None else out_dtype
     if o is None:
         o = torch.empty((B, H, n, 2), dtype=out_dtype, device=q.device)
+    _dtype_code(o)
     _check(dict(q=(q, (B, H, m, 2)), k=(k, (B, H, m, 2)), v=(v, (B, H, n, 2)), alpha=(alpha, (B, H, m)),
                 theta=(theta, (B, H, m)), beta=(beta, (B, H)), S=(S, (B, H, m, n, 2)), o=(o, (B, H, n, 2))))
     st = lib.sfda_step(_ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(theta), _ptr(beta),

@@ -76,6 +76,9 @@ def test_chunk_argument_errors(lib):
     big = dict(zip(("q", "k", "v", "a", "th", "b", "s0", "o", "st"), Pf))
     assert chunk(lib, T=8388608, m=64, n=64, din=1, dout=1, **big) == 2
     assert chunk(lib, T=4194304, m=64, n=64, din=1, dout=0, **big) == 2    # fp32 o
+    # the float32 path addresses one chunk's rows of v and o with 32-bit byte offsets:
+    # C * n * 8 < 2^31 (n = 2^22 is refused at C = 64, though m * n * 8 < 2^31 with m = 1)
+    assert chunk(lib, T=64, m=1, n=1 << 22, C=64, **big) == 2
     # B*H == 0 is a no-op and never touches the pointers
     assert chunk(lib, B=0, q=None, o=None) == 0
 
@@ -169,6 +172,7 @@ def test_bwd_argument_errors(lib):
     assert bwd(lib, din=5) == 4
     assert bwd(lib, m=65) == 2
     assert bwd(lib, T=-1) == 2
+    assert bwd(lib, m=1, n=1 << 22, C=64) == 2                 # C * n * 8 >= 2^31 (32-bit row offsets)
     for idx in list(range(6)) + [7] + list(range(9, 15)):     # required: inputs, dO, gradients
         p = list(PB)
         p[idx] = 0
@@ -235,3 +239,37 @@ def test_binding_checks_shapes_and_devices(lib):
                   torch.zeros(B, H, m, n, 2))
     with pytest.raises(ValueError, match="shape"):
         sfda.chunk_bwd(q, k, v, a, th, b, None, torch.zeros(B, H, T, n + 1, 2), C=16)
+
+
+def test_binding_checks_state_and_output_dtypes(lib):
+    """A caller-supplied S_T (or S, dS_T) of half width would be overrun by the library's
+    m * n * 8 bytes per head; the binding refuses it, and an o of an unsupported dtype,
+    before any call (CPU only)."""
+    import torch
+    from paper_2607_11897_amd import sfda
+    B, H, T, m, n = 1, 2, 8, 8, 4
+    q = torch.zeros(B, H, T, m, 2)
+    k = torch.zeros(B, H, T, m, 2)
+    v = torch.zeros(B, H, T, n, 2)
+    a = torch.ones(B, H, T, m)
+    th = torch.zeros(B, H, T, m)
+    b = torch.zeros(B, H, T)
+    half_state = torch.zeros(B, H, m, n, 2, dtype=torch.bfloat16)
+    with pytest.raises(TypeError, match="S_T must be float32"):
+        sfda.chunk_fwd(q, k, v, a, th, b, C=16, S_T=half_state)
+    with pytest.raises(TypeError, match="S0 must be float32"):
+        sfda.chunk_fwd(q, k, v, a, th, b, half_state, C=16)
+    with pytest.raises(TypeError, match="S_T must be float32"):
+        sfda.chunk_fwd_gated(q, k, v, a, th, b, C=16, alpha_min=0.5, alpha_max=1.0, theta_max=1.0,
+                             eps=0.0, S_T=half_state)
+    with pytest.raises(TypeError, match="S_T must be float32"):
+        sfda.chunk_fwd_decoupled(q, k, k, v, a, th, b, b, C=16, S_T=half_state)
+    with pytest.raises(TypeError, match="unsupported dtype"):
+        sfda.chunk_fwd(q, k, v, a, th, b, C=16, o=torch.zeros(B, H, T, n, 2, dtype=torch.float16))
+    with pytest.raises(TypeError, match="dS_T must be float32"):
+        sfda.chunk_bwd(q, k, v, a, th, b, None, torch.zeros(B, H, T, n, 2), half_state, C=16)
+    with pytest.raises(TypeError, match="S must be float32"):
+        sfda.step(q[:, :, 0], k[:, :, 0], v[:, :, 0], a[:, :, 0], th[:, :, 0], b[:, :, 0], half_state)
+    with pytest.raises(TypeError, match="unsupported dtype"):
+        sfda.step(q[:, :, 0], k[:, :, 0], v[:, :, 0], a[:, :, 0], th[:, :, 0], b[:, :, 0],
+                  torch.zeros(B, H, m, n, 2), o=torch.zeros(B, H, n, 2, dtype=torch.float16))
