@@ -11,7 +11,12 @@ Also reported on the same JSON line:
                 with achieved MFMA rates (useful causal flops, dense-tile flops and the
                 executed matrix-core flops counted by SQ_INSTS_VALU_MFMA_MOPS_BF16) beside it
   decode        the sfda_step kernel on the state [512, 32, 64, 64] complex fp32 (HBM-bound)
-  cpu_baseline  the CPU oracle (complex128 recurrence) on a bounded sample of the workload
+  launch_ms     mean (= ms_per_step), median, minimum and maximum of the K per-launch
+                intervals between HIP events recorded on the launch stream
+  cpu_baseline  the CPU oracle (complex128 recurrence) on a bounded sample of the workload,
+                on every host thread and on one thread, with the CPU model
+The decode step is timed first; its untimed settle phase (about 0.3 s of decode steps)
+brings the GPU to steady clocks before the chunk kernel's warm-up and timed launches.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--only chunk|decode]
        [--no-cpu-baseline] [--mode copy|rmw|long|gated|bwd|dec|f32]   (copy: a plain device copy, for counter
@@ -44,6 +49,7 @@ PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ["paper_2607_11897_amd/csrc/sfda_chunk_bf16.hip", "paper_2607_11897_amd/csrc/sfda_step.hip",
                   "paper_2607_11897_amd/csrc/sfda_device.h"]
 FP32_MFMA_PEAK_TFLOPS = 157.3
+SETTLE_S = 0.3
 
 
 def kernel_hash() -> str:
@@ -104,19 +110,41 @@ def load_mfma_counters(kernel: str, workload: str):
     return d.get("mfma_flops_per_launch")
 
 
-def timed(fn, steps, warmup, stream):
+def timed_stats(fn, steps, warmup, stream):
+    """W untimed launches, then exactly K launches with a HIP event recorded on the launch
+    stream before the first and after every launch.  Returns the mean over the whole
+    bracketed region (total / K, the ms_per_step of the bench line) and the median,
+    minimum and maximum of the per-launch event intervals, in ms."""
     import torch
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for _ in range(steps):
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    evs[0].record(stream)
+    for i in range(steps):
         fn()
-    end.record(stream)
+        evs[i + 1].record(stream)
     torch.cuda.synchronize()
-    return start.elapsed_time(end) / steps   # ms per call
+    per = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(steps))
+    mid = steps // 2
+    median = per[mid] if steps % 2 else 0.5 * (per[mid - 1] + per[mid])
+    return {"mean": evs[0].elapsed_time(evs[-1]) / steps, "median": median, "min": per[0],
+            "max": per[-1]}
+
+
+def timed(fn, steps, warmup, stream):
+    return timed_stats(fn, steps, warmup, stream)["mean"]   # ms per call
+
+
+def settle_clocks(fn, seconds, stream):
+    """Untimed launches of fn for about `seconds` of wall time (the GPU's clocks ramp up
+    over the first tens of milliseconds of work after it has been idle)."""
+    import torch
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(20):
+            fn()
+        torch.cuda.synchronize()
 
 
 def bench_chunk(args, stream):
@@ -146,7 +174,8 @@ def bench_chunk(args, stream):
                        o=o, S_T=S_T, stream=stream)
 
     print(f"# timing sfda_chunk_fwd: warmup {args.warmup}, steps {args.steps}", file=sys.stderr, flush=True)
-    ms = timed(run, args.steps, args.warmup, stream)
+    stats = timed_stats(run, args.steps, args.warmup, stream)
+    ms = stats["mean"]
     units = B * H * T
     bytes_alg = chunk_bytes_per_token_head(m, n, T, 2, 2) * units
     useful, tile = chunk_flops_per_chunk_head(w.C, m, n)
@@ -157,6 +186,7 @@ def bench_chunk(args, stream):
     exec_flops = load_mfma_counters("chunk_fwd", w.name)
     return dict(
         w=w, ms=ms, tokens_per_s=B * T / sec, x=x,
+        launch_ms={k: round(v, 4) for k, v in stats.items()},
         roofline={"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                   "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                   "traffic": traffic,
@@ -193,11 +223,14 @@ def bench_decode(args, stream):
         sfda.step(q, k, v, a, th, bt, S, o=o, stream=stream)
 
     steps = max(20, args.steps)
-    print(f"# timing sfda_step: steps {steps}", file=sys.stderr, flush=True)
-    ms = timed(run, steps, max(3, args.warmup), stream)
+    print(f"# timing sfda_step: {SETTLE_S} s of untimed steps, then {steps} steps", file=sys.stderr, flush=True)
+    settle_clocks(run, SETTLE_S, stream)
+    stats = timed_stats(run, steps, max(3, args.warmup), stream)
+    ms = stats["mean"]
     bytes_step = decode_bytes_per_head(m, n) * B * H
     gbs = bytes_step / (ms / 1e3) / 1e9
     return {"workload": D["name"], "us_per_step": round(ms * 1e3, 2),
+            "launch_us": {k: round(v * 1e3, 2) for k, v in stats.items()},
             "tokens_per_s": round(B / (ms / 1e3), 1),
             "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS,
                          "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
@@ -206,27 +239,48 @@ def bench_decode(args, stream):
                          "bytes_per_launch": int(bytes_step)}}
 
 
-def cpu_baseline(x, budget_s=12.0):
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(x, budget_s=12.0, single_budget_s=6.0):
     """The oracle on whole batch elements of the workload (all H heads, all T tokens), one
     after another -- passing over the batch again if it finishes early -- until about
-    budget_s seconds of CPU time have been spent."""
+    budget_s seconds have been spent, on every host thread; then the same on one thread
+    for about single_budget_s seconds."""
     import oracle
     B, H, T, m, n = x.shape
+
+    def run(nthreads, budget):
+        done = 0
+        t0 = time.perf_counter()
+        while True:
+            b = done % B
+            oracle.recurrence(x.q[b:b + 1], x.k[b:b + 1], x.v[b:b + 1], x.alpha[b:b + 1],
+                              x.theta[b:b + 1], x.beta[b:b + 1],
+                              None if x.S0 is None else x.S0[b:b + 1], nthreads=nthreads)
+            done += 1
+            if time.perf_counter() - t0 >= budget:
+                break
+        return done, time.perf_counter() - t0
+
     threads = oracle.max_threads()
-    done = 0
-    t0 = time.perf_counter()
-    while True:
-        b = done % B
-        oracle.recurrence(x.q[b:b + 1], x.k[b:b + 1], x.v[b:b + 1], x.alpha[b:b + 1],
-                          x.theta[b:b + 1], x.beta[b:b + 1],
-                          None if x.S0 is None else x.S0[b:b + 1])
-        done += 1
-        if time.perf_counter() - t0 >= budget_s:
-            break
-    el = time.perf_counter() - t0
+    done, el = run(0, budget_s)
+    done1, el1 = run(1, single_budget_s)
     return {"value": round(done * T / el, 1), "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"{done} batch elements of {B} (taken in turn) x {H} heads x {T} tokens "
-                      f"(complex128 recurrence), {el:.1f} s"}
+                      f"(complex128 recurrence), {el:.1f} s",
+            "cpu_model": cpu_model(),
+            "single_thread": {"value": round(done1 * T / el1, 1), "unit": "tokens/s", "cores": 1,
+                              "sample": f"{done1} batch elements x {H} heads x {T} tokens, {el1:.1f} s"}}
 
 
 def cpu_baseline_backward(x, dO, dS, budget_s=10.0):
@@ -618,9 +672,11 @@ def main():
         out["decode"] = bench_decode(args, stream)
         print(json.dumps(out), flush=True)
         return
-    r = bench_chunk(args, stream)
+    # the decode step runs first: its untimed settle phase brings the GPU to steady clocks
+    # before the chunk kernel's W warm-up and K timed launches
     if args.only is None:
         out["decode"] = bench_decode(args, stream)
+    r = bench_chunk(args, stream)
     w = r["w"]
     line = {
         "metric": METRIC, "value": round(r["tokens_per_s"], 1), "unit": "tokens/s", "n_gpus": 1,
@@ -629,6 +685,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "T": w.T, "d_k": 2 * w.m, "d_v": 2 * w.n,
                    "m_complex": w.m, "n_complex": w.n, "C": w.C, "state": "fp32", "accum": "fp32"},
+        "launch_ms": r["launch_ms"],
         "roofline": r["roofline"],
     }
     if "decode" in out:
