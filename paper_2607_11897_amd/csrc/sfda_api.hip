@@ -35,7 +35,7 @@ const char* sfda_status_string(sfda_status_t s)
         case SFDA_OK: return "ok";
         case SFDA_ERR_NULL: return "a required pointer is NULL";
         case SFDA_ERR_SHAPE: return "a size is out of range";
-        case SFDA_ERR_CHUNK: return "unsupported chunk length (C must be 16, 32 or 64)";
+        case SFDA_ERR_CHUNK: return "unsupported chunk length (C must be 16, 32, 64 or 128)";
         case SFDA_ERR_DTYPE: return "unsupported dtype";
         case SFDA_ERR_ALIGN: return "a pointer is not 16-byte aligned";
         case SFDA_ERR_ALIAS: return "an output buffer overlaps another buffer";
@@ -49,8 +49,11 @@ int sfda_abi_version(void) { return SFDA_ABI_VERSION; }
 // one head's state (m x n complex float32) is addressed with 32-bit byte offsets
 static bool state_fits(int m, int n) { return static_cast<long>(m) * n * 8 < 0x80000000L; }
 // the float32 path addresses one chunk's rows of v, o and dL/do (C x n complex, at most 8
-// bytes per element) with 32-bit byte offsets
-static bool chunk_rows_fit(int C, int n) { return static_cast<long>(C) * n * 8 < 0x80000000L; }
+// bytes per element, C <= 32 in those kernels) with 32-bit byte offsets
+static bool chunk_rows_fit(int n) { return static_cast<long>(32) * n * 8 < 0x80000000L; }
+// chunk lengths the entry points accept (the kernels' blocking does not change the result,
+// Thm 6.1)
+static bool chunk_ok(int C) { return C == 16 || C == 32 || C == 64 || C == 128; }
 
 static sfda_status_t chunk_fwd_impl(const void* q, const void* k, const void* v,
                                     const void* alpha, const void* theta, const void* beta,
@@ -62,8 +65,8 @@ static sfda_status_t chunk_fwd_impl(const void* q, const void* k, const void* v,
 {
     if (!dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return SFDA_ERR_DTYPE;
     if (B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1 || !state_fits(m, n)) return SFDA_ERR_SHAPE;
-    if (C != 16 && C != 32 && C != 64) return SFDA_ERR_CHUNK;
-    if (!chunk_rows_fit(C, n)) return SFDA_ERR_SHAPE;
+    if (!chunk_ok(C)) return SFDA_ERR_CHUNK;
+    if (!chunk_rows_fit(n)) return SFDA_ERR_SHAPE;
     if (slice < 8 || slice > 64 || (slice & 7) != 0) return SFDA_ERR_SHAPE;
     const long BH = static_cast<long>(B) * H;
     if (BH * ((n + slice - 1) / slice) > 0x7FFFFFFFL) return SFDA_ERR_SHAPE;
@@ -144,9 +147,12 @@ sfda_status_t sfda_chunk_fwd_gated(const void* q, const void* k_raw, const void*
                                    float theta_max, float eps, sfda_dtype_t in_dtype,
                                    sfda_dtype_t out_dtype, sfda_stream_t stream)
 {
-    // 0 < alpha_min <= alpha_max <= 1 (a zero decay has no inverse in the chunk factors),
-    // theta_max and eps finite and >= 0 (NaN fails every comparison)
-    if (!(alpha_min > 0.f && alpha_min <= alpha_max && alpha_max <= 1.f)) return SFDA_ERR_SHAPE;
+    // ALPHA_MIN_GATED <= alpha_min <= alpha_max <= 1: the kernels' 16-token blocks divide by
+    // the decay over one block, which stays inside the float range (>= 2^-126) whenever every
+    // alpha is at least 2^(-126/16); theta_max and eps finite and >= 0 (NaN fails every
+    // comparison)
+    constexpr float ALPHA_MIN_GATED = 0.0042719f;     // 2^(-7.875), rounded up
+    if (!(alpha_min >= ALPHA_MIN_GATED && alpha_min <= alpha_max && alpha_max <= 1.f)) return SFDA_ERR_SHAPE;
     if (!(theta_max >= 0.f && theta_max < 3.4e38f && eps >= 0.f && eps < 3.4e38f)) return SFDA_ERR_SHAPE;
     const int slice = n <= 64 ? ((n + 7) / 8) * 8 : 64;
     sfda::GateParams gp{true, alpha_min, alpha_max, theta_max, eps};
@@ -167,7 +173,6 @@ sfda_status_t sfda_chunk_fwd_decoupled(const void* q, const void* k, const void*
                                              C, in_dtype, out_dtype, stream, slice, nullptr, 0,
                                              /*check_only=*/true);
     if (st0 != SFDA_OK) return st0;
-    if (C == 64) return SFDA_ERR_CHUNK;        // C = 16 or 32 (the kernel's LDS budget)
     const long BH = static_cast<long>(B) * H;
     if (BH == 0) return SFDA_OK;
     if (T > 0 && (!r || !beta)) return SFDA_ERR_NULL;
@@ -207,7 +212,7 @@ sfda_status_t sfda_chunk_fwd_segmented(const void* q, const void* k, const void*
     const int slice_n = n <= 64 ? ((n + 7) / 8) * 8 : 64;
     // the shared checks (and the whole call when there is nothing to split)
     if (T == 0 || static_cast<long>(B) * H == 0 || !dtype_ok(in_dtype) || !dtype_ok(out_dtype) ||
-        B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1 || !state_fits(m, n) || (C != 16 && C != 32 && C != 64))
+        B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1 || !state_fits(m, n) || !chunk_ok(C))
         return chunk_fwd_impl(q, k, v, alpha, theta, beta, S0, o, S_T, B, H, T, m, n, C, in_dtype,
                               out_dtype, stream, slice_n);
     if (T % (static_cast<long>(G) * C) != 0) return SFDA_ERR_SHAPE;
@@ -260,15 +265,15 @@ sfda_status_t sfda_chunk_fwd_segmented(const void* q, const void* k, const void*
     return SFDA_OK;
 }
 
-// the backward's chunk length: C = 64 runs at 32 (the gradient pass stages a block of
-// value columns beside the chunk's operands in LDS; every C gives the same gradients up to
-// rounding)
+// the backward's chunk length: C = 64 and 128 run at 32 (the gradient pass stages a block
+// of value columns beside the chunk's operands in LDS; every C gives the same gradients up
+// to rounding)
 static int bwd_chunk(int C) { return C > 32 ? 32 : C; }
 
 size_t sfda_chunk_bwd_workspace_bytes(int B, int H, int T, int m, int n, int C)
 {
     if (B <= 0 || H <= 0 || T < 0 || m < 1 || m > 64 || n < 1) return 0;
-    if (C != 16 && C != 32 && C != 64) return 0;
+    if (!chunk_ok(C)) return 0;
     C = bwd_chunk(C);
     const size_t chunks = static_cast<size_t>(B) * H * ((static_cast<size_t>(T) + C - 1) / C);
     // per chunk: S entering and dL/dS leaving (m x n each), Delta and G_F (C x n each)
@@ -285,8 +290,8 @@ sfda_status_t sfda_chunk_bwd(const void* q, const void* k, const void* v, const 
 {
     if (!dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return SFDA_ERR_DTYPE;
     if (B < 0 || H < 0 || T < 0 || m < 1 || m > 64 || n < 1 || !state_fits(m, n)) return SFDA_ERR_SHAPE;
-    if (C != 16 && C != 32 && C != 64) return SFDA_ERR_CHUNK;
-    if (!chunk_rows_fit(C, n)) return SFDA_ERR_SHAPE;
+    if (!chunk_ok(C)) return SFDA_ERR_CHUNK;
+    if (!chunk_rows_fit(n)) return SFDA_ERR_SHAPE;
     const size_t need = sfda_chunk_bwd_workspace_bytes(B, H, T, m, n, C);
     C = bwd_chunk(C);
     const long BH = static_cast<long>(B) * H;

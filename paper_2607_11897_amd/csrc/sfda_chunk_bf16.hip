@@ -1,52 +1,65 @@
 // Chunkwise SFDA forward for bfloat16 inputs on gfx950: a producer/consumer pipeline inside
 // one workgroup per (batch, head, slice of value columns).
 //
-// Method.  Inside a chunk of C tokens, with g_t = lambda_1 ... lambda_t (the diagonal of
-// Gamma_t) and S the state entering the chunk, the recurrence reads
-// S_t = Lambda_t S_{t-1} + k_t delta_t with delta_t = beta_t (v_t^* - k_t^* Lambda_t S_{t-1}).
-// Unrolling it gives the chunk-WY factors of Thm 4.2 / Cor. 4.3 in closed form and
-//   (I + D_beta L') Delta = D_beta (conj(V) - (conj(K) * G) S)             (i)
-//   L'[t, j] = k_t^* diag(g_t / g_j) k_j  (j < t)
-//   O^*   = (conj(Q) * G) S + tril(A) Delta,  A[r, j] = q_r^* diag(g_r / g_j) k_j  (j <= r)
-//   S_out = diag(g_C) (S + (K / G)^T Delta)
-// i.e. the exact affine chunk transfer of Thm 4.4 (the paper's M is (I + L' D_beta)^{-1})
-// with the prefix outputs of Thm 4.5, applied by the boundary-state scan (apply-transfer
-// equation, Thm 6.1).  Equation (i) is solved per chunk by blocked forward substitution:
-// with 16 x 16 blocks, Delta_p = N_pp (R_p - sum_{q<p} (D_beta L')_pq Delta_q) where
-// N_pp = (I + (D_beta L')_pp)^{-1}.  The state-independent work is therefore the cumulative
-// phase-decay g, the operands conj(Q)G, conj(K)G, K/G, the Gram blocks of L' and A, and the
-// four 16 x 16 inverses N_pp; the state-dependent work is five small complex GEMMs.
+// Method.  The recurrence S_t = Lambda_t S_{t-1} + k_t delta_t with
+// delta_t = beta_t (v_t^* - k_t^* Lambda_t S_{t-1}) is evaluated on blocks of 16 tokens.  For
+// one block with entering state S, and g_t the product of lambda over the block's tokens up
+// to t (the diagonal of the block's Gamma_t), unrolling it gives the chunk-WY factors of
+// Thm 4.2 / Cor. 4.3 in closed form:
+//   (I + D_beta L) Delta = D_beta (conj(V) - (conj(K) * G) S)          L[t, j] = k_t^* diag(g_t / g_j) k_j, j < t
+//   O^*   = (conj(Q) * G) S + tril(A) Delta                             A[r, j] = q_r^* diag(g_r / g_j) k_j, j <= r
+//   S_out = diag(g_16) S + (K * (g_16 / G))^T Delta
+// -- the exact affine block transfer of Thm 4.4 (the paper's M is (I + L D_beta)^{-1}) with the
+// prefix outputs of Thm 4.5.  The blocks are chained by the boundary-state scan (apply-transfer
+// equation, Thm 6.1); a pipeline step takes four blocks (64 tokens).
 //
-// Pipeline (512 threads = 8 waves, two per SIMD):
-//   waves 0-3 (consumers) own 16 value columns each and hold their columns of S in MFMA
-//     accumulators for the whole scan; for chunk c they compute Delta and the A Gram
-//     blocks (phase 1), then O and S_out and the off-diagonal L' blocks of chunk c + 1
-//     (phase 2);
-//   waves 4-7 (producers) prepare chunk c + 1: phase 1 turns q, k, alpha, theta, beta
-//     (prefetched a chunk ahead) into g -- running products of alpha and running sums of
-//     theta -- and writes conj(Q)G, conj(K)G, K/G (bf16) to LDS; phase 2 forms the
-//     diagonal blocks of L' on MFMA, inverts the diagonal blocks of I + D_beta L' (one per
-//     wave) and starts the scan of the chunk after.
-//   Operands live in two LDS sets (chunk c and chunk c + 1); two barriers per chunk.
+// Decay range.  Every decay factor is a product of alphas over tokens inside one block,
+// taken forwards from the block's start (P_t, in conj(Q) * G and conj(K) * G) or backwards
+// from its end (Q_t, in K * (g_16 / G)), so these operands never exceed |q| or |k| and an
+// underflow only ever drops a contribution that is itself below the float range.  Only the
+// right operand of the block's own Gram matrices divides, k_j / P_j, and stays finite while
+// the product of alpha over the block is at least 2^-126 (every alpha >= 0.0043 suffices);
+// a step holding a block outside that range returns NaN from there on (its state is set to
+// NaN).  Phases are kept as running sums of theta / 2 pi reduced to [0, 1) revolutions
+// from the start of the sequence (a global frame: the state is held rotated by
+// exp(-i phi) of the phase reached so far, and rotated back once at the end), so only
+// magnitudes need block-local references (the paper's remark on log-decays and local
+// renormalisation inside chunks, App. C.4).
+//
+// Pipeline (512 threads = 8 waves, two per SIMD; one barrier per step):
+//   waves 0-3 (consumers) own 16 value columns each and hold their columns of the rotated
+//     state in MFMA accumulators for the whole scan; they walk the four blocks of step s:
+//       P = conj(K)G S,  O = conj(Q)G S,  Delta = N D_beta (conj(V) - P),  O += A Delta,
+//       S <- |D| S + (K Q)^T Delta      (|D| the block's decay magnitude per channel);
+//   waves 4-7 (producers) prepare step s + 1, one block each: the block's prefix and suffix
+//     decay products and phases (scans over the lane's four tokens and the wave's four token
+//     segments; phase offsets of the earlier blocks from LDS), the operands conj(Q)G,
+//     conj(K)G, K Q (bf16, to LDS), then the block's Gram matrices L, A on the matrix cores
+//     from its own rows (no barrier: one wave wrote them) and the inverse
+//     N = (I + D_beta L)^{-1} in fp32; then the scans of step s + 2.
+//   Operands live in two LDS sets (steps s and s + 1).
 //
 // Complex products.  A complex 16 x 16 result block is held as two MFMA accumulator tiles,
 // its real and its imaginary part (lane (c, g) holds row 4g + r, column c of each, r = 0..3).
 // The left operand X is interleaved complex bf16 (lane word r = (Re, Im) of X[c][4g + r]);
 // the right operand Y enters two MFMAs, one per output part:
 //   real part:      B words (Re Y, -Im Y)        imaginary part:  B words (Im Y, Re Y)
-// built in-lane from either a split accumulator pair or an interleaved LDS word, so no lane
-// exchange is needed anywhere in the state-dependent chain.  Four real multiply-adds per
-// complex one (the real-coordinate view of Prop. 3.3), fp32 accumulation.
+// built in-lane (two converts from a split accumulator, or a sign flip and a half swap of
+// an LDS word), so no lane exchange is needed anywhere in the state-dependent chain.  Four
+// real multiply-adds per complex one (the real-coordinate view of Prop. 3.3), fp32
+// accumulation.
 //
 // Global memory goes through buffer resources: every lane offset is fixed for the whole
-// scan, the per-chunk part is folded into the resource base, and positions past the end of
+// scan, the per-step part is folded into the resource base, and positions past the end of
 // the sequence or past the last column read as zero (stores there are dropped), so the
 // ragged tail needs no branches.
 //
-// LDS layouts.  A C x 64 complex bf16 array has rows padded from 256 to 272 bytes; a
+// LDS layouts.  A 64 x 64 complex bf16 array has rows padded from 256 to 272 bytes; a
 // 16 x 16 complex bf16 block has 64-byte rows whose 16-byte chunks are XOR-swizzled by
 // (row >> 2) & 3.  Either way one MFMA operand fragment (4 consecutive complex values of one
-// row) is a single conflict-free 16-byte read.
+// row) is a single conflict-free 16-byte read.  conj(Q)G, conj(K)G and k_j / P_j are stored
+// token-major (rows = tokens), K Q channel-major (rows = channels), each the layout its
+// product reads as fragments.
 #include <utility>
 
 #include "sfda_device.h"
@@ -57,6 +70,8 @@ namespace pipe {
 
 constexpr int MP = 64;          // key channels per workgroup (m zero-padded)
 constexpr int NTH = 512;
+constexpr int CP = 64;          // tokens per pipeline step
+constexpr int NB = CP / 16;     // 16-token blocks per step
 
 typedef uint32_t u32;
 typedef u32 u32x2 __attribute__((ext_vector_type(2)));
@@ -96,12 +111,16 @@ __device__ __forceinline__ BPair bwords(u32x4 w) {
     return b;
 }
 
-// from a split accumulator pair holding Y[4g + r][c] (rounded to bf16 once)
+// from a split accumulator pair holding Y[4g + r][c]: (Re, -Im) and (Im, Re), each
+// component rounded to bf16 once (the same bits as a sign flip and half swap of one pair)
 __device__ __forceinline__ BPair bsplit(const CAcc& y) {
-    u32x4 w;
+    BPair b;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) w[r] = pack_bf16(y.re[r], y.im[r]);
-    return bwords(w);
+    for (int r = 0; r < 4; ++r) {
+        b.re[r] = pack_bf16(y.re[r], -y.im[r]);
+        b.im[r] = pack_bf16(y.im[r], y.re[r]);
+    }
+    return b;
 }
 
 // z += X Y over one K-block of 16 complex indices
@@ -152,14 +171,17 @@ template <int K>
 __device__ __forceinline__ float row_lane(float x) {
     return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x150 + K, 0xF, 0xF, false));
 }
-// quad permutation (DPP quad_perm selector P)
+// quad permutation (DPP quad_perm selector P: lane i of a quad takes lane (P >> 2i) & 3).
+// Call it where every lane of the wave is active (never as the unevaluated arm of a
+// conditional expression): under a reduced exec mask a lane whose source lane is switched
+// off reads the old register value instead of the source's data.
 template <int P>
 __device__ __forceinline__ float quad_lane(float x) {
     return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), P, 0xF, 0xF, false));
 }
 // ------------------------------------------------------------------ LDS addressing (bytes)
 
-// C x 64 complex bf16, row-major, rows padded to 272 bytes (68 words: consecutive rows start
+// 64 x 64 complex bf16, row-major, rows padded to 272 bytes (68 words: consecutive rows start
 // 4 banks apart, so 16 rows x one 16-byte chunk, or 16 consecutive words of 4 rows spaced
 // 4 apart, touch distinct banks).  Offsets are linear in row and column, so every fragment
 // address is one lane base plus an immediate.
@@ -176,8 +198,8 @@ __device__ __forceinline__ int blk_frag(int row, int chunk) {
 
 // ------------------------------------------------------------------ 16 x 16 inverse
 
-// N = (I - X)^{-1} for X strictly lower triangular (X = -(D_beta L') on a diagonal block),
-// i.e. N = I + X N, by forward substitution over the pivots s = 0 .. 14.  Lane (i, cg) --
+// N = (I - X)^{-1} for X strictly lower triangular (X = -(D_beta L) on a block), i.e.
+// N = I + X N, by forward substitution over the pivots s = 0 .. 14.  Lane (i, cg) --
 // i = lane % 16, cg = lane / 16 -- holds row i of X (zero on and above the diagonal, so
 // rows i <= s take no update) and row i, columns cg, cg + 4, cg + 8, cg + 12 of N (slot k
 // holds column 4k + cg); the pivot row N(s, .) is lane s of the lane's own 16-lane row (DPP
@@ -204,24 +226,22 @@ __device__ __forceinline__ void inv_steps(float (&nr)[4], float (&ni)[4], const 
 
 // ------------------------------------------------------------------ shared memory
 
-template <int C>
 struct Smem {
-    static constexpr int NRB = C / 16;
-    static constexpr int NLB = NRB * (NRB - 1) / 2 > 0 ? NRB * (NRB - 1) / 2 : 1;
-    static constexpr int NAQ = NRB * (NRB + 1) / 2;
     struct Set {
-        u32x4 qg[C * RP / 16];   // conj(q) g      [t][i]
-        u32x4 kg[C * RP / 16];   // conj(k) g      [t][i]
-        u32x4 ki[C * RP / 16];   // k / g          [t][i]
-        u32x4 lb[NLB * 64];      // -(D_beta L') off-diagonal blocks (p > q)
-        u32x4 nd[NRB * 64];      // N_pp = (I + (D_beta L')_pp)^{-1}
-        u32x4 aq[NAQ * 64];      // A lower blocks, zero above the diagonal
-        float beta[C];
-        float2 gc[MP];           // g_C
+        u32x4 qb[CP * RP / 16];  // conj(q_t) e^{i phi_t} P_t         [token][channel]
+        u32x4 kb[CP * RP / 16];  // conj(k_t) e^{i phi_t} P_t         [token][channel]
+        u32x4 kr[MP * RP / 16];  // k_t e^{-i phi_t} Q_t              [channel][token]
+        u32x4 nd[NB * 64];       // N_p = (I + D_beta L_p)^{-1}, one 16 x 16 block per block p
+        u32x4 aq[NB * 64];       // A_p, lower triangle with the diagonal
+        float beta[CP];
+        float dm[NB][MP];        // |D_p|: decay magnitude over block p, per channel
+        int bad[NB];             // block p lies outside the decay range
     };
     Set set[2];
-    float2 tot[4][MP];           // per producer wave: product of alpha, sum of theta / 2 pi
-    float2 xs[4][16][18];        // per producer wave: X of its diagonal block (fp32, padded)
+    u32x4 kd[CP * RP / 16];      // k_t e^{-i phi_t} / P_t (right operand of the blocks' Grams)
+    float2 xs[NB][16][18];       // per producer wave: X of its block (fp32, padded)
+    float tph[2][NB][MP];        // per block: theta / 2 pi summed over it, reduced to [0, 1)
+    float2 rot[MP];              // e^{i phi} at the last token: the final state rotation
 };
 
 struct Args {
@@ -244,55 +264,18 @@ __device__ __forceinline__ float tanh_f(float x) {
     return 1.f - 2.f * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(2.8853900817779268f * x));
 }
 
-// Gram units: 16 x 16 blocks (rb, jb) of a C x C Gram matrix, split over the four consumer
-// waves.  a_units: all blocks jb <= rb (the A Gram); l_units: the blocks jb < rb (the
-// off-diagonal part of L'; its diagonal blocks go to the producer that inverts them).
-__device__ __forceinline__ int a_units(int nrb, int wv, int (&units)[3][2])
-{
-    units[1][0] = units[1][1] = units[2][0] = units[2][1] = 0;
-    if (nrb == 4) {
-        const int tab[4][3][2] = {{{0, 0}, {3, 0}, {3, 1}}, {{1, 1}, {1, 0}, {3, 2}},
-                                  {{2, 2}, {2, 0}, {0, 0}}, {{3, 3}, {2, 1}, {0, 0}}};
-#pragma unroll
-        for (int k = 0; k < 3; ++k) { units[k][0] = tab[wv][k][0]; units[k][1] = tab[wv][k][1]; }
-        return wv < 2 ? 3 : 2;
-    }
-    if (nrb == 2) {
-        const int tab[4][2] = {{0, 0}, {1, 1}, {1, 0}, {0, 0}};
-        units[0][0] = tab[wv][0]; units[0][1] = tab[wv][1];
-        return wv < 3 ? 1 : 0;
-    }
-    units[0][0] = 0; units[0][1] = 0;
-    return wv == 0 ? 1 : 0;
-}
-__device__ __forceinline__ int l_units(int nrb, int wv, int (&units)[2][2])
-{
-    units[0][0] = 1; units[0][1] = 0; units[1][0] = 1; units[1][1] = 0;
-    if (nrb == 4) {
-        // waves 0, 1 carry three A units, so they take one L' unit and waves 2, 3 two
-        const int tab[4][2][2] = {{{3, 0}, {1, 0}}, {{3, 1}, {1, 0}}, {{3, 2}, {1, 0}}, {{2, 1}, {2, 0}}};
-#pragma unroll
-        for (int k = 0; k < 2; ++k) { units[k][0] = tab[wv][k][0]; units[k][1] = tab[wv][k][1]; }
-        return wv < 2 ? 1 : 2;
-    }
-    if (nrb == 2) return wv == 0 ? 1 : 0;
-    return 0;
-}
-
-template <typename TOUT, int C, bool GATED>
+template <typename TOUT, bool GATED>
 __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
 {
-    constexpr int NRB = C / 16;
-    constexpr int TPL = C / 16;          // tokens per producer lane (16 segments of TPL)
-    typedef typename Smem<C>::Set Set;
-    __shared__ Smem<C> sm;
+    typedef Smem::Set Set;
+    __shared__ Smem sm;
 
     const int T = args.T, m = args.m, n = args.n;
     const long bh = blockIdx.x / args.n_slices;
     const int sl = blockIdx.x - static_cast<int>(bh) * args.n_slices;
     const int n0 = sl * args.slice;
     const int scols = min(args.slice, n - n0);          // value columns of this slice
-    const int nchunks = (T + C - 1) / C;
+    const int nsteps = (T + CP - 1) / CP;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -307,19 +290,8 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
     const long base_t = bh * static_cast<long>(T);
 
     auto set_ptr = [&](int s) -> char* { return reinterpret_cast<char*>(&sm.set[s]); };
-    constexpr int OFF_QG = offsetof(Set, qg), OFF_KG = offsetof(Set, kg), OFF_KI = offsetof(Set, ki);
-    constexpr int OFF_LB = offsetof(Set, lb), OFF_ND = offsetof(Set, nd), OFF_AQ = offsetof(Set, aq);
-
-    // one Gram unit: z = rows rb of X (conj(Q)G or conj(K)G) times (K/G)^T, key block jb
-    auto gram = [&](const char* S, int xoff, int rb, int jb, CAcc& z) {
-        czero(z);
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-            const u32x4 a = *reinterpret_cast<const u32x4*>(S + xoff + rm_frag(rb * 16 + c, kb * 4 + g));
-            const u32x4 w = *reinterpret_cast<const u32x4*>(S + OFF_KI + rm_frag(jb * 16 + c, kb * 4 + g));
-            cmma(z, a, bwords(w));
-        }
-    };
+    constexpr int OFF_QB = offsetof(Set, qb), OFF_KB = offsetof(Set, kb), OFF_KR = offsetof(Set, kr);
+    constexpr int OFF_ND = offsetof(Set, nd), OFF_AQ = offsetof(Set, aq);
 
     if (consumer) {
         // ============================================================ consumer waves
@@ -340,218 +312,90 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         // (an access outside a buffer range touches no memory)
         const int v_row_bytes = args.v ? n * 4 : 0;
         const int o_row_bytes = args.o ? n * Out<TOUT>::BYTES : 0;
-        CAcc Sa[4];          // S rows kb*16 + 4g + r, column jw
-        BPair sb[4];         // S at the start of the chunk, as right operands
-        BPair db[NRB];       // Delta blocks as right operands
-        u32 vv[NRB][4];      // v of the chunk in flight (complex bf16), prefetched
+        CAcc Sa[4];          // rotated state, rows kb*16 + 4g + r, column jw
+        u32 vv[NB][4];       // v of the step in flight (complex bf16), prefetched
 
-        auto load_v = [&](int ch) {
+        auto load_v = [&](int st, int p) {
+            const int t0 = st * CP + p * 16;
+            const rsrc_t rv = make_rsrc(args.v + 2 * (base_tn + static_cast<long>(t0) * n),
+                                        max(T - t0, 0) * v_row_bytes);
 #pragma unroll
-            for (int p = 0; p < NRB; ++p) {
-                const int t0 = ch * C + p * 16;
-                const rsrc_t rv = make_rsrc(args.v + 2 * (base_tn + static_cast<long>(t0) * n),
-                                            max(T - t0, 0) * v_row_bytes);
-#pragma unroll
-                for (int r = 0; r < 4; ++r) vv[p][r] = ld32(rv, voff_v[r]);
-            }
+            for (int r = 0; r < 4; ++r) vv[p][r] = ld32(rv, voff_v[r]);
         };
 
-        // The products below run as software pipelines: the LDS operand fragments of stage
-        // s + 1 are requested before the MFMAs of stage s, and a scheduling barrier keeps the
-        // compiler from sinking the reads back next to their uses.
-        auto consume1 = [&](int ch) {          // Delta of chunk ch
-            const char* S = set_ptr(ch & 1);
-            const Set& st = sm.set[ch & 1];
+        TOUT* const go = static_cast<TOUT*>(args.o);
+        auto consume = [&](int st) {
+            const char* S = set_ptr(st & 1);
+            const Set& ss = sm.set[st & 1];
+            const int bad = __builtin_amdgcn_readfirstlane(ss.bad[0] | ss.bad[1] | ss.bad[2] | ss.bad[3]);
+            if (bad) {
+                const float nan = __builtin_nanf("");
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb) sb[kb] = bsplit(Sa[kb]);
-            // P = conj(K)G S: stage kb multiplies the kb-th channel block of every row block
-            CAcc R[NRB];
+                for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-            for (int p = 0; p < NRB; ++p) czero(R[p]);
-            u32x4 buf[2][NRB];
-            auto kg_load = [&](int kb, u32x4 (&f)[NRB]) {
-#pragma unroll
-                for (int p = 0; p < NRB; ++p)
-                    f[p] = *reinterpret_cast<const u32x4*>(S + OFF_KG + rm_frag(p * 16 + c, kb * 4 + g));
-            };
-            kg_load(0, buf[0]);
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb) {
-                if (kb + 1 < 4) kg_load(kb + 1, buf[(kb + 1) & 1]);
-                __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                for (int p = 0; p < NRB; ++p) cmma(R[p], buf[kb & 1][p], sb[kb]);
+                    for (int r = 0; r < 4; ++r) { Sa[kb].re[r] = nan; Sa[kb].im[r] = nan; }
             }
-            // the substitution's operands (diagonal inverses, off-diagonal blocks) in flight
-            // while R is formed
-            constexpr int NLBK = NRB * (NRB - 1) / 2;
-            u32x4 fn[NRB], fl[NLBK > 0 ? NLBK : 1];
 #pragma unroll
-            for (int p = 0; p < NRB; ++p)
-                fn[p] = *reinterpret_cast<const u32x4*>(S + OFF_ND + p * 1024 + blk_frag(c, g));
+            for (int p = 0; p < NB; ++p) {
+                const int t0 = st * CP + p * 16;
+                // the state as right operands (channel blocks kb)
+                BPair sb[4];
 #pragma unroll
-            for (int e = 0; e < NLBK; ++e)
-                fl[e] = *reinterpret_cast<const u32x4*>(S + OFF_LB + e * 1024 + blk_frag(c, g));
-            // R = D_beta (conj(V) - P)
+                for (int kb = 0; kb < 4; ++kb) sb[kb] = bsplit(Sa[kb]);
+                // P = conj(K)G S and O = conj(Q)G S over the block's 16 tokens
+                CAcc R, O;
+                czero(R);
+                czero(O);
 #pragma unroll
-            for (int p = 0; p < NRB; ++p) {
-                const float4 bt = *reinterpret_cast<const float4*>(&st.beta[p * 16 + 4 * g]);
+                for (int kb = 0; kb < 4; ++kb) {
+                    const u32x4 ak = *reinterpret_cast<const u32x4*>(S + OFF_KB + rm_frag(p * 16 + c, kb * 4 + g));
+                    const u32x4 aq = *reinterpret_cast<const u32x4*>(S + OFF_QB + rm_frag(p * 16 + c, kb * 4 + g));
+                    cmma(R, ak, sb[kb]);
+                    cmma(O, aq, sb[kb]);
+                }
+                // the state decays over the block: S <- |D_p| S (its operand form is taken)
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb) {
+                    const float4 d4 = *reinterpret_cast<const float4*>(&ss.dm[p][kb * 16 + 4 * g]);
+                    const float dr[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) { Sa[kb].re[r] *= dr[r]; Sa[kb].im[r] *= dr[r]; }
+                }
+                // R = D_beta (conj(V) - P)
+                const float4 bt = *reinterpret_cast<const float4*>(&ss.beta[p * 16 + 4 * g]);
                 const float btr[4] = {bt.x, bt.y, bt.z, bt.w};
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const u32 w = vv[p][r];
-                    R[p].re[r] = btr[r] * (bf_lo(w) - R[p].re[r]);
-                    R[p].im[r] = -btr[r] * (bf_hi(w) + R[p].im[r]);
+                    R.re[r] = btr[r] * (bf_lo(w) - R.re[r]);
+                    R.im[r] = -btr[r] * (bf_hi(w) + R.im[r]);
                 }
-            }
-            // Delta_p = N_pp (R_p + sum_{q<p} (-(D_beta L'))_pq Delta_q)
-#pragma unroll
-            for (int p = 0; p < NRB; ++p) {
-#pragma unroll
-                for (int q2 = 0; q2 < p; ++q2) cmma(R[p], fl[p * (p - 1) / 2 + q2], db[q2]);
+                if (st + 1 < nsteps) load_v(st + 1, p);     // this block's v is consumed
+                // Delta = N_p R
+                const u32x4 fn = *reinterpret_cast<const u32x4*>(S + OFF_ND + p * 1024 + blk_frag(c, g));
                 CAcc d;
                 czero(d);
-                cmma(d, fn[p], bsplit(R[p]));
-                db[p] = bsplit(d);
-            }
-            if (ch + 1 < nchunks) load_v(ch + 1);   // v of this chunk is consumed
-        };
-
-        TOUT* const go = static_cast<TOUT*>(args.o);
-        auto consume2 = [&](int ch) {          // outputs and state update of chunk ch
-            const char* S = set_ptr(ch & 1);
-            const Set& st = sm.set[ch & 1];
-            const int t0 = ch * C;
-            // stages: conj(Q)G S by channel block (4), tril(A) Delta by key block (NRB), then
-            // the state update (K/G)^T Delta two fragments at a time (2 NRB)
-            constexpr int NQ = 4, NA = NRB, NK = 2 * NRB, NST = NQ + NA + NK;
-            // state-update stage i multiplies fragments (tb, 2 kb2) and (tb', 2 kb2 + 1), tb' half
-            // the blocks away: independent accumulators, and the two fragments' rows far apart
-            // so that the compiler pairs each fragment's own reads
-            auto ki_tb = [&](int i, int e) { return e == 0 ? i % NRB : (i % NRB + NRB / 2) % NRB; };
-            auto ki_kb = [&](int i, int e) { return 2 * (i / NRB) + e; };
-            CAcc O[NRB];
+                cmma(d, fn, bsplit(R));
+                const BPair db = bsplit(d);
+                // O += A_p Delta; o = conj(O^*), rows past T and columns past the slice dropped
+                const u32x4 fa = *reinterpret_cast<const u32x4*>(S + OFF_AQ + p * 1024 + blk_frag(c, g));
+                cmma(O, fa, db);
+                const rsrc_t ro = make_rsrc(go + 2 * (base_tn + static_cast<long>(t0) * n),
+                                            max(T - t0, 0) * o_row_bytes);
 #pragma unroll
-            for (int rb = 0; rb < NRB; ++rb) czero(O[rb]);
-            u32x4 buf[2][4];
-            auto load = [&](int sg, u32x4 (&f)[4]) {
-                if (sg < NQ) {
+                for (int r = 0; r < 4; ++r) Out<TOUT>::store(ro, voff_o[r], O.re[r], -O.im[r]);
+                // S += (K Q)^T Delta: rows = channels kb*16 + c, K = the block's tokens
 #pragma unroll
-                    for (int rb = 0; rb < NRB; ++rb)
-                        f[rb] = *reinterpret_cast<const u32x4*>(S + OFF_QG + rm_frag(rb * 16 + c, sg * 4 + g));
-                } else if (sg < NQ + NA) {
-                    const int jb = sg - NQ;
-#pragma unroll
-                    for (int rb = 0; rb < NRB; ++rb)
-                        if (rb >= jb)
-                            f[rb] = *reinterpret_cast<const u32x4*>(S + OFF_AQ + (rb * (rb + 1) / 2 + jb) * 1024 + blk_frag(c, g));
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 2; ++e) {
-                        const int tb = ki_tb(sg - NQ - NA, e), kb = ki_kb(sg - NQ - NA, e);
-#pragma unroll
-                        for (int r = 0; r < 4; ++r)
-                            f[e][r] = *reinterpret_cast<const u32*>(S + OFF_KI + rm_off(tb * 16 + 4 * g + r, kb * 16 + c));
-                    }
-                }
-            };
-            auto mma = [&](int sg, const u32x4 (&f)[4]) {
-                if (sg < NQ) {
-#pragma unroll
-                    for (int rb = 0; rb < NRB; ++rb) cmma(O[rb], f[rb], sb[sg]);
-                } else if (sg < NQ + NA) {
-                    const int jb = sg - NQ;
-#pragma unroll
-                    for (int rb = 0; rb < NRB; ++rb)
-                        if (rb >= jb) cmma(O[rb], f[rb], db[jb]);
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 2; ++e) cmma(Sa[ki_kb(sg - NQ - NA, e)], f[e], db[ki_tb(sg - NQ - NA, e)]);
-                }
-            };
-            // o = conj(O^*) is final after the tril(A) Delta stages; its stores are spread
-            // over the state-update stages (two rows of four per stage), so they issue while
-            // those products run.  Rows past T and columns past the slice are dropped by the
-            // buffer range.
-            auto store_o = [&](int q) {
-                const int rb = q / 4, r = q % 4;
-                const int tr = t0 + rb * 16;
-                const rsrc_t ro = make_rsrc(go + 2 * (base_tn + static_cast<long>(tr) * n),
-                                            max(T - tr, 0) * o_row_bytes);
-                Out<TOUT>::store(ro, voff_o[r], O[rb].re[r], -O[rb].im[r]);
-            };
-            constexpr int SPS = 4 * NRB / NK;      // stores per state-update stage
-            load(0, buf[0]);
-#pragma unroll
-            for (int sg = 0; sg < NST; ++sg) {
-                if (sg + 1 < NST) load(sg + 1, buf[(sg + 1) & 1]);
-                __builtin_amdgcn_sched_barrier(0);
-                mma(sg, buf[sg & 1]);
-                if (sg >= NQ + NA) {
-#pragma unroll
-                    for (int e = 0; e < SPS; ++e) store_o((sg - NQ - NA) * SPS + e);
-                }
-            }
-            // S <- diag(g_C) (S + (K/G)^T Delta)
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const float2 gg = st.gc[kb * 16 + 4 * g + r];
-                    const float sr = Sa[kb].re[r], si = Sa[kb].im[r];
-                    Sa[kb].re[r] = __builtin_fmaf(gg.x, sr, -gg.y * si);
-                    Sa[kb].im[r] = __builtin_fmaf(gg.x, si, gg.y * sr);
-                }
-        };
-
-        auto consume_gram = [&](int ch) {      // A blocks of chunk ch (set ch & 1)
-            char* S = set_ptr(ch & 1);
-            int units[3][2];
-            const int nu = a_units(NRB, wave, units);
-            CAcc z[3];
-#pragma unroll
-            for (int u = 0; u < 3; ++u)
-                if (u < nu) gram(S, OFF_QG, units[u][0], units[u][1], z[u]);
-#pragma unroll
-            for (int u = 0; u < 3; ++u) {
-                if (u >= nu) continue;
-                const int rb = units[u][0], jb = units[u][1];
-                char* aqb = S + OFF_AQ + (rb * (rb + 1) / 2 + jb) * 1024;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const bool keep = jb < rb || c <= 4 * g + r;
-                    *reinterpret_cast<u32*>(aqb + blk_off(4 * g + r, c)) =
-                        keep ? pack_bf16(z[u].re[r], z[u].im[r]) : 0u;
+                for (int kb = 0; kb < 4; ++kb) {
+                    const u32x4 f = *reinterpret_cast<const u32x4*>(S + OFF_KR + rm_frag(kb * 16 + c, p * 4 + g));
+                    cmma(Sa[kb], f, db);
                 }
             }
         };
 
-        auto consume_lgram = [&](int ch) {     // off-diagonal blocks of -(D_beta L'), chunk ch
-            char* S = set_ptr(ch & 1);
-            const Set& st = sm.set[ch & 1];
-            int units[2][2];
-            const int nu = l_units(NRB, wave, units);
-            CAcc z[2];
-#pragma unroll
-            for (int u = 0; u < 2; ++u)
-                if (u < nu) gram(S, OFF_KG, units[u][0], units[u][1], z[u]);
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                if (u >= nu) continue;
-                const int rb = units[u][0], jb = units[u][1];
-                const float4 bt = *reinterpret_cast<const float4*>(&st.beta[rb * 16 + 4 * g]);
-                const float btr[4] = {bt.x, bt.y, bt.z, bt.w};
-                char* lbb = S + OFF_LB + (rb * (rb - 1) / 2 + jb) * 1024;
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    *reinterpret_cast<u32*>(lbb + blk_off(4 * g + r, c)) =
-                        pack_bf16(-btr[r] * z[u].re[r], -btr[r] * z[u].im[r]);
-            }
-        };
-
-        // The role test is wave-uniform and encloses each role's whole life (prologue, chunk
+        // The role test is wave-uniform and encloses each role's whole life (prologue, step
         // loop, epilogue), so each role keeps only its own registers live.  Both loops pass
-        // the same sequence of workgroup barriers: two per chunk plus the lead-in chunk.
+        // the same sequence of workgroup barriers: one per step plus the lead-in.
         if (active) {
             const rsrc_t rs = make_rsrc(args.S0 ? args.S0 + 2 * base_mn : args.S0,
                                         args.S0 ? m * n * 8 : 0);
@@ -565,18 +409,18 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     Sa[kb].re[r] = __uint_as_float(x.x);
                     Sa[kb].im[r] = __uint_as_float(x.y);
                 }
-            if (nchunks > 0) load_v(0);
+            if (nsteps > 0) {
+#pragma unroll
+                for (int p = 0; p < NB; ++p) load_v(0, p);
+            }
         }
         __syncthreads();          // matches the producers' lead-in barrier
-        for (int ch = -1; ch < nchunks; ++ch) {
-            if (active && ch >= 0) consume1(ch);
-            if (ch >= 0) consume_gram(ch);
-            __syncthreads();
-            if (active && ch >= 0) consume2(ch);
-            if (ch + 1 < nchunks) consume_lgram(ch + 1);  // operands written in phase 1
+        for (int st = -1; st < nsteps; ++st) {
+            if (active && st >= 0) consume(st);
             __syncthreads();
         }
         if (active && args.S_T != nullptr) {
+            // back from the rotated frame: S_T = diag(e^{i phi_T}) S
             const rsrc_t rs = make_rsrc(args.S_T + 2 * base_mn, m * n * 8);
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb)
@@ -584,50 +428,56 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 for (int r = 0; r < 4; ++r) {
                     const int i = kb * 16 + 4 * g + r;
                     const u32 off = (col_ok && i < m) ? static_cast<u32>(i * n + jw) * 8u : OOB;
-                    const u32x2 w = {__float_as_uint(Sa[kb].re[r]), __float_as_uint(Sa[kb].im[r])};
+                    float sr = Sa[kb].re[r], si = Sa[kb].im[r];
+                    if (nsteps > 0) {
+                        const float2 z = sm.rot[i];
+                        const float tr = __builtin_fmaf(z.x, sr, -z.y * si);
+                        si = __builtin_fmaf(z.x, si, z.y * sr);
+                        sr = tr;
+                    }
+                    const u32x2 w = {__float_as_uint(sr), __float_as_uint(si)};
                     __builtin_amdgcn_raw_buffer_store_b64(w, rs, off, 0, 0);
                 }
         }
     } else {
         // ============================================================ producer waves
-        // Wave pw owns tokens pw * C/4 .. pw * C/4 + C/4 - 1 of the chunk for all channels, so
+        // Wave pw owns block pw (tokens 16 pw .. 16 pw + 15) of every step for all channels, so
         // one load instruction covers whole rows of q, k, alpha, theta (whole cache lines).
-        // Lane = (channel group cg: channels 4cg .. 4cg+3; token segment tsg: TPL tokens).
-        constexpr int TPW = C / 4;                     // tokens per producer wave
+        // Lane = (channel group cg: channels 4cg .. 4cg+3; token segment tsg: 4 tokens).
         const int pw = wave - 4;
         const int tsg = lane & 3;
         const int cg = lane >> 2;
         const int pc0 = cg * 4;                        // first of this lane's 4 channels
-        const int tl0 = pw * TPW + tsg * TPL;          // first token (in the chunk) of the lane
+        const int tl0 = pw * 16 + tsg * 4;             // first token (in the step) of the lane
         const bool wide = (m & 3) == 0;               // 4-channel vector loads
-        u32 poff2[TPL], poff4[TPL];                   // byte offsets (bf16 / complex bf16)
+        u32 poff2[4], poff4[4];                       // byte offsets (bf16 / complex bf16)
 #pragma unroll
-        for (int u = 0; u < TPL; ++u) {
+        for (int u = 0; u < 4; ++u) {
             const u32 e = static_cast<u32>((tl0 + u) * m + pc0);
             poff2[u] = pc0 < m ? e * 2u : OOB;
             poff4[u] = pc0 < m ? e * 4u : OOB;
         }
-        uint2 pa[TPL], pt[TPL];           // alpha, theta of the 4 channels (bf16 pairs)
-        u32x4 pq[TPL], pk[TPL];           // q, k of the 4 channels (complex bf16)
+        uint2 pa[4], pt[4];               // alpha, theta of the 4 channels (bf16 pairs)
+        u32x4 pq[4], pk[4];               // q, k of the 4 channels (complex bf16)
         u32 pbeta = 0;
 
-        // alpha, theta of chunk ch (consumed by the scan, a phase before the rest)
-        auto load_at = [&](int ch) {
-            const int t0 = ch * C;
+        // alpha, theta of step st (consumed by the scan, a step before the rest)
+        auto load_at = [&](int st) {
+            const int t0 = st * CP;
             const long e0 = base_tm + static_cast<long>(t0) * m;
             const int rows = T - t0;
             const rsrc_t ra = make_rsrc(args.alpha + e0, rows * m * 2);
             const rsrc_t rt = make_rsrc(args.theta + e0, rows * m * 2);
             if (wide) {
 #pragma unroll
-                for (int u = 0; u < TPL; ++u) {
+                for (int u = 0; u < 4; ++u) {
                     const u32x2 a = ld64(ra, poff2[u]), t = ld64(rt, poff2[u]);
                     pa[u] = make_uint2(a.x, a.y);
                     pt[u] = make_uint2(t.x, t.y);
                 }
             } else {                    // any m: one channel per load
 #pragma unroll
-                for (int u = 0; u < TPL; ++u) {
+                for (int u = 0; u < 4; ++u) {
                     u32 a4[4], t4[4];
 #pragma unroll
                     for (int k = 0; k < 4; ++k) {
@@ -641,22 +491,22 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 }
             }
         };
-        // q, k, beta of chunk ch
-        auto load_qk = [&](int ch) {
-            const int t0 = ch * C;
+        // q, k, beta of step st (beta: lanes 0..15 hold the block's 16 tokens)
+        auto load_qk = [&](int st) {
+            const int t0 = st * CP;
             const long e0 = base_tm + static_cast<long>(t0) * m;
             const int rows = T - t0;
             const rsrc_t rq = make_rsrc(args.q + 2 * e0, rows * m * 4);
             const rsrc_t rk = make_rsrc(args.k + 2 * e0, rows * m * 4);
             if (wide) {
 #pragma unroll
-                for (int u = 0; u < TPL; ++u) {
+                for (int u = 0; u < 4; ++u) {
                     pq[u] = ld128(rq, poff4[u]);
                     pk[u] = ld128(rk, poff4[u]);
                 }
             } else {
 #pragma unroll
-                for (int u = 0; u < TPL; ++u)
+                for (int u = 0; u < 4; ++u)
 #pragma unroll
                     for (int k = 0; k < 4; ++k) {
                         const u32 e = static_cast<u32>((tl0 + u) * m + pc0 + k);
@@ -666,92 +516,111 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     }
             }
             const rsrc_t rb = make_rsrc(args.beta + base_t + t0, rows * 2);
-            pbeta = ld16(rb, static_cast<u32>(lane & (C - 1)) * 2u);
+            pbeta = ld16(rb, lane < 16 ? static_cast<u32>(pw * 16 + lane) * 2u : OOB);
         };
 
-        // Cumulative decay g_t = prod_{s <= t} alpha_s e^{i theta_s} per channel: the running
-        // product of alpha and the running sum of theta (in revolutions, the unit of the
-        // hardware sin / cos) are scanned in three levels -- over the lane's TPL tokens, over
-        // the four token segments of the wave (quad DPP), and over the waves (their totals,
-        // through LDS).  Positions past T or past m read as zero; alpha = 0 there is taken as
-        // 1 (a valid decay is positive), so g stays finite and g_C of a ragged chunk is g at
-        // its last token.
+        // Scans of one block per channel (three levels: the lane's 4 tokens, the wave's four
+        // segments by quad DPP, and for the phase the earlier blocks through LDS):
+        //   P_t = prod of alpha from the block's first token to t    (forwards, <= 1)
+        //   Q_t = prod of alpha from t + 1 to the block's last token (backwards, <= 1)
+        //   phi_t = sum of theta / 2 pi up to t, reduced to [0, 1) revolutions
+        // Positions past T or past m are identity tokens (alpha = 1, theta = 0).
         constexpr float INV_2PI = 0.15915494309189535f;
-        float lm[TPL][4], lph[TPL][4];    // inclusive over the lane's tokens
-        float qm[4], qph[4];              // exclusive over the wave's earlier segments
-        auto pretot_body = [&](int ch, auto padded) {
-            const bool s0 = tsg == 0, s01 = tsg < 2;
-            float tm[4], tp[4];
+        float Pf[4][4], Qb[4][4], ph[4][4];   // [token u][channel k] of the lane
+        float dtot[4], invd[4];               // block decay magnitude D and 1 / D per channel
+        int oor = 0;                          // a channel of the block decays below 2^-126
+        auto pretot_body = [&](int st, auto padded) {
+            const bool s0 = tsg == 0, s01 = tsg < 2, s3 = tsg == 3, s23 = tsg >= 2;
+            float tpk[4];
+            bool low = false;
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
-                float rm = 1.f, rp = 0.f;
+                float a[4], lp[4];
+                float rp = 0.f;
 #pragma unroll
-                for (int u = 0; u < TPL; ++u) {
+                for (int u = 0; u < 4; ++u) {
                     const u32 wa = k < 2 ? pa[u].x : pa[u].y;
                     const u32 wt = k < 2 ? pt[u].x : pt[u].y;
-                    float a = (k & 1) ? bf_hi(wa) : bf_lo(wa);
+                    float av = (k & 1) ? bf_hi(wa) : bf_lo(wa);
                     float th = (k & 1) ? bf_hi(wt) : bf_lo(wt);
                     if constexpr (GATED) {
-                        // a, th hold the pre-activations; padding (past T or m) stays the
-                        // identity token: alpha = 1 there, and tanh(0) = 0
-                        a = args.amin + args.aspan * sigmoid_f(a);
+                        av = args.amin + args.aspan * sigmoid_f(av);
                         th = args.tmax * tanh_f(th);
-                        if constexpr (decltype(padded)::value)
-                            a = (ch * C + tl0 + u < T && pc0 + k < m) ? a : 1.f;
-                    } else {
-                        if constexpr (decltype(padded)::value) a = a == 0.f ? 1.f : a;
                     }
-                    rm *= a;
-                    rp = __builtin_fmaf(th, INV_2PI, rp);
-                    lm[u][k] = rm;
-                    lph[u][k] = rp;
+                    if constexpr (decltype(padded)::value) {
+                        const bool ok = st * CP + tl0 + u < T && pc0 + k < m;
+                        av = ok ? av : 1.f;
+                        th = ok ? th : 0.f;
+                    }
+                    a[u] = av;
+                    rp = __builtin_amdgcn_fractf(__builtin_fmaf(th, INV_2PI, rp));
+                    lp[u] = rp;
                 }
-                // inclusive scan over the quad: shift by 1, then by 2
-                float ym = quad_lane<0x90>(rm), yp = quad_lane<0x90>(rp);     // [0, 0, 1, 2]
-                rm *= s0 ? 1.f : ym;
-                rp += s0 ? 0.f : yp;
-                ym = quad_lane<0x40>(rm); yp = quad_lane<0x40>(rp);           // [0, 0, 0, 1]
-                rm *= s01 ? 1.f : ym;
-                rp += s01 ? 0.f : yp;
-                ym = quad_lane<0x90>(rm); yp = quad_lane<0x90>(rp);
-                qm[k] = s0 ? 1.f : ym;
-                qph[k] = s0 ? 0.f : yp;
-                tm[k] = quad_lane<0xFF>(rm);                                   // [3, 3, 3, 3]
-                tp[k] = quad_lane<0xFF>(rp);
-            }
-            if (s0) {
-                float4* tw = reinterpret_cast<float4*>(&sm.tot[pw][pc0]);
-                tw[0] = make_float4(tm[0], tp[0], tm[1], tp[1]);
-                tw[1] = make_float4(tm[2], tp[2], tm[3], tp[3]);
-            }
-        };
-
-        // first two levels for chunk ch (inputs in pa, pt), wave totals to LDS.  Only a chunk
-        // with padding (ragged tail, m < 64) needs the alpha = 0 -> 1 substitution.
-        auto pretot = [&](int ch) {
-            if ((ch + 1) * C <= T && m == MP) pretot_body(ch, std::false_type{});
-            else pretot_body(ch, std::true_type{});
-        };
-
-        // phase 1: g and the operands conj(Q)G, conj(K)G, K/G of chunk ch into set ch & 1
-        auto produce1 = [&](int ch) {
-            char* S = set_ptr(ch & 1);
-            Set& st = sm.set[ch & 1];
-            float em[4], eph[4];
+                // lane level: inclusive prefix and exclusive suffix of alpha
+                const float m0 = a[0], m1 = m0 * a[1], m2 = m1 * a[2], m3 = m2 * a[3];
+                const float x2 = a[3], x1 = a[2] * a[3], x0 = a[1] * x1;
+                // quad level over the segments: exclusive prefix (earlier segments) and
+                // exclusive suffix (later segments) of the segment products, phase prefix
+                float im = m3, ip = rp, is = m3;
+                float y = quad_lane<0x90>(im), yp = quad_lane<0x90>(ip);       // [0, 0, 1, 2]
+                im *= s0 ? 1.f : y;
+                ip += s0 ? 0.f : yp;
+                y = quad_lane<0x40>(im); yp = quad_lane<0x40>(ip);             // [0, 0, 0, 1]
+                im *= s01 ? 1.f : y;
+                ip += s01 ? 0.f : yp;
+                float ys = quad_lane<0xF9>(is);                                // [1, 2, 3, 3]
+                is *= s3 ? 1.f : ys;
+                ys = quad_lane<0xFE>(is);                                      // [2, 3, 3, 3]
+                is *= s23 ? 1.f : ys;
+                // every lane takes part in each move; the selects come after
+                const float pm = quad_lane<0x90>(im), pp = quad_lane<0x90>(ip);
+                const float ps = quad_lane<0xF9>(is);
+                const float D = quad_lane<0xFF>(im), pt3 = quad_lane<0xFF>(ip);   // [3, 3, 3, 3]
+                const float em = s0 ? 1.f : pm;                                // exclusive prefix
+                const float ep = s0 ? 0.f : pp;
+                const float es = s3 ? 1.f : ps;                                // exclusive suffix
+                tpk[k] = __builtin_amdgcn_fractf(pt3);
+                Pf[0][k] = em * m0; Pf[1][k] = em * m1; Pf[2][k] = em * m2; Pf[3][k] = em * m3;
+                Qb[0][k] = es * x0; Qb[1][k] = es * x1; Qb[2][k] = es * x2; Qb[3][k] = es;
 #pragma unroll
-            for (int k = 0; k < 4; ++k) { em[k] = qm[k]; eph[k] = qph[k]; }
-            for (int w2 = 0; w2 < pw; ++w2) {          // totals of the earlier waves
-                const float4* tw = reinterpret_cast<const float4*>(&sm.tot[w2][pc0]);
-                const float4 t01 = tw[0], t23 = tw[1];
-                em[0] *= t01.x; eph[0] += t01.y; em[1] *= t01.z; eph[1] += t01.w;
-                em[2] *= t23.x; eph[2] += t23.y; em[3] *= t23.z; eph[3] += t23.w;
+                for (int u = 0; u < 4; ++u) ph[u][k] = ep + lp[u];
+                dtot[k] = D;
+                invd[k] = __builtin_amdgcn_rcpf(D);
+                low = low || !(D >= 1.17549435e-38f);          // below the normal range (or NaN)
+            }
+            oor = __builtin_amdgcn_readfirstlane(static_cast<int>(__builtin_amdgcn_ballot_w64(low) != 0));
+            if (s0) {
+                float4* tw = reinterpret_cast<float4*>(&sm.tph[st & 1][pw][pc0]);
+                tw[0] = make_float4(tpk[0], tpk[1], tpk[2], tpk[3]);
+            }
+        };
+
+        // scans of step st (inputs in pa, pt), the block's phase total to LDS.  Only a step
+        // with padding (ragged tail, m < 64) needs the identity-token substitution.
+        auto pretot = [&](int st) {
+            if ((st + 1) * CP <= T && m == MP) pretot_body(st, std::false_type{});
+            else pretot_body(st, std::true_type{});
+        };
+
+        float base[4] = {0.f, 0.f, 0.f, 0.f};   // phase (revolutions) before the step, per channel
+
+        // operands of step st into set st & 1: conj(Q)G, conj(K)G, K Q and the Gram operand
+        auto produce = [&](int st) {
+            char* S = set_ptr(st & 1);
+            Set& ss = sm.set[st & 1];
+            float off[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) off[k] = base[k];
+            for (int w2 = 0; w2 < pw; ++w2) {          // phases of the earlier blocks
+                const float4 t4 = *reinterpret_cast<const float4*>(&sm.tph[st & 1][w2][pc0]);
+                off[0] += t4.x; off[1] += t4.y; off[2] += t4.z; off[3] += t4.w;
             }
             // GATED: 1 / (||k~_t|| + eps) of the lane's tokens; a token row lives on the 16
             // lanes tsg + 4 cg (four per 16-lane row): rotate by 4 and 8 inside the row, then
             // exchange across rows
-            float kinv[TPL];
+            float kinv[4];
 #pragma unroll
-            for (int u = 0; u < TPL; ++u) {
+            for (int u = 0; u < 4; ++u) {
                 kinv[u] = 1.f;
                 if constexpr (GATED) {
                     float s2 = 0.f;
@@ -768,60 +637,94 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     kinv[u] = den > 0.f ? __builtin_amdgcn_rcpf(den) : 0.f;
                 }
             }
+            const bool last = st == nsteps - 1 && pw == NB - 1 && tsg == 3;
+            u32 krw[4][4];                       // [channel k][token u]
 #pragma unroll
-            for (int u = 0; u < TPL; ++u) {
+            for (int u = 0; u < 4; ++u) {
                 const int tl = tl0 + u;
-                u32x4 wq, wk, wi;
-                float2 gl[4];
+                u32x4 wq, wk, wd;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
-                    const float A = em[k] * lm[u][k];                // |g|
-                    const float Ph = eph[k] + lph[u][k];             // arg g / 2 pi
-                    const float ei = __builtin_amdgcn_rcpf(A);
-                    const float Ak = A * kinv[u], eik = ei * kinv[u];
+                    const float Ph = off[k] + ph[u][k];
                     const float sn = __builtin_amdgcn_sinf(Ph), cs = __builtin_amdgcn_cosf(Ph);
-                    const float gr = A * cs, gi = A * sn;
                     const u32 qw = pq[u][k], kw = pk[u][k];
                     const float qr = bf_lo(qw), qi = bf_hi(qw), kr = bf_lo(kw), ki = bf_hi(kw);
-                    // conj(k) e^{i phi}; conj(k) g = |g| of it, k / g = its conjugate / |g|
+                    // conj(q) e^{i phi}, conj(k) e^{i phi}; k e^{-i phi} is the latter's conjugate
+                    const float qur = __builtin_fmaf(qr, cs, qi * sn), qui = __builtin_fmaf(qr, sn, -qi * cs);
                     const float kur = __builtin_fmaf(kr, cs, ki * sn), kui = __builtin_fmaf(kr, sn, -ki * cs);
-                    wq[k] = pack_bf16(__builtin_fmaf(qr, gr, qi * gi), __builtin_fmaf(qr, gi, -qi * gr));
-                    wk[k] = pack_bf16(Ak * kur, Ak * kui);
-                    wi[k] = pack_bf16(eik * kur, -eik * kui);
-                    gl[k] = make_float2(gr, gi);
+                    const float P = Pf[u][k];
+                    const float Pk = P * kinv[u], Qk = Qb[u][k] * kinv[u];
+                    const float Dk = Qk * invd[k];             // 1 / P_t (= Q_t / D), times kinv
+                    wq[k] = pack_bf16(qur * P, qui * P);
+                    wk[k] = pack_bf16(kur * Pk, kui * Pk);
+                    wd[k] = pack_bf16(kur * Dk, -kui * Dk);
+                    krw[k][u] = pack_bf16(kur * Qk, -kui * Qk);
+                    if (last && u == 3) sm.rot[pc0 + k] = make_float2(cs, sn);
                 }
-                *reinterpret_cast<u32x4*>(S + OFF_QG + rm_off(tl, pc0)) = wq;
-                *reinterpret_cast<u32x4*>(S + OFF_KG + rm_off(tl, pc0)) = wk;
-                *reinterpret_cast<u32x4*>(S + OFF_KI + rm_off(tl, pc0)) = wi;
-                if (u == TPL - 1 && pw == 3 && tsg == 3) {     // token C - 1
-                    float4* gp = reinterpret_cast<float4*>(&st.gc[pc0]);
-                    gp[0] = make_float4(gl[0].x, gl[0].y, gl[1].x, gl[1].y);
-                    gp[1] = make_float4(gl[2].x, gl[2].y, gl[3].x, gl[3].y);
-                }
+                *reinterpret_cast<u32x4*>(S + OFF_QB + rm_off(tl, pc0)) = wq;
+                *reinterpret_cast<u32x4*>(S + OFF_KB + rm_off(tl, pc0)) = wk;
+                *reinterpret_cast<u32x4*>(reinterpret_cast<char*>(sm.kd) + rm_off(tl, pc0)) = wd;
             }
-            if (pw == 0 && lane < C) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const u32x4 w = {krw[k][0], krw[k][1], krw[k][2], krw[k][3]};
+                *reinterpret_cast<u32x4*>(S + OFF_KR + rm_off(pc0 + k, tl0)) = w;
+            }
+            // the phase reached after the step, for the next one
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                float tot = base[k];
+#pragma unroll
+                for (int w2 = 0; w2 < NB; ++w2) tot += sm.tph[st & 1][w2][pc0 + k];
+                base[k] = __builtin_amdgcn_fractf(tot);
+            }
+            if (lane < 16) {
                 float bt = bf16_bits_to_f32(static_cast<uint16_t>(pbeta));
-                if constexpr (GATED) bt = ch * C + lane < T ? sigmoid_f(bt) : 0.f;
-                st.beta[lane] = bt;
+                if constexpr (GATED) bt = st * CP + pw * 16 + lane < T ? sigmoid_f(bt) : 0.f;
+                ss.beta[pw * 16 + lane] = bt;
             }
+            if (tsg == 0) *reinterpret_cast<float4*>(&ss.dm[pw][pc0]) = make_float4(dtot[0], dtot[1], dtot[2], dtot[3]);
+            if (lane == 0) ss.bad[pw] = oor;
         };
 
-        // phase 2: diagonal blocks of L' and their inverses, chunk ch
-        auto invert_diag = [&](int ch) {
-            char* S = set_ptr(ch & 1);
-            const Set& st = sm.set[ch & 1];
-            CAcc z;
-            gram(S, OFF_KG, pw, pw, z);
-            // X = -(D_beta L') on the diagonal block, zero on and above the diagonal, to the
-            // wave's scratch; each lane then reads back one row
-            const float4 bt = *reinterpret_cast<const float4*>(&st.beta[pw * 16 + 4 * g]);
+        // the block's Gram matrices L (strict lower) and A (with the diagonal) and the
+        // inverse N = (I + D_beta L)^{-1}, from the rows this wave has just written
+        auto diag = [&](int st) {
+            char* S = set_ptr(st & 1);
+            const Set& ss = sm.set[st & 1];
+            // the wave's own LDS writes are complete before it reads them back
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            const char* KD = reinterpret_cast<const char*>(sm.kd);
+            CAcc zl, za;
+            czero(zl);
+            czero(za);
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) {
+                const u32x4 ak = *reinterpret_cast<const u32x4*>(S + OFF_KB + rm_frag(pw * 16 + c, kb * 4 + g));
+                const u32x4 aq = *reinterpret_cast<const u32x4*>(S + OFF_QB + rm_frag(pw * 16 + c, kb * 4 + g));
+                const u32x4 w = *reinterpret_cast<const u32x4*>(KD + rm_frag(pw * 16 + c, kb * 4 + g));
+                const BPair bw = bwords(w);
+                cmma(zl, ak, bw);
+                cmma(za, aq, bw);
+            }
+            // A_p: lower triangle with the diagonal, zero above
+            char* aqb = S + OFF_AQ + pw * 1024;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const bool keep = c <= 4 * g + r;
+                *reinterpret_cast<u32*>(aqb + blk_off(4 * g + r, c)) = keep ? pack_bf16(za.re[r], za.im[r]) : 0u;
+            }
+            // X = -(D_beta L), zero on and above the diagonal, to the wave's scratch; each
+            // lane then reads back one row
+            const float4 bt = *reinterpret_cast<const float4*>(&ss.beta[pw * 16 + 4 * g]);
             const float btr[4] = {bt.x, bt.y, bt.z, bt.w};
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const bool low = c < 4 * g + r;
-                sm.xs[pw][4 * g + r][c] = make_float2(low ? -btr[r] * z.re[r] : 0.f,
-                                                      low ? -btr[r] * z.im[r] : 0.f);
+                const bool lo = c < 4 * g + r;
+                sm.xs[pw][4 * g + r][c] = make_float2(lo ? -btr[r] * zl.re[r] : 0.f,
+                                                      lo ? -btr[r] * zl.im[r] : 0.f);
             }
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
             const int i = c, cgi = g;
             float2 xrow[16];
 #pragma unroll
@@ -840,26 +743,21 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     pack_bf16(nr[k], ni[k]);
         };
 
-        // phase 2: diagonal blocks of L' and their inverses, chunk ch; then the first two
-        // scan levels of chunk ch + 1 (alpha, theta fetched a phase earlier)
-        auto produce2 = [&](int ch) {
-            if (ch + 1 < nchunks) load_qk(ch + 1);
-            if (pw < NRB) invert_diag(ch);
-            if (ch + 1 < nchunks) pretot(ch + 1);
-        };
-
-        if (nchunks > 0) {
+        if (nsteps > 0) {
             load_at(0);
             load_qk(0);
             pretot(0);
         }
-        __syncthreads();          // wave totals of chunk 0
-        for (int ch = -1; ch < nchunks; ++ch) {
-            // alpha and theta two chunks ahead: the scan of chunk ch + 1 has consumed them
-            if (ch + 2 < nchunks) load_at(ch + 2);
-            if (ch + 1 < nchunks) produce1(ch + 1);
-            __syncthreads();
-            if (ch + 1 < nchunks) produce2(ch + 1);
+        __syncthreads();          // block phase totals of step 0
+        for (int st = -1; st < nsteps; ++st) {
+            // alpha and theta two steps ahead: the scan of step st + 1 has consumed them
+            if (st + 2 < nsteps) load_at(st + 2);
+            if (st + 1 < nsteps) {
+                produce(st + 1);
+                if (st + 2 < nsteps) load_qk(st + 2);
+                diag(st + 1);
+            }
+            if (st + 2 < nsteps) pretot(st + 2);
             __syncthreads();
         }
         // The compiler joins the two roles' control flow after the producer's exit, and the
@@ -884,21 +782,8 @@ static hipError_t launch_t(const ChunkLaunch& L, hipStream_t st)
     a.n_slices = (L.n + L.slice - 1) / L.slice;
     a.amin = L.alpha_min; a.aspan = L.alpha_max - L.alpha_min; a.tmax = L.theta_max; a.eps = L.eps;
     const dim3 grid(static_cast<unsigned>(static_cast<long>(L.B) * L.H * a.n_slices));
-    if (L.gated) {
-        switch (L.C) {
-            case 16: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 16, true>), grid, dim3(NTH), 0, st, a); break;
-            case 32: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 32, true>), grid, dim3(NTH), 0, st, a); break;
-            case 64: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 64, true>), grid, dim3(NTH), 0, st, a); break;
-            default: return hipErrorInvalidValue;
-        }
-        return hipGetLastError();
-    }
-    switch (L.C) {
-        case 16: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 16, false>), grid, dim3(NTH), 0, st, a); break;
-        case 32: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 32, false>), grid, dim3(NTH), 0, st, a); break;
-        case 64: hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, 64, false>), grid, dim3(NTH), 0, st, a); break;
-        default: return hipErrorInvalidValue;
-    }
+    if (L.gated) hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, true>), grid, dim3(NTH), 0, st, a);
+    else hipLaunchKernelGGL((chunk_pipe_kernel<TOUT, false>), grid, dim3(NTH), 0, st, a);
     return hipGetLastError();
 }
 

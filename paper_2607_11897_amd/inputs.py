@@ -38,7 +38,7 @@ import numpy as np
 @dataclasses.dataclass(frozen=True)
 class Laws:
     """Distribution laws of one workload (all drawn per token, per head)."""
-    alpha: tuple          # ("uniform", lo, hi) | ("softplus", scale)
+    alpha: tuple          # ("uniform", lo, hi) | ("softplus", scale) | ("mixed", lo, hi)
     theta: tuple          # ("uniform", lo, hi) | ("normal", std)
     beta: tuple           # ("uniform", lo, hi)
     s0_scale: Optional[float]  # None => zero initial state
@@ -138,6 +138,10 @@ def _cn(rng: np.random.Generator, shape) -> np.ndarray:
 def _alpha(rng, law, shape):
     if law[0] == "uniform":
         return rng.uniform(law[1], law[2], shape)
+    if law[0] == "mixed":           # even channels exactly 1, odd channels U(lo, hi)
+        a = rng.uniform(law[1], law[2], shape)
+        a[..., 0::2] = 1.0
+        return a
     if law[0] == "softplus":
         x = rng.standard_normal(shape)
         return np.exp(-np.logaddexp(0.0, x) / law[1])

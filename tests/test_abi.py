@@ -62,7 +62,7 @@ def test_chunk_argument_errors(lib):
     assert chunk(lib, o=None) == 1
     assert chunk(lib, m=0) == 2 and chunk(lib, m=65) == 2 and chunk(lib, n=0) == 2
     assert chunk(lib, T=-1) == 2 and chunk(lib, B=-1) == 2
-    assert chunk(lib, C=8) == 3 and chunk(lib, C=128) == 3
+    assert chunk(lib, C=8) == 3 and chunk(lib, C=256) == 3 and chunk(lib, C=48) == 3
     assert chunk(lib, din=2) == 4 and chunk(lib, dout=-1) == 4
     assert chunk(lib, q=P[0] + 8) == 5
     assert chunk(lib, o=P[0]) == 6                    # o on top of q
@@ -76,9 +76,9 @@ def test_chunk_argument_errors(lib):
     big = dict(zip(("q", "k", "v", "a", "th", "b", "s0", "o", "st"), Pf))
     assert chunk(lib, T=8388608, m=64, n=64, din=1, dout=1, **big) == 2
     assert chunk(lib, T=4194304, m=64, n=64, din=1, dout=0, **big) == 2    # fp32 o
-    # the float32 path addresses one chunk's rows of v and o with 32-bit byte offsets:
-    # C * n * 8 < 2^31 (n = 2^22 is refused at C = 64, though m * n * 8 < 2^31 with m = 1)
-    assert chunk(lib, T=64, m=1, n=1 << 22, C=64, **big) == 2
+    # the float32 kernels address one chunk's rows of v and o (at most 32 tokens) with 32-bit
+    # byte offsets: 32 * n * 8 < 2^31 (n = 2^23 is refused, though m * n * 8 < 2^31 with m = 1)
+    assert chunk(lib, T=64, m=1, n=1 << 23, C=64, **big) == 2
     # B*H == 0 is a no-op and never touches the pointers
     assert chunk(lib, B=0, q=None, o=None) == 0
 
@@ -114,6 +114,7 @@ def gated(lib, amin=0.9, amax=1.0, tmax=0.5, eps=0.0, C=16, q=P[0]):
 
 def test_gated_argument_errors(lib):
     assert gated(lib, amin=0.0) == 2                   # alpha must stay positive
+    assert gated(lib, amin=0.0042) == 2                # alpha_min^16 < 2^-126: outside the block range
     assert gated(lib, amin=0.95, amax=0.9) == 2
     assert gated(lib, amax=1.5) == 2
     assert gated(lib, tmax=-0.1) == 2
@@ -160,6 +161,7 @@ def test_bwd_workspace_bytes(lib):
     assert lib.sfda_chunk_bwd_workspace_bytes(8, 16, 4096, 64, 64, 64) == \
         lib.sfda_chunk_bwd_workspace_bytes(8, 16, 4096, 64, 64, 32)
     assert lib.sfda_chunk_bwd_workspace_bytes(1, 1, 65, 8, 8, 64) == 3 * (2 * 8 * 8 + 2 * 32 * 8) * 8
+    assert lib.sfda_chunk_bwd_workspace_bytes(1, 1, 65, 8, 8, 128) == 3 * (2 * 8 * 8 + 2 * 32 * 8) * 8
     assert lib.sfda_chunk_bwd_workspace_bytes(1, 1, 65, 8, 8, 16) == 5 * (2 * 8 * 8 + 2 * 16 * 8) * 8
     assert lib.sfda_chunk_bwd_workspace_bytes(1, 1, 0, 8, 8, 16) == 0
     for bad in [(0, 1, 4, 8, 8, 16), (1, 1, 4, 65, 8, 16), (1, 1, 4, 8, 0, 16), (1, 1, 4, 8, 8, 48)]:
@@ -172,7 +174,7 @@ def test_bwd_argument_errors(lib):
     assert bwd(lib, din=5) == 4
     assert bwd(lib, m=65) == 2
     assert bwd(lib, T=-1) == 2
-    assert bwd(lib, m=1, n=1 << 22, C=64) == 2                 # C * n * 8 >= 2^31 (32-bit row offsets)
+    assert bwd(lib, m=1, n=1 << 23, C=64) == 2                 # 32 * n * 8 >= 2^31 (32-bit row offsets)
     for idx in list(range(6)) + [7] + list(range(9, 15)):     # required: inputs, dO, gradients
         p = list(PB)
         p[idx] = 0
@@ -200,7 +202,7 @@ def test_decoupled_argument_errors(lib):
             B=1, H=1, T=4, m=8, n=8, C=16, din=0, dout=0):
         return lib.sfda_chunk_fwd_decoupled(q, k, r, v, a, th, eta, b, s0, o, st, B, H, T, m, n, C, din, dout, None)
     assert dec(B=0) == 0
-    assert dec(C=64) == 3
+    assert dec(C=256) == 3
     assert dec(C=48) == 3
     assert dec(r=0) == 1
     assert dec(b=0) == 1

@@ -89,15 +89,21 @@ def test_decoupled_tied_case_equals_chunk_fwd():
     assert eo <= 1e-5 and es <= 1e-5
 
 
-def test_decoupled_c64_is_rejected():
+def test_decoupled_chunk_lengths():
+    """C = 64 and 128 run at chunk length 32 (same bits as C = 32); other lengths are refused."""
     import torch
     from paper_2607_11897_amd import sfda
-    x = I.make_decoupled_inputs(1, 1, 16, 8, 8, "f32", seed=1)
+    x = I.make_decoupled_inputs(1, 2, 100, 16, 8, "f32", seed=1)
+    say("decoupled chunk lengths")
+    o32, S32 = run_dec(x, 32)
+    for C in (64, 128):
+        o, S = run_dec(x, C)
+        assert np.array_equal(o, o32) and np.array_equal(S, S32), C
     st = x.storage()
     d = {k: to_device(st[k], "f32") for k in ("q", "k", "r", "v", "alpha", "theta", "eta", "beta")}
     with pytest.raises(sfda.SfdaError):
         sfda.chunk_fwd_decoupled(d["q"], d["k"], d["r"], d["v"], d["alpha"], d["theta"], d["eta"], d["beta"],
-                                 None, C=64)
+                                 None, C=48)
     torch.cuda.synchronize()
 
 

@@ -30,7 +30,7 @@ def say(*a):
     print("[case]", *a, flush=True)
 
 
-def run_gated(g, C, eps, out_dtype=None):
+def run_gated(g, C, eps, out_dtype=None, gates=GATES):
     import torch
     from paper_2607_11897_amd import sfda
     st = g.storage()
@@ -38,16 +38,16 @@ def run_gated(g, C, eps, out_dtype=None):
     S0 = None if st["S0"] is None else to_device(st["S0"], "f32")
     od = None if out_dtype is None else {"f32": torch.float32, "bf16": torch.bfloat16}[out_dtype]
     o, S = sfda.chunk_fwd_gated(d["q"], d["k_raw"], d["v"], d["a"], d["b"], d["c"], S0, C=C,
-                                eps=eps, out_dtype=od, **GATES)
+                                eps=eps, out_dtype=od, **gates)
     torch.cuda.synchronize()
     return to_complex(o), to_complex(S)
 
 
-def oracle_gated(g, eps):
+def oracle_gated(g, eps, gp=GATES):
     import oracle
     from oracle import gates
-    alpha, theta, beta, k = gates.gates(g.a, g.b, g.c, g.k_raw, GATES["alpha_min"],
-                                        GATES["alpha_max"], GATES["theta_max"], eps)
+    alpha, theta, beta, k = gates.gates(g.a, g.b, g.c, g.k_raw, gp["alpha_min"],
+                                        gp["alpha_max"], gp["theta_max"], eps)
     return oracle.recurrence(g.q, k, g.v, alpha, theta, beta, g.S0)
 
 
@@ -73,6 +73,22 @@ def test_gated_matches_oracle(dtype, B, H, T, m, n, C, eps, zero_every):
     assert eo <= tol and es <= tol
 
 
+@pytest.mark.parametrize("dtype,C", [("f32", 64), ("bf16", 64), ("bf16", 16)])
+def test_gated_strong_decay(dtype, C):
+    """alpha_min = 0.01 with pre-activations a ~ N(-4, 3^2): most decays sit near alpha_min,
+    so a 16-token block decays to about 1e-32 (inside the range) and a 64-token chunk far
+    below the float range."""
+    gp = dict(alpha_min=0.01, alpha_max=1.0, theta_max=2.0)
+    g = I.make_gated_inputs(1, 2, 203, 64, 64, dtype, seed=41, a_mean=-4.0, a_std=3.0)
+    say("gated strong decay", dtype, "C", C)
+    o, S = run_gated(g, C, 1e-6, gates=gp)
+    o_ref, S_ref = oracle_gated(g, 1e-6, gp)
+    eo, es = rel_err(o, o_ref), rel_err(S, S_ref)
+    say("err(o)", eo, "err(S_T)", es)
+    tol = 1e-4 if dtype == "f32" else 2e-2
+    assert eo <= tol and es <= tol
+
+
 def test_gated_zero_state():
     g = I.make_gated_inputs(1, 2, 96, 64, 64, "f32", seed=3, s0_scale=None)
     o, S = run_gated(g, 32, 1e-6)
@@ -87,6 +103,7 @@ def test_gated_bad_parameters_raise():
     st = g.storage()
     d = {k: to_device(st[k], "f32") for k in ("q", "k_raw", "v", "a", "b", "c")}
     for bad in (dict(alpha_min=0.0, alpha_max=1.0, theta_max=0.5, eps=0.0),
+                dict(alpha_min=0.004, alpha_max=1.0, theta_max=0.5, eps=0.0),
                 dict(alpha_min=0.9, alpha_max=0.8, theta_max=0.5, eps=0.0),
                 dict(alpha_min=0.9, alpha_max=1.1, theta_max=0.5, eps=0.0),
                 dict(alpha_min=0.9, alpha_max=1.0, theta_max=-1.0, eps=0.0),
