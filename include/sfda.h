@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define SFDA_ABI_VERSION 1
+#define SFDA_ABI_VERSION 2
 
 typedef enum { SFDA_F32 = 0, SFDA_BF16 = 1 } sfda_dtype_t;
 
@@ -55,7 +55,9 @@ typedef enum {
     SFDA_ERR_DTYPE = 4,  /* unknown dtype                                                 */
     SFDA_ERR_ALIGN = 5,  /* a pointer is not 16-byte aligned                              */
     SFDA_ERR_ALIAS = 6,  /* an output overlaps an input or another output                 */
-    SFDA_ERR_HIP = 7     /* the HIP runtime reported an error when launching              */
+    SFDA_ERR_HIP = 7,    /* the HIP runtime reported an error when launching              */
+    SFDA_ERR_SCRATCH = 8 /* sfda_chunk_fwd_segmented_noalloc: the call needs more workspace
+                            than SFDA_NOALLOC_SCRATCH_BYTES                                */
 } sfda_status_t;
 
 /* A hipStream_t passed as an opaque pointer; NULL means the default (null) stream. */
@@ -175,6 +177,29 @@ sfda_status_t sfda_chunk_fwd_decoupled(const void* q, const void* k, const void*
  *   S_T == S0 (in place) is allowed.
  */
 size_t sfda_chunk_fwd_segmented_workspace_bytes(int B, int H, int m, int n, int G);
+
+/*
+ * sfda_chunk_fwd_segmented_noalloc -- sfda_chunk_fwd_segmented for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the workspace is a static device array of SFDA_NOALLOC_SCRATCH_BYTES
+ * inside the library, one per GPU, held until the process ends.  The call itself allocates
+ * nothing (no hipMalloc, hipFree or allocating library routine); its first call on a device
+ * looks up that device's scratch address (hipGetSymbolAddress, with the device current).
+ *   Arguments, results and errors as sfda_chunk_fwd_segmented without the workspace; a call
+ *   whose workspace (sfda_chunk_fwd_segmented_workspace_bytes) exceeds
+ *   SFDA_NOALLOC_SCRATCH_BYTES returns SFDA_ERR_SCRATCH before anything is launched.
+ *   Every call on one GPU shares that GPU's scratch (no initial contents are needed; each
+ *   call overwrites what it uses): calls that overlap in time on one GPU (different
+ *   streams, or different host threads without ordering) race.
+ */
+#define SFDA_NOALLOC_SCRATCH_BYTES (32u * 1024u * 1024u)
+
+sfda_status_t sfda_chunk_fwd_segmented_noalloc(const void* q, const void* k, const void* v,
+                                               const void* alpha, const void* theta,
+                                               const void* beta, const float* S0, void* o,
+                                               float* S_T, int B, int H, int T, int m, int n,
+                                               int C, int G, sfda_dtype_t in_dtype,
+                                               sfda_dtype_t out_dtype, sfda_stream_t stream);
 
 sfda_status_t sfda_chunk_fwd_segmented(const void* q, const void* k, const void* v,
                                        const void* alpha, const void* theta, const void* beta,

@@ -1,8 +1,16 @@
 // C-ABI entry points of libsfda: argument validation, then one kernel launch.
 #include <stdint.h>
 
+#include <mutex>
+
 #include "../../include/sfda.h"
 #include "sfda_launch.h"
+
+// Workspace of sfda_chunk_fwd_segmented_noalloc: a file-scope device array, one copy per GPU
+// the library runs on, held until the process ends.  In host code its name is only a
+// stand-in; the device address comes from hipGetSymbolAddress (per device, with that device
+// current) and only that address is handed to kernels.
+static __device__ __align__(256) unsigned char scratch[SFDA_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -25,6 +33,25 @@ long esize(sfda_dtype_t d) { return d == SFDA_BF16 ? 2 : 4; }
 
 bool dtype_ok(sfda_dtype_t d) { return d == SFDA_F32 || d == SFDA_BF16; }
 
+// the device address of `scratch` on the current device, looked up once per device
+constexpr int MAX_DEVICES = 64;
+std::mutex scratch_mu;
+void* scratch_ptr[MAX_DEVICES];
+
+sfda_status_t scratch_address(void** out)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES) return SFDA_ERR_HIP;
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    if (scratch_ptr[dev] == nullptr) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return SFDA_ERR_HIP;
+        scratch_ptr[dev] = p;
+    }
+    *out = scratch_ptr[dev];
+    return SFDA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -40,6 +67,7 @@ const char* sfda_status_string(sfda_status_t s)
         case SFDA_ERR_ALIGN: return "a pointer is not 16-byte aligned";
         case SFDA_ERR_ALIAS: return "an output buffer overlaps another buffer";
         case SFDA_ERR_HIP: return "the HIP runtime reported an error";
+        case SFDA_ERR_SCRATCH: return "the call needs more workspace than the static scratch holds";
     }
     return "unknown status";
 }
@@ -201,12 +229,14 @@ size_t sfda_chunk_fwd_segmented_workspace_bytes(int B, int H, int m, int n, int 
     return static_cast<size_t>(segs) * (static_cast<size_t>(m) * m + 2 * static_cast<size_t>(m) * n) * 8;
 }
 
-sfda_status_t sfda_chunk_fwd_segmented(const void* q, const void* k, const void* v,
-                                       const void* alpha, const void* theta, const void* beta,
-                                       const float* S0, void* o, float* S_T, int B, int H, int T,
-                                       int m, int n, int C, int G, sfda_dtype_t in_dtype,
-                                       sfda_dtype_t out_dtype, void* workspace,
-                                       size_t workspace_bytes, sfda_stream_t stream)
+// sfda_chunk_fwd_segmented, and with noalloc the workspace taken from the static scratch
+// (its size checked first, its address fetched only after every other argument check)
+static sfda_status_t segmented_impl(const void* q, const void* k, const void* v,
+                                    const void* alpha, const void* theta, const void* beta,
+                                    const float* S0, void* o, float* S_T, int B, int H, int T,
+                                    int m, int n, int C, int G, sfda_dtype_t in_dtype,
+                                    sfda_dtype_t out_dtype, void* workspace,
+                                    size_t workspace_bytes, sfda_stream_t stream, bool noalloc)
 {
     if (G < 1) return SFDA_ERR_SHAPE;
     const int slice_n = n <= 64 ? ((n + 7) / 8) * 8 : 64;
@@ -218,6 +248,17 @@ sfda_status_t sfda_chunk_fwd_segmented(const void* q, const void* k, const void*
     if (T % (static_cast<long>(G) * C) != 0) return SFDA_ERR_SHAPE;
     const long BH = static_cast<long>(B) * H;
     if (BH * G > 0x7FFFFFFFL) return SFDA_ERR_SHAPE;
+    if (noalloc) {
+        if (sfda_chunk_fwd_segmented_workspace_bytes(B, H, m, n, G) > SFDA_NOALLOC_SCRATCH_BYTES)
+            return SFDA_ERR_SCRATCH;
+        const sfda_status_t st0 = chunk_fwd_impl(q, k, v, alpha, theta, beta, S0, o, S_T, B, H, T,
+                                                 m, n, C, in_dtype, out_dtype, stream, slice_n,
+                                                 nullptr, 0, /*check_only=*/true);
+        if (st0 != SFDA_OK) return st0;
+        const sfda_status_t st1 = scratch_address(&workspace);
+        if (st1 != SFDA_OK) return st1;
+        workspace_bytes = SFDA_NOALLOC_SCRATCH_BYTES;
+    }
     if (!workspace) return SFDA_ERR_NULL;
     if (!aligned16(workspace)) return SFDA_ERR_ALIGN;
     const size_t need = sfda_chunk_fwd_segmented_workspace_bytes(B, H, m, n, G);
@@ -263,6 +304,28 @@ sfda_status_t sfda_chunk_fwd_segmented(const void* q, const void* k, const void*
     L.S0 = Sin; L.S_T = nullptr; L.o = o;
     if (sfda::launch_chunk(L, st) != hipSuccess) return SFDA_ERR_HIP;
     return SFDA_OK;
+}
+
+sfda_status_t sfda_chunk_fwd_segmented(const void* q, const void* k, const void* v,
+                                       const void* alpha, const void* theta, const void* beta,
+                                       const float* S0, void* o, float* S_T, int B, int H, int T,
+                                       int m, int n, int C, int G, sfda_dtype_t in_dtype,
+                                       sfda_dtype_t out_dtype, void* workspace,
+                                       size_t workspace_bytes, sfda_stream_t stream)
+{
+    return segmented_impl(q, k, v, alpha, theta, beta, S0, o, S_T, B, H, T, m, n, C, G, in_dtype,
+                          out_dtype, workspace, workspace_bytes, stream, false);
+}
+
+sfda_status_t sfda_chunk_fwd_segmented_noalloc(const void* q, const void* k, const void* v,
+                                               const void* alpha, const void* theta,
+                                               const void* beta, const float* S0, void* o,
+                                               float* S_T, int B, int H, int T, int m, int n,
+                                               int C, int G, sfda_dtype_t in_dtype,
+                                               sfda_dtype_t out_dtype, sfda_stream_t stream)
+{
+    return segmented_impl(q, k, v, alpha, theta, beta, S0, o, S_T, B, H, T, m, n, C, G, in_dtype,
+                          out_dtype, nullptr, 0, stream, true);
 }
 
 // the backward's chunk length: C = 64 and 128 run at 32 (the gradient pass stages a block

@@ -16,9 +16,11 @@ LIB_PATH = os.path.join(HERE, "libsfda.so")
 
 SFDA_F32, SFDA_BF16 = 0, 1
 STATUS = {0: "SFDA_OK", 1: "SFDA_ERR_NULL", 2: "SFDA_ERR_SHAPE", 3: "SFDA_ERR_CHUNK",
-          4: "SFDA_ERR_DTYPE", 5: "SFDA_ERR_ALIGN", 6: "SFDA_ERR_ALIAS", 7: "SFDA_ERR_HIP"}
+          4: "SFDA_ERR_DTYPE", 5: "SFDA_ERR_ALIGN", 6: "SFDA_ERR_ALIAS", 7: "SFDA_ERR_HIP",
+          8: "SFDA_ERR_SCRATCH"}
+NOALLOC_SCRATCH_BYTES = 32 * 1024 * 1024      # SFDA_NOALLOC_SCRATCH_BYTES
 EXPORTS = ("sfda_chunk_fwd", "sfda_chunk_fwd_sliced", "sfda_chunk_fwd_gated", "sfda_chunk_fwd_decoupled",
-           "sfda_chunk_fwd_segmented",
+           "sfda_chunk_fwd_segmented", "sfda_chunk_fwd_segmented_noalloc",
            "sfda_chunk_fwd_segmented_workspace_bytes", "sfda_chunk_bwd", "sfda_chunk_bwd_workspace_bytes",
            "sfda_step", "sfda_status_string", "sfda_abi_version")
 
@@ -53,6 +55,8 @@ def load_library(path: str = LIB_PATH):
     lib.sfda_chunk_fwd_decoupled.restype = i
     lib.sfda_chunk_fwd_segmented.argtypes = [vp] * 9 + [i] * 7 + [i, i, vp, ctypes.c_size_t, vp]
     lib.sfda_chunk_fwd_segmented.restype = i
+    lib.sfda_chunk_fwd_segmented_noalloc.argtypes = [vp] * 9 + [i] * 7 + [i, i, vp]
+    lib.sfda_chunk_fwd_segmented_noalloc.restype = i
     lib.sfda_chunk_fwd_segmented_workspace_bytes.argtypes = [i] * 5
     lib.sfda_chunk_fwd_segmented_workspace_bytes.restype = ctypes.c_size_t
     lib.sfda_chunk_bwd.argtypes = [vp] * 16 + [i] * 6 + [i, i, vp, ctypes.c_size_t, vp]
@@ -175,6 +179,38 @@ def chunk_fwd(q, k, v, alpha, theta, beta, S0=None, C: int = 64, *, o=None, S_T=
         st = lib.sfda_chunk_fwd_sliced(*args, slice, in_code, _dtype_code(o), _stream(stream))
     if st != 0:
         raise SfdaError(st, "sfda_chunk_fwd")
+    return o, S_T
+
+
+def chunk_fwd_segmented_noalloc(q, k, v, alpha, theta, beta, S0=None, C: int = 64, *, segments: int,
+                                o=None, S_T=None, out_dtype=None, want_state: bool = True,
+                                stream=None) -> Tuple:
+    """chunk_fwd with `segments` parallel segments per head whose workspace is the library's
+    static scratch (sfda_chunk_fwd_segmented_noalloc: the call allocates no device memory;
+    o and S_T are allocated here only when not given).  Shapes and results as chunk_fwd."""
+    import torch
+    lib = load_library()
+    B, H, T, m, _ = _dims(q, v, 5)
+    n = v.shape[3]
+    in_code = _dtype_code(q)
+    for t in (k, v, alpha, theta, beta):
+        if t.dtype != q.dtype:
+            raise TypeError("q, k, v, alpha, theta, beta must share one dtype")
+    out_dtype = q.dtype if out_dtype is None else out_dtype
+    if o is None:
+        o = torch.empty((B, H, T, n, 2), dtype=out_dtype, device=q.device)
+    if S_T is None and want_state:
+        S_T = torch.empty((B, H, m, n, 2), dtype=torch.float32, device=q.device)
+    _need_f32(S0=S0, S_T=S_T)
+    _dtype_code(o)
+    _check(dict(q=(q, (B, H, T, m, 2)), k=(k, (B, H, T, m, 2)), v=(v, (B, H, T, n, 2)),
+                alpha=(alpha, (B, H, T, m)), theta=(theta, (B, H, T, m)), beta=(beta, (B, H, T)),
+                S0=(S0, (B, H, m, n, 2)), o=(o, (B, H, T, n, 2)), S_T=(S_T, (B, H, m, n, 2))))
+    st = lib.sfda_chunk_fwd_segmented_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(theta), _ptr(beta),
+                                              _ptr(S0), _ptr(o), _ptr(S_T), B, H, T, m, n, C, segments,
+                                              in_code, _dtype_code(o), _stream(stream))
+    if st != 0:
+        raise SfdaError(st, "sfda_chunk_fwd_segmented_noalloc")
     return o, S_T
 
 
