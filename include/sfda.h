@@ -102,8 +102,10 @@ sfda_status_t sfda_chunk_fwd(const void* q, const void* k, const void* v,
  * columns are independent in the recurrence (column j of S only mixes with column j of
  * v^*), so the library splits them into ceil(n / slice) workgroups per (b, h); a smaller
  * slice gives more workgroups at the cost of repeating the chunk factors per slice.
- * sfda_chunk_fwd uses slice = min(64, n rounded up to a multiple of 8).  Results are the
- * same up to rounding for every slice.
+ * sfda_chunk_fwd uses slice = min(64, n rounded up to a multiple of 8), halved to 32 when
+ * the heads alone would leave more than half of the device's compute units idle
+ * (2 * B * H * ceil(n / slice) <= compute units).  Every column's arithmetic is the same for
+ * every slice, so the results are bitwise the same.
  */
 sfda_status_t sfda_chunk_fwd_sliced(const void* q, const void* k, const void* v,
                                     const void* alpha, const void* theta, const void* beta,

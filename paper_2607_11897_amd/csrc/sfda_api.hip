@@ -52,6 +52,36 @@ sfda_status_t scratch_address(void** out)
     return SFDA_OK;
 }
 
+// compute units of the current device (0 if it cannot be queried), looked up once per device
+std::mutex cu_mu;
+int cu_count_cache[MAX_DEVICES];
+
+int device_cus()
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES) return 0;
+    std::lock_guard<std::mutex> lock(cu_mu);
+    if (cu_count_cache[dev] == 0) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+        cu_count_cache[dev] = v;
+    }
+    return cu_count_cache[dev];
+}
+
+// sfda_chunk_fwd's value columns per workgroup: all of a head's columns (up to 64), halved
+// to 32 while the heads alone would leave more than half of the compute units idle (each
+// workgroup scans its head's sequence on one compute unit; the column slices of a head repeat
+// its chunk factors but scan in parallel).  Every column's arithmetic is the same for every
+// slice, so the results do not depend on it.
+int auto_slice(long BH, int n)
+{
+    int slice = n <= 64 ? ((n + 7) / 8) * 8 : 64;
+    const long cus = device_cus();
+    if (slice > 32 && cus > 0 && 2 * BH * ((n + slice - 1) / slice) <= cus) slice = 32;
+    return slice;
+}
+
 }  // namespace
 
 extern "C" {
@@ -153,7 +183,7 @@ sfda_status_t sfda_chunk_fwd(const void* q, const void* k, const void* v, const 
                              float* S_T, int B, int H, int T, int m, int n, int C,
                              sfda_dtype_t in_dtype, sfda_dtype_t out_dtype, sfda_stream_t stream)
 {
-    const int slice = n <= 64 ? ((n + 7) / 8) * 8 : 64;
+    const int slice = auto_slice(static_cast<long>(B) * H, n);
     return chunk_fwd_impl(q, k, v, alpha, theta, beta, S0, o, S_T, B, H, T, m, n, C, in_dtype,
                           out_dtype, stream, slice);
 }
@@ -182,7 +212,7 @@ sfda_status_t sfda_chunk_fwd_gated(const void* q, const void* k_raw, const void*
     constexpr float ALPHA_MIN_GATED = 0.0042719f;     // 2^(-7.875), rounded up
     if (!(alpha_min >= ALPHA_MIN_GATED && alpha_min <= alpha_max && alpha_max <= 1.f)) return SFDA_ERR_SHAPE;
     if (!(theta_max >= 0.f && theta_max < 3.4e38f && eps >= 0.f && eps < 3.4e38f)) return SFDA_ERR_SHAPE;
-    const int slice = n <= 64 ? ((n + 7) / 8) * 8 : 64;
+    const int slice = auto_slice(static_cast<long>(B) * H, n);
     sfda::GateParams gp{true, alpha_min, alpha_max, theta_max, eps};
     return chunk_fwd_impl(q, k_raw, v, a, b, c, S0, o, S_T, B, H, T, m, n, C, in_dtype, out_dtype,
                           stream, slice, nullptr, 0, false, &gp);

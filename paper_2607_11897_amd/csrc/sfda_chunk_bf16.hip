@@ -72,6 +72,7 @@ constexpr int MP = 64;          // key channels per workgroup (m zero-padded)
 constexpr int NTH = 512;
 constexpr int CP = 64;          // tokens per pipeline step
 constexpr int NB = CP / 16;     // 16-token blocks per step
+constexpr int NB1 = 3;          // blocks the consumers walk before the step's middle barrier
 
 typedef uint32_t u32;
 typedef u32 u32x2 __attribute__((ext_vector_type(2)));
@@ -324,11 +325,11 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         };
 
         TOUT* const go = static_cast<TOUT*>(args.o);
-        auto consume = [&](int st) {
+        auto consume = [&](int st, int p0, int p1) {
             const char* S = set_ptr(st & 1);
             const Set& ss = sm.set[st & 1];
             const int bad = __builtin_amdgcn_readfirstlane(ss.bad[0] | ss.bad[1] | ss.bad[2] | ss.bad[3]);
-            if (bad) {
+            if (p0 == 0 && bad) {
                 const float nan = __builtin_nanf("");
 #pragma unroll
                 for (int kb = 0; kb < 4; ++kb)
@@ -337,6 +338,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             }
 #pragma unroll
             for (int p = 0; p < NB; ++p) {
+                if (p < p0 || p >= p1) continue;
                 const int t0 = st * CP + p * 16;
                 // the state as right operands (channel blocks kb)
                 BPair sb[4];
@@ -393,6 +395,62 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             }
         };
 
+        // block `wave` of step st: its Gram matrices L (strict lower) and A (with the diagonal)
+        // and the inverse N = (I + D_beta L)^{-1}, from the operands the producers wrote before
+        // the last barrier
+        auto diag = [&](int st) {
+            const int pw = wave;                 // this wave's block
+            char* S = set_ptr(st & 1);
+            const Set& ss = sm.set[st & 1];
+            const char* KD = reinterpret_cast<const char*>(sm.kd);
+            CAcc zl, za;
+            czero(zl);
+            czero(za);
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) {
+                const u32x4 ak = *reinterpret_cast<const u32x4*>(S + OFF_KB + rm_frag(pw * 16 + c, kb * 4 + g));
+                const u32x4 aq = *reinterpret_cast<const u32x4*>(S + OFF_QB + rm_frag(pw * 16 + c, kb * 4 + g));
+                const u32x4 w = *reinterpret_cast<const u32x4*>(KD + rm_frag(pw * 16 + c, kb * 4 + g));
+                const BPair bw = bwords(w);
+                cmma(zl, ak, bw);
+                cmma(za, aq, bw);
+            }
+            // A_p: lower triangle with the diagonal, zero above
+            char* aqb = S + OFF_AQ + pw * 1024;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const bool keep = c <= 4 * g + r;
+                *reinterpret_cast<u32*>(aqb + blk_off(4 * g + r, c)) = keep ? pack_bf16(za.re[r], za.im[r]) : 0u;
+            }
+            // X = -(D_beta L), zero on and above the diagonal, to the wave's scratch; each
+            // lane then reads back one row
+            const float4 bt = *reinterpret_cast<const float4*>(&ss.beta[pw * 16 + 4 * g]);
+            const float btr[4] = {bt.x, bt.y, bt.z, bt.w};
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const bool lo = c < 4 * g + r;
+                sm.xs[pw][4 * g + r][c] = make_float2(lo ? -btr[r] * zl.re[r] : 0.f,
+                                                      lo ? -btr[r] * zl.im[r] : 0.f);
+            }
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            const int i = c, cgi = g;
+            float2 xrow[16];
+#pragma unroll
+            for (int s2 = 0; s2 < 16; s2 += 2) {
+                const float4 x2 = *reinterpret_cast<const float4*>(&sm.xs[pw][i][s2]);
+                xrow[s2] = make_float2(x2.x, x2.y);
+                xrow[s2 + 1] = make_float2(x2.z, x2.w);
+            }
+            float nr[4], ni[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) { nr[k] = i == 4 * k + cgi ? 1.f : 0.f; ni[k] = 0.f; }
+            inv_steps(nr, ni, xrow, std::make_integer_sequence<int, 15>{});
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                *reinterpret_cast<u32*>(S + OFF_ND + pw * 1024 + blk_off(i, 4 * k + cgi)) =
+                    pack_bf16(nr[k], ni[k]);
+        };
+
         // The role test is wave-uniform and encloses each role's whole life (prologue, step
         // loop, epilogue), so each role keeps only its own registers live.  Both loops pass
         // the same sequence of workgroup barriers: one per step plus the lead-in.
@@ -416,7 +474,12 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         }
         __syncthreads();          // matches the producers' lead-in barrier
         for (int st = -1; st < nsteps; ++st) {
-            if (active && st >= 0) consume(st);
+            // phase 1: the first NB1 blocks of step st (the producers form step st + 1's operands)
+            if (active && st >= 0) consume(st, 0, NB1);
+            __syncthreads();
+            // phase 2: this wave's block of step st + 1 (Grams, inverse), the rest of step st
+            if (st + 1 < nsteps) diag(st + 1);
+            if (active && st >= 0) consume(st, NB1, NB);
             __syncthreads();
         }
         if (active && args.S_T != nullptr) {
@@ -458,8 +521,12 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             poff4[u] = pc0 < m ? e * 4u : OOB;
         }
         uint2 pa[4], pt[4];               // alpha, theta of the 4 channels (bf16 pairs)
-        u32x4 pq[4], pk[4];               // q, k of the 4 channels (complex bf16)
-        u32 pbeta = 0;
+        // q, k of the 4 channels (complex bf16) and beta of one step; two of them, so that a
+        // step's q and k are requested a whole step before their operands are formed (global
+        // loads take several thousand cycles under this load); the copy waits for loads issued
+        // a step earlier
+        struct QK { u32x4 q[4], k[4]; u32 beta; };
+        QK cur, nxt;
 
         // alpha, theta of step st (consumed by the scan, a step before the rest)
         auto load_at = [&](int st) {
@@ -492,7 +559,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             }
         };
         // q, k, beta of step st (beta: lanes 0..15 hold the block's 16 tokens)
-        auto load_qk = [&](int st) {
+        auto load_qk = [&](int st, QK& b) {
             const int t0 = st * CP;
             const long e0 = base_tm + static_cast<long>(t0) * m;
             const int rows = T - t0;
@@ -501,8 +568,8 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             if (wide) {
 #pragma unroll
                 for (int u = 0; u < 4; ++u) {
-                    pq[u] = ld128(rq, poff4[u]);
-                    pk[u] = ld128(rk, poff4[u]);
+                    b.q[u] = ld128(rq, poff4[u]);
+                    b.k[u] = ld128(rk, poff4[u]);
                 }
             } else {
 #pragma unroll
@@ -511,12 +578,12 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     for (int k = 0; k < 4; ++k) {
                         const u32 e = static_cast<u32>((tl0 + u) * m + pc0 + k);
                         const bool ok = pc0 + k < m;
-                        pq[u][k] = ld32(rq, ok ? e * 4u : OOB);
-                        pk[u][k] = ld32(rk, ok ? e * 4u : OOB);
+                        b.q[u][k] = ld32(rq, ok ? e * 4u : OOB);
+                        b.k[u][k] = ld32(rk, ok ? e * 4u : OOB);
                     }
             }
             const rsrc_t rb = make_rsrc(args.beta + base_t + t0, rows * 2);
-            pbeta = ld16(rb, lane < 16 ? static_cast<u32>(pw * 16 + lane) * 2u : OOB);
+            b.beta = ld16(rb, lane < 16 ? static_cast<u32>(pw * 16 + lane) * 2u : OOB);
         };
 
         // Scans of one block per channel (three levels: the lane's 4 tokens, the wave's four
@@ -605,7 +672,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         float base[4] = {0.f, 0.f, 0.f, 0.f};   // phase (revolutions) before the step, per channel
 
         // operands of step st into set st & 1: conj(Q)G, conj(K)G, K Q and the Gram operand
-        auto produce = [&](int st) {
+        auto produce = [&](int st, const QK& b) {
             char* S = set_ptr(st & 1);
             Set& ss = sm.set[st & 1];
             float off[4];
@@ -626,7 +693,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     float s2 = 0.f;
 #pragma unroll
                     for (int k = 0; k < 4; ++k) {
-                        const float kr = bf_lo(pk[u][k]), ki = bf_hi(pk[u][k]);
+                        const float kr = bf_lo(b.k[u][k]), ki = bf_hi(b.k[u][k]);
                         s2 = __builtin_fmaf(kr, kr, __builtin_fmaf(ki, ki, s2));
                     }
                     s2 += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(s2), 0x124, 0xF, 0xF, false));
@@ -647,7 +714,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 for (int k = 0; k < 4; ++k) {
                     const float Ph = off[k] + ph[u][k];
                     const float sn = __builtin_amdgcn_sinf(Ph), cs = __builtin_amdgcn_cosf(Ph);
-                    const u32 qw = pq[u][k], kw = pk[u][k];
+                    const u32 qw = b.q[u][k], kw = b.k[u][k];
                     const float qr = bf_lo(qw), qi = bf_hi(qw), kr = bf_lo(kw), ki = bf_hi(kw);
                     // conj(q) e^{i phi}, conj(k) e^{i phi}; k e^{-i phi} is the latter's conjugate
                     const float qur = __builtin_fmaf(qr, cs, qi * sn), qui = __builtin_fmaf(qr, sn, -qi * cs);
@@ -679,7 +746,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 base[k] = __builtin_amdgcn_fractf(tot);
             }
             if (lane < 16) {
-                float bt = bf16_bits_to_f32(static_cast<uint16_t>(pbeta));
+                float bt = bf16_bits_to_f32(static_cast<uint16_t>(b.beta));
                 if constexpr (GATED) bt = st * CP + pw * 16 + lane < T ? sigmoid_f(bt) : 0.f;
                 ss.beta[pw * 16 + lane] = bt;
             }
@@ -687,77 +754,29 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             if (lane == 0) ss.bad[pw] = oor;
         };
 
-        // the block's Gram matrices L (strict lower) and A (with the diagonal) and the
-        // inverse N = (I + D_beta L)^{-1}, from the rows this wave has just written
-        auto diag = [&](int st) {
-            char* S = set_ptr(st & 1);
-            const Set& ss = sm.set[st & 1];
-            // the wave's own LDS writes are complete before it reads them back
-            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-            const char* KD = reinterpret_cast<const char*>(sm.kd);
-            CAcc zl, za;
-            czero(zl);
-            czero(za);
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb) {
-                const u32x4 ak = *reinterpret_cast<const u32x4*>(S + OFF_KB + rm_frag(pw * 16 + c, kb * 4 + g));
-                const u32x4 aq = *reinterpret_cast<const u32x4*>(S + OFF_QB + rm_frag(pw * 16 + c, kb * 4 + g));
-                const u32x4 w = *reinterpret_cast<const u32x4*>(KD + rm_frag(pw * 16 + c, kb * 4 + g));
-                const BPair bw = bwords(w);
-                cmma(zl, ak, bw);
-                cmma(za, aq, bw);
-            }
-            // A_p: lower triangle with the diagonal, zero above
-            char* aqb = S + OFF_AQ + pw * 1024;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const bool keep = c <= 4 * g + r;
-                *reinterpret_cast<u32*>(aqb + blk_off(4 * g + r, c)) = keep ? pack_bf16(za.re[r], za.im[r]) : 0u;
-            }
-            // X = -(D_beta L), zero on and above the diagonal, to the wave's scratch; each
-            // lane then reads back one row
-            const float4 bt = *reinterpret_cast<const float4*>(&ss.beta[pw * 16 + 4 * g]);
-            const float btr[4] = {bt.x, bt.y, bt.z, bt.w};
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const bool lo = c < 4 * g + r;
-                sm.xs[pw][4 * g + r][c] = make_float2(lo ? -btr[r] * zl.re[r] : 0.f,
-                                                      lo ? -btr[r] * zl.im[r] : 0.f);
-            }
-            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-            const int i = c, cgi = g;
-            float2 xrow[16];
-#pragma unroll
-            for (int s2 = 0; s2 < 16; s2 += 2) {
-                const float4 x2 = *reinterpret_cast<const float4*>(&sm.xs[pw][i][s2]);
-                xrow[s2] = make_float2(x2.x, x2.y);
-                xrow[s2 + 1] = make_float2(x2.z, x2.w);
-            }
-            float nr[4], ni[4];
-#pragma unroll
-            for (int k = 0; k < 4; ++k) { nr[k] = i == 4 * k + cgi ? 1.f : 0.f; ni[k] = 0.f; }
-            inv_steps(nr, ni, xrow, std::make_integer_sequence<int, 15>{});
-#pragma unroll
-            for (int k = 0; k < 4; ++k)
-                *reinterpret_cast<u32*>(S + OFF_ND + pw * 1024 + blk_off(i, 4 * k + cgi)) =
-                    pack_bf16(nr[k], ni[k]);
-        };
-
         if (nsteps > 0) {
             load_at(0);
-            load_qk(0);
+            load_qk(0, nxt);
             pretot(0);
+            if (nsteps > 1) load_at(1);
         }
         __syncthreads();          // block phase totals of step 0
         for (int st = -1; st < nsteps; ++st) {
-            // alpha and theta two steps ahead: the scan of step st + 1 has consumed them
-            if (st + 2 < nsteps) load_at(st + 2);
-            if (st + 1 < nsteps) {
-                produce(st + 1);
-                if (st + 2 < nsteps) load_qk(st + 2);
-                diag(st + 1);
+            // phase 1: the operands of step st + 1 (q, k requested a step ago), the next q, k.
+            // The gated variant's scans hold more registers: it keeps one buffer and requests
+            // the next q, k once the operands are formed.
+            if constexpr (GATED) {
+                if (st + 1 < nsteps) produce(st + 1, nxt);
+                if (st + 2 < nsteps) load_qk(st + 2, nxt);
+            } else {
+                if (st + 1 < nsteps) cur = nxt;
+                if (st + 2 < nsteps) load_qk(st + 2, nxt);
+                if (st + 1 < nsteps) produce(st + 1, cur);
             }
+            __syncthreads();
+            // phase 2: the scans of step st + 2, alpha and theta of the step after
             if (st + 2 < nsteps) pretot(st + 2);
+            if (st + 3 < nsteps) load_at(st + 3);
             __syncthreads();
         }
         // The compiler joins the two roles' control flow after the producer's exit, and the

@@ -291,6 +291,18 @@ def test_bf16_slices(slice):
     check(small(T=130, n=64, dtype="bf16"), 64, 2e-2, slice=slice, label=f"bf16 slice{slice}")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_slices_bitwise_equal(dtype):
+    """Every value column's arithmetic is the same whatever the column slice, so the slice
+    sfda_chunk_fwd picks by itself (32 columns when heads are few) changes no bit."""
+    x = small(T=150, B=1, H=2, n=64, dtype=dtype)
+    say("slices bitwise", dtype)
+    o0, S0 = run_chunk(x, 64)
+    for sl in (64, 32, 16):
+        o, S = run_chunk(x, 64, slice=sl)
+        assert np.array_equal(o, o0) and np.array_equal(S, S0), sl
+
+
 def test_bf16_in_f32_out():
     check(small(T=150, dtype="bf16"), 64, 2e-2, out_dtype="f32", label="bf16 in, f32 out")
 
