@@ -233,7 +233,7 @@ __device__ __forceinline__ void adjoint_chunk(ChunkSmem<C>& sm, const ChunkArgs&
 // backward, chunks in reverse order (below).
 template <int P, typename TIN, typename TOUT, int C, bool GATED, int MODE, typename SM = ChunkSmem<C>,
           int NW = 4>
-__device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsigned block)
+__device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsigned block, long heads = 0)
 {
     constexpr int NRB = C / 16;          // 16-token blocks per chunk
     constexpr int SEG = C / 4;           // tokens per thread in the cumulative sums
@@ -244,8 +244,9 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
     TOUT* __restrict__ go = static_cast<TOUT*>(args.o);
 
     const int T = args.T, m = args.m, n = args.n;
-    const long bh = block / args.n_slices;
-    const int sl = block - static_cast<int>(bh) * args.n_slices;
+    long bh;
+    int sl;
+    head_slice(block, args.n_slices, heads, bh, sl);
     const int n0 = sl * args.slice;                       // first value column of the slice
     const int ncb = (min(args.slice, n - n0) + 7) / 8;    // active column blocks
 
@@ -732,7 +733,7 @@ __global__ __launch_bounds__(scan_waves<C>() * 64, 1) void chunk_kernel(ChunkArg
 {
     using SM = std::conditional_t<MODE == 3, ChunkSmemDec<C>, ChunkSmem<C>>;
     __shared__ SM sm;
-    chunk_scan<P, TIN, TOUT, C, GATED, MODE, SM, scan_waves<C>()>(sm, args, blockIdx.x);
+    chunk_scan<P, TIN, TOUT, C, GATED, MODE, SM, scan_waves<C>()>(sm, args, blockIdx.x, gridDim.x / args.n_slices);
 }
 
 // The backward's two scans in one launch: the first nfwd workgroups run the recording

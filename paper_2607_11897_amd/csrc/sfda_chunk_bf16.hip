@@ -272,8 +272,9 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
     __shared__ Smem sm;
 
     const int T = args.T, m = args.m, n = args.n;
-    const long bh = blockIdx.x / args.n_slices;
-    const int sl = blockIdx.x - static_cast<int>(bh) * args.n_slices;
+    long bh;
+    int sl;
+    head_slice(blockIdx.x, args.n_slices, gridDim.x / args.n_slices, bh, sl);
     const int n0 = sl * args.slice;
     const int scols = min(args.slice, n - n0);          // value columns of this slice
     const int nsteps = (T + CP - 1) / CP;

@@ -148,4 +148,23 @@ __device__ __forceinline__ void mma<PREC_BF16>(f32x4& acc, const Frag8& a, const
 
 __device__ __forceinline__ f32x4 zero4() { f32x4 z = {0.f, 0.f, 0.f, 0.f}; return z; }
 
+// ----------------------------------------------------------------- workgroup placement
+
+// Workgroup w of a grid of `heads` x S (head, value-column slice) pairs.  The dispatcher
+// hands workgroups to the 8 XCDs round-robin by index and each XCD has its own L2, so the S
+// slices of a head -- which read the same q, k, alpha, theta and beta -- are given indices
+// 8 S j + 8 s + x (head 8 j + x, slice s): one XCD, one L2.  With a head count that is not a
+// multiple of 8 the plain order (head-major) is used.
+__device__ __forceinline__ void head_slice(unsigned w, int S, long heads, long& bh, int& sl) {
+    if (S > 1 && heads > 0 && (heads & 7) == 0) {
+        const unsigned x = w & 7u, q = w >> 3;
+        const unsigned j = q / static_cast<unsigned>(S);
+        sl = static_cast<int>(q - j * static_cast<unsigned>(S));
+        bh = 8L * j + x;
+    } else {
+        bh = w / S;
+        sl = static_cast<int>(w - bh * S);
+    }
+}
+
 }  // namespace sfda
