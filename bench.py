@@ -190,7 +190,7 @@ def bench_chunk(args, stream):
         roofline={"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                   "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                   "traffic": traffic,
-                  "kernel": "sfda::pipe::chunk_pipe_kernel<bf16 out, C=64>",
+                  "kernel": "sfda::pipe::chunk_pipe_kernel<bf16 out> (C=64, two workgroups per head)",
                   "bytes_per_launch": int(bytes_alg),
                   "bytes_per_token_head": chunk_bytes_per_token_head(m, n, T, 2, 2),
                   "mfma": {"peak_tflops": BF16_MFMA_PEAK_TFLOPS,
