@@ -45,9 +45,13 @@ extern "C" {
 
 #define SFDA_ABI_VERSION 2
 
-typedef enum { SFDA_F32 = 0, SFDA_BF16 = 1 } sfda_dtype_t;
+/* Element types and status codes are plain ints (the names below are their values), so
+ * any value a caller passes is well defined: an unknown dtype is SFDA_ERR_DTYPE, an unknown
+ * status has its own text. */
+enum { SFDA_F32 = 0, SFDA_BF16 = 1 };
+typedef int sfda_dtype_t;
 
-typedef enum {
+enum {
     SFDA_OK = 0,
     SFDA_ERR_NULL = 1,   /* a required pointer is NULL                                   */
     SFDA_ERR_SHAPE = 2,  /* a size is out of range (see each entry point)                 */
@@ -58,7 +62,8 @@ typedef enum {
     SFDA_ERR_HIP = 7,    /* the HIP runtime reported an error when launching              */
     SFDA_ERR_SCRATCH = 8 /* sfda_chunk_fwd_segmented_noalloc: the call needs more workspace
                             than SFDA_NOALLOC_SCRATCH_BYTES                                */
-} sfda_status_t;
+};
+typedef int sfda_status_t;
 
 /* A hipStream_t passed as an opaque pointer; NULL means the default (null) stream. */
 typedef void* sfda_stream_t;

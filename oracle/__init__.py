@@ -23,26 +23,38 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
+# another build of oracle.c to load instead (the sanitizer pass points here); loaded as is
+_LIB_OVERRIDE = os.environ.get("SFDA_ORACLE_LIB")
 _lib = None
 
 
-def build(verbose: bool = False) -> str:
-    """Compile oracle.c into liboracle.so (plain C, OpenMP, no fast-math)."""
-    cmd = ["gcc", "-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared", "-Wall",
-           "-o", _LIB + ".tmp", _SRC, "-lm"]
+def build(verbose: bool = False, sanitize: bool = False, out: str = _LIB) -> str:
+    """Compile oracle.c into liboracle.so (plain C, OpenMP, no fast-math).  sanitize builds
+    it with clang under AddressSanitizer and UndefinedBehaviorSanitizer instead (serial: the
+    OpenMP pragmas only split the loops over heads); out is the library path."""
+    if sanitize:
+        cmd = ["/opt/rocm/llvm/bin/clang", "-O1", "-g", "-std=c99", "-fPIC", "-shared", "-Wall",
+               "-Wno-unknown-pragmas", "-fsanitize=address,undefined", "-fno-omit-frame-pointer",
+               "-fno-sanitize-recover=undefined", "-o", out + ".tmp", _SRC, "-lm"]
+    else:
+        cmd = ["gcc", "-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared", "-Wall",
+               "-o", out + ".tmp", _SRC, "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)
-    os.replace(_LIB + ".tmp", _LIB)
-    return _LIB
+    os.replace(out + ".tmp", out)
+    return out
 
 
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-            build()
-        lib = ctypes.CDLL(_LIB)
+        if _LIB_OVERRIDE:
+            lib = ctypes.CDLL(_LIB_OVERRIDE)
+        else:
+            if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+                build()
+            lib = ctypes.CDLL(_LIB)
         d = ctypes.POINTER(ctypes.c_double)
         i = ctypes.c_int
         lib.oracle_recurrence.argtypes = [i, i, i, i, i, d, d, d, d, d, d, d, d, d, i]

@@ -14,16 +14,23 @@ SOURCES = ["sfda_api.hip", "sfda_chunk.hip", "sfda_chunk_grad.hip", "sfda_chunk_
 ARCH = "gfx950"
 
 
-def build(verbose: bool = True) -> str:
-    """Compile every HIP source for gfx950 into one shared library (always recompiles)."""
+# host code checked by AddressSanitizer and UndefinedBehaviorSanitizer (device code is
+# compiled as usual); the sanitizer runtime must be preloaded into the loading process
+SANITIZE_FLAGS = ["-Xarch_host", "-fsanitize=address,undefined", "-Xarch_host", "-fno-omit-frame-pointer",
+                  "-Xarch_host", "-fno-sanitize-recover=undefined"]
+
+
+def build(verbose: bool = True, sanitize: bool = False, out: str = LIB) -> str:
+    """Compile every HIP source for gfx950 into one shared library (always recompiles).
+    sanitize adds ASan/UBSan instrumentation of the host code; out is the library path."""
     cmd = [
         "hipcc", f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
         "-Wall", "-Wno-unused-variable",
         # packed fp32 instructions are kept out of the generated code
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
         "-I", os.path.join(ROOT, "include"),
-        "-o", LIB + ".tmp",
-    ] + [os.path.join(CSRC, s) for s in SOURCES]
+        "-o", out + ".tmp",
+    ] + (SANITIZE_FLAGS if sanitize else []) + [os.path.join(CSRC, s) for s in SOURCES]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -33,8 +40,8 @@ def build(verbose: bool = True) -> str:
         raise RuntimeError("hipcc failed:\n" + msgs)
     if verbose and msgs.strip():
         print(msgs)
-    os.replace(LIB + ".tmp", LIB)
-    return LIB
+    os.replace(out + ".tmp", out)
+    return out
 
 
 if __name__ == "__main__":

@@ -232,7 +232,10 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
         const float A = la[u] + oa;
         const float Ph = ph[u] + op;
         const float e = __expf(A);
-        const float ei = __expf(-A);
+        // 1 / |g_t| stays finite while the chunk's decay so far is at least 2^-126; past
+        // that the operand is NaN, so the chunk's outputs from here on and every later
+        // state are NaN rather than silently wrong
+        const float ei = A >= -87.3365447f ? __expf(-A) : __builtin_nanf("");
         float sn, cs;
         __sincosf(Ph, &sn, &cs);
         const float gr = e * cs, gi = e * sn;        // g_t

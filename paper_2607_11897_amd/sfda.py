@@ -12,7 +12,8 @@ import os
 from typing import Optional, Tuple
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libsfda.so")
+# the in-tree build; SFDA_LIBRARY names another build to load (the sanitizer pass uses it)
+LIB_PATH = os.environ.get("SFDA_LIBRARY") or os.path.join(HERE, "libsfda.so")
 
 SFDA_F32, SFDA_BF16 = 0, 1
 STATUS = {0: "SFDA_OK", 1: "SFDA_ERR_NULL", 2: "SFDA_ERR_SHAPE", 3: "SFDA_ERR_CHUNK",

@@ -105,18 +105,24 @@ def test_unit_and_tiny_decay_across_channels(dtype, s0):
           label=f"mixed {dtype} S0 {s0}")
 
 
-def test_bf16_decay_outside_range_returns_nan():
+@pytest.mark.parametrize("dtype,ok_until,nan_from", [("bf16", 128, 128), ("f32", 144, 156)])
+def test_decay_outside_range_returns_nan(dtype, ok_until, nan_from):
     """One channel decaying by 1e-48 over a whole 16-token block (alpha = 0.001, tokens
-    144..159, the second block of the third 64-token step) is outside the decay range: the
-    outputs of the steps before it are unaffected and match the oracle, from that step on
-    the outputs and S_T are NaN."""
-    x = small(T=200, dtype="bf16")
-    x.alpha[..., 144:160, 7] = I.round_to_storage(np.full(16, 0.001), "bf16")
-    say("bf16 out of range")
+    144..159) is outside the decay range.  bf16 evaluates 64-token steps of 16-token blocks:
+    the steps before the one holding that block (tokens < 128) are unaffected and match the
+    oracle, from that step on the outputs and S_T are NaN.  float32 evaluates 16-token
+    chunks and poisons the operand of a token once the chunk's decay so far drops below
+    2^-126 (0.001^13 = 1e-39, token 156): the chunks before (tokens < 144) match the oracle,
+    every output from that token on and S_T are NaN (the chunk's triangular solve may carry
+    the NaN to its earlier rows too)."""
+    x = small(T=200, dtype=dtype)
+    x.alpha[..., 144:160, 7] = I.round_to_storage(np.full(16, 0.001), dtype)
+    say(dtype, "out of range")
     o, S = run_chunk(x, 64)
     o_ref, _ = run_oracle(x)
-    assert rel_err(o[:, :, :128], o_ref[:, :, :128]) <= 2e-2
-    assert np.all(np.isnan(o[:, :, 128:])) and np.all(np.isnan(S))
+    tol = 2e-2 if dtype == "bf16" else 1e-4
+    assert rel_err(o[:, :, :ok_until], o_ref[:, :, :ok_until]) <= tol
+    assert np.all(np.isnan(o[:, :, nan_from:])) and np.all(np.isnan(S))
 
 
 def test_bf16_every_chunk_length_bitwise_equal():
