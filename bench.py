@@ -467,9 +467,9 @@ def backward(args):
     from paper_2607_11897_amd import inputs as I
     from paper_2607_11897_amd import sfda
     import numpy as np
-    # the backward's chunk length is free (the gradients do not depend on it, to rounding);
-    # C = 32 is its fastest on MI355X (two waves per SIMD in both scans)
-    C_BWD = 32
+    # the backward runs 16-token chunks whatever C it is given (the gradients do not depend
+    # on the chunk length, to rounding; 16 keeps 1 / g in range for strong decay)
+    C_BWD = 16
     res = {"mode": "bwd", "kernel_hash_bwd": bwd_hash(), "C_bwd": C_BWD, "runs": []}
     for name in ("fwd_bf16_b8h16_t4k", "fwd_f32_b4h8_t2k"):
         w = I.WORKLOADS[name]

@@ -494,17 +494,18 @@ __global__ __launch_bounds__(GW * 64, C <= 16 ? 4 : 2) void grad_kernel(GradArgs
         // G_Kg's value part is -G_E S^* = -D_beta (G_F S^*)
 #pragma unroll
         for (int r = 0; r < 4; ++r) gkg[it][r] *= -sm.beta[rb * 16 + 4 * g + r];
-        // + G_L'^T conj(conj(K)G) + G_A^T conj(conj(Q)G)
+        // + G_L'^T conj(conj(K)G) + G_A^T conj(conj(Q)G); G_A's diagonal is left out of this
+        // product and of G_Qg's (added in the elementwise stage, below)
 #pragma unroll
         for (int kb = rb; kb < NRB; ++kb) {
             RC::mma(gki[it], cc_frag(true, row, kb, 2), lds_right(sm.kg, kb, icol));    // G_L'[jt][row], jt > row
-            RC::mma(gki[it], cc_frag(false, row, kb, 3), lds_right(sm.qg, kb, icol));   // G_A[jt][row], jt >= row
+            RC::mma(gki[it], cc_frag(false, row, kb, 2), lds_right(sm.qg, kb, icol));   // G_A[jt][row], jt > row
         }
         // G_Qg += G_A conj(K/G),  G_Kg += G_L' conj(K/G)
 #pragma unroll
         for (int kb = 0; kb <= rb; ++kb) {
             const Op b = lds_right(sm.ki, kb, icol);
-            RC::mma(gqg[it], cc_frag(true, row, kb, 1), b);                             // G_A[row][jt], jt <= row
+            RC::mma(gqg[it], cc_frag(true, row, kb, 0), b);                             // G_A[row][jt], jt < row
             RC::mma(gkg[it], cc_frag(false, row, kb, 0), b);                            // G_L'[row][jt], jt < row
         }
     }
@@ -568,8 +569,9 @@ __global__ __launch_bounds__(GW * 64, C <= 16 ? 4 : 2) void grad_kernel(GradArgs
         }
         // g of this thread's tokens: running sums of log alpha and theta over its segment,
         // offset by the segments before it (padding is the identity token: alpha read as 0
-        // there counts as 1)
-        float2 gkeep[SEG];
+        // there counts as 1); 1 / g from the negated sums (finite while the chunk's decay so
+        // far is at least 2^-126, NaN past that, as in the load stage)
+        float2 gkeep[SEG], gikeep[SEG];
         {
             float sa = 0.f, sp2 = 0.f;
 #pragma unroll
@@ -592,10 +594,13 @@ __global__ __launch_bounds__(GW * 64, C <= 16 ? 4 : 2) void grad_kernel(GradArgs
             }
 #pragma unroll
             for (int u = 0; u < SEG; ++u) {
-                const float e = __expf(la[u] + oa);
+                const float A = la[u] + oa;
+                const float e = __expf(A);
+                const float ei = A >= -87.3365447f ? __expf(-A) : __builtin_nanf("");
                 float sn, cs;
                 __sincosf(ph[u] + op2, &sn, &cs);
                 gkeep[u] = make_float2(e * cs, e * sn);
+                gikeep[u] = make_float2(ei * cs, -ei * sn);
             }
             __syncthreads();                           // before sega / segp are reused below
         }
@@ -609,32 +614,37 @@ __global__ __launch_bounds__(GW * 64, C <= 16 ? 4 : 2) void grad_kernel(GradArgs
             const bool ok = t < T && i < m;
             const long e = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
             const float2 gqv = sm.kg[tl * LDX + i], gkv = sm.ki[tl * LDX + i], gkiv = sm.qg[tl * LDX + i];
-            const float2 gg = gkeep[u];
-            const float inv2 = 1.f / (gg.x * gg.x + gg.y * gg.y);
-            const float2 gi = make_float2(gg.x * inv2, -gg.y * inv2);            // 1 / g
+            const float2 gg = gkeep[u], gi = gikeep[u];                          // g, 1 / g
+            const float2 q1 = qq[u], k1 = kk[u];
+            const float2 kg2 = make_float2(k1.x * gi.x - k1.y * gi.y, k1.x * gi.y + k1.y * gi.x);     // k / g
+            // G_A's diagonal a = G_A[t][t]: its terms in G_Qg and G_Ki, a conj(k / g) and
+            // a q conj(g), go into dq and dk here in float32.  In dL/dz they cancel exactly
+            // (A[t][t] = q_t . conj(k_t) does not depend on the decay), so dL/dz leaves both
+            // out rather than subtracting two separately rounded products.
+            const float2 ga = sm.g2[tl * LDG + tl];
+            const float2 qcg = make_float2(q1.x * gg.x + q1.y * gg.y, q1.y * gg.x - q1.x * gg.y);    // q conj(g)
+            const float2 gqf = make_float2(gqv.x + ga.x * kg2.x + ga.y * kg2.y, gqv.y + ga.y * kg2.x - ga.x * kg2.y);
+            const float2 gkif = make_float2(gkiv.x + ga.x * qcg.x - ga.y * qcg.y, gkiv.y + ga.x * qcg.y + ga.y * qcg.x);
             // dq = g conj(G_Qg); dk = g conj(G_Kg) + conj(1/g) G_Ki
-            const float2 vq = make_float2(gg.x * gqv.x + gg.y * gqv.y, gg.y * gqv.x - gg.x * gqv.y);
-            const float2 vk = make_float2(gg.x * gkv.x + gg.y * gkv.y + gi.x * gkiv.x + gi.y * gkiv.y,
-                                          gg.y * gkv.x - gg.x * gkv.y + gi.x * gkiv.y - gi.y * gkiv.x);
+            const float2 vq = make_float2(gg.x * gqf.x + gg.y * gqf.y, gg.y * gqf.x - gg.x * gqf.y);
+            const float2 vk = make_float2(gg.x * gkv.x + gg.y * gkv.y + gi.x * gkif.x + gi.y * gkif.y,
+                                          gg.y * gkv.x - gg.x * gkv.y + gi.x * gkif.y - gi.y * gkif.x);
             if (ok) {          // (a worker thread)
                 Elem<TIN>::store2(dq, e, vq.x, vq.y);
                 Elem<TIN>::store2(dk, e, vk.x, vk.y);
             }
-            // dL/dg = q G_Qg + k G_Kg - conj(k / g^2) G_Ki
-            const float2 q1 = qq[u], k1 = kk[u];
-            const float2 kg2 = make_float2(k1.x * gi.x - k1.y * gi.y, k1.x * gi.y + k1.y * gi.x);     // k / g
-            const float2 kg3 = make_float2(kg2.x * gi.x - kg2.y * gi.y, kg2.x * gi.y + kg2.y * gi.x); // k / g^2
-            float2 dg = make_float2(q1.x * gqv.x - q1.y * gqv.y + k1.x * gkv.x - k1.y * gkv.y
-                                        - (kg3.x * gkiv.x + kg3.y * gkiv.y),
-                                    q1.x * gqv.y + q1.y * gqv.x + k1.x * gkv.y + k1.y * gkv.x
-                                        - (kg3.x * gkiv.y - kg3.y * gkiv.x));
+            // dL/dg = q G_Qg + k G_Kg - conj(k / g^2) G_Ki (+ dL/dg_C at the chunk's last
+            // token), and dL/dz = conj(g) dL/dg: the last term becomes conj(k / g) G_Ki, so
+            // no operand goes below 1 / g
+            float2 dp = make_float2(q1.x * gqv.x - q1.y * gqv.y + k1.x * gkv.x - k1.y * gkv.y,
+                                    q1.x * gqv.y + q1.y * gqv.x + k1.x * gkv.y + k1.y * gkv.x);
             if (tl == C - 1 && i < m) {
-                dg.x += gs.ggc[2 * i];
-                dg.y += gs.ggc[2 * i + 1];
+                dp.x += gs.ggc[2 * i];
+                dp.y += gs.ggc[2 * i + 1];
             }
-            // dL/dz = conj(g) dL/dg, suffix sums over the chunk
-            sl += gg.x * dg.x + gg.y * dg.y;
-            sp += gg.x * dg.y - gg.y * dg.x;
+            // suffix sums of dL/dz over the chunk
+            sl += gg.x * dp.x + gg.y * dp.y - (kg2.x * gkiv.x + kg2.y * gkiv.y);
+            sp += gg.x * dp.y - gg.y * dp.x - (kg2.x * gkiv.y - kg2.y * gkiv.x);
             gl[u] = sl;
             gp[u] = sp;
         }

@@ -174,12 +174,12 @@ def bwd(lib, ptrs=None, B=1, H=1, T=40, m=8, n=8, C=16, din=0, dout=0, ws_bytes=
 
 
 def test_bwd_workspace_bytes(lib):
-    # per chunk: two m x n and two C x n complex float32 blocks; C = 64 runs at chunk length 32
-    assert lib.sfda_chunk_bwd_workspace_bytes(8, 16, 4096, 64, 64, 32) == 8 * 16 * 128 * (2 * 64 * 64 + 2 * 32 * 64) * 8
-    assert lib.sfda_chunk_bwd_workspace_bytes(8, 16, 4096, 64, 64, 64) == \
-        lib.sfda_chunk_bwd_workspace_bytes(8, 16, 4096, 64, 64, 32)
-    assert lib.sfda_chunk_bwd_workspace_bytes(1, 1, 65, 8, 8, 64) == 3 * (2 * 8 * 8 + 2 * 32 * 8) * 8
-    assert lib.sfda_chunk_bwd_workspace_bytes(1, 1, 65, 8, 8, 128) == 3 * (2 * 8 * 8 + 2 * 32 * 8) * 8
+    # per chunk: two m x n and two C x n complex float32 blocks; every C runs 16-token chunks
+    assert lib.sfda_chunk_bwd_workspace_bytes(8, 16, 4096, 64, 64, 16) == 8 * 16 * 256 * (2 * 64 * 64 + 2 * 16 * 64) * 8
+    for C in (32, 64, 128):
+        assert lib.sfda_chunk_bwd_workspace_bytes(8, 16, 4096, 64, 64, C) == \
+            lib.sfda_chunk_bwd_workspace_bytes(8, 16, 4096, 64, 64, 16)
+    assert lib.sfda_chunk_bwd_workspace_bytes(1, 1, 65, 8, 8, 64) == 5 * (2 * 8 * 8 + 2 * 16 * 8) * 8
     assert lib.sfda_chunk_bwd_workspace_bytes(1, 1, 65, 8, 8, 16) == 5 * (2 * 8 * 8 + 2 * 16 * 8) * 8
     assert lib.sfda_chunk_bwd_workspace_bytes(1, 1, 0, 8, 8, 16) == 0
     for bad in [(0, 1, 4, 8, 8, 16), (1, 1, 4, 65, 8, 16), (1, 1, 4, 8, 0, 16), (1, 1, 4, 8, 8, 48)]:

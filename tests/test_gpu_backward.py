@@ -93,6 +93,49 @@ def test_bwd_matches_oracle(dtype, B, H, T, m, n, C):
     check(got, ref, 1e-4 if dtype == "f32" else 2e-2, f"{dtype} {(B, H, T, m, n)} C{C}")
 
 
+STRONG = I.Laws(alpha=("uniform", 0.02, 0.1), theta=("uniform", -3.14159, 3.14159),
+                beta=("uniform", 0.0, 1.0), s0_scale=0.1)
+MIXED = I.Laws(alpha=("mixed", 0.005, 0.01), theta=("uniform", -3.14159, 3.14159),
+               beta=("uniform", 0.0, 1.0), s0_scale=0.1)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("law", ["strong", "mixed"])
+def test_bwd_strong_decay(dtype, law):
+    """alpha ~ U(0.02, 0.1) (a 64-token chunk decays to 1e-109), and alpha exactly 1 on the
+    even channels with U(0.005, 0.01) on the odd ones: every gradient within the bars."""
+    laws = STRONG if law == "strong" else MIXED
+    w = I.Workload("bwd", 1, 2, 3 * 64 + 37, 64, 64, 64, dtype, laws, 31, 1e-4)
+    x = I.make_chunk_inputs(w)
+    dO, dS = I.make_cotangents(1, 2, w.T, 64, 64, dtype, seed=32)
+    say(dtype, law, "decay")
+    got = run_bwd(x, dO, dS, 64, dtype)
+    ref = oracle_bwd(x, dO, dS)
+    check(got, ref, 1e-4 if dtype == "f32" else 2e-2, f"{dtype} {law} decay")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_bwd_decay_outside_range_returns_nan(dtype):
+    """alpha = 0.001 on one channel for the 16 tokens 144..159 (one chunk of the backward,
+    decaying by 1e-48) is outside the range: dS0 and dv of that chunk and of every earlier
+    one are NaN, dv of the later chunks (which the adjoint reaches first) matches the
+    oracle."""
+    x = make(1, 2, 200, 64, 64, dtype, seed=33)
+    x.alpha[..., 144:160, 7] = I.round_to_storage(np.full(16, 0.001), dtype)
+    dO, dS = I.make_cotangents(1, 2, 200, 64, 64, dtype, seed=34)
+    say(dtype, "backward out of range")
+    import torch
+    from paper_2607_11897_amd import sfda
+    d = upload(x)
+    g = sfda.chunk_bwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], d["S0"],
+                       to_device(I.to_storage(dO, dtype), dtype), to_device(I.to_storage(dS, "f32"), "f32"), C=64)
+    torch.cuda.synchronize()
+    dv, dS0 = as_np(g["dv"], True), as_np(g["dS0"], True)
+    ref = oracle_bwd(x, dO, dS)
+    assert np.all(np.isnan(dS0)) and np.all(np.isnan(dv[:, :, :160]))
+    assert rel_err(dv[:, :, 160:], ref["dv"][:, :, 160:]) <= (1e-4 if dtype == "f32" else 2e-2)
+
+
 def test_bwd_zero_state_and_no_state_gradient():
     x = make(1, 2, 96, 64, 64, "f32", seed=9, zero_state=True)
     dO, _ = I.make_cotangents(1, 2, 96, 64, 64, "f32", seed=10, dS_scale=None)
