@@ -82,13 +82,23 @@ typedef void* sfda_stream_t;
  *          S_T == S0 (same pointer) is allowed and updates the state in place; any other
  *          overlap between S_T and another buffer is SFDA_ERR_ALIAS.
  *   B, H >= 0 (B*H == 0 is a no-op); T >= 0 (T == 0 writes S_T = S0, or zeros);
- *   1 <= m <= 64; n >= 1 with m * n < 2^28 and C * n < 2^28 (one head's state and one
- *   chunk's rows of v and o are addressed with 32-bit byte offsets; SFDA_ERR_SHAPE
- *   otherwise); C in {16, 32, 64} (SFDA_ERR_CHUNK otherwise).  The
- *   last chunk may be ragged (T mod C != 0).
- *   Numerical range: the chunk factorisation divides by the in-chunk cumulative decay, so
- *   prod over any C consecutive tokens of alpha_t[i] must stay above about 1e-30 for every
- *   channel i (e.g. alpha >= 0.35 for C = 64, alpha >= 0.014 for C = 16); alpha must be > 0.
+ *   1 <= m <= 64; n >= 1 with m * n < 2^28 and n < 2^23 (one head's state and 32 tokens'
+ *   rows of v and o are addressed with 32-bit byte offsets; SFDA_ERR_SHAPE otherwise);
+ *   C in {16, 32, 64, 128} (SFDA_ERR_CHUNK otherwise).  The last chunk may be ragged
+ *   (T mod C != 0).
+ *   Chunk length: C fixes the paper's chunking; the result does not depend on it (Thm 6.1,
+ *   up to rounding), and the kernels choose their own blocking.  bf16 inputs run 64-token
+ *   steps of four 16-token blocks for every C (bitwise the same result for every C);
+ *   float32 inputs run 16-token chunks for every C.
+ *   Numerical range (App. C.4, local renormalisation): the decay is referenced to the start
+ *   of each aligned 16-token block (tokens 16 j .. 16 j + 15), so the kernels divide by at
+ *   most the decay over part of one block.  The result is exact to rounding for every
+ *   alpha in (0, 1] whose product over each aligned 16-token block, per channel, is at
+ *   least 2^-126 (e.g. any alpha >= 0.0043; alpha may be exactly 1 or vary per channel and
+ *   token; the decay over longer stretches is unbounded).  Past that the outputs are NaN
+ *   rather than wrong: with bf16 inputs from the 64-token step holding such a block on,
+ *   with float32 inputs from the first token whose block decay so far is below 2^-126 (its
+ *   16-token chunk's earlier rows may be NaN too); S_T is NaN in both cases.
  *   Accumulation and state are float32 for both dtypes; with in_dtype == SFDA_BF16 the
  *   matrix products take bfloat16 operands, and each head's share of q, k, v and o must
  *   stay below 2 GiB (T * max(m, n) * 2 * sizeof(out element) < 2^31; SFDA_ERR_SHAPE
@@ -129,9 +139,9 @@ sfda_status_t sfda_chunk_fwd_sliced(const void* q, const void* k, const void* v,
  *   k_t     = k_raw_t / (||k_raw_t||_2 + eps)   (norm over the m complex channels)
  * q, v, S0, o, S_T, sizes, dtypes, layouts, errors and results as sfda_chunk_fwd (a, b, c,
  * k_raw take the places of alpha, theta, beta, k).  Requires 0 < alpha_min <= alpha_max
- * <= 1 and finite theta_max, eps >= 0 (SFDA_ERR_SHAPE otherwise); the decay-range
- * precondition of sfda_chunk_fwd applies to alpha (alpha_min^C above about 1e-30 always
- * satisfies it).  With eps == 0 an all-zero raw key gives k = 0.
+ * <= 1, alpha_min >= 0.0042719 (so that alpha_min^16 >= 2^-126: every input is inside
+ * sfda_chunk_fwd's numerical range) and finite theta_max, eps >= 0 (SFDA_ERR_SHAPE
+ * otherwise).  With eps == 0 an all-zero raw key gives k = 0.
  */
 sfda_status_t sfda_chunk_fwd_gated(const void* q, const void* k_raw, const void* v,
                                    const void* a, const void* b, const void* c,
@@ -151,8 +161,8 @@ sfda_status_t sfda_chunk_fwd_gated(const void* q, const void* k_raw, const void*
  * r-state products).  r = k with eta = beta gives sfda_chunk_fwd's result.
  *   r   : [B,H,T,m] complex write directions (device, in_dtype).
  *   eta : [B,H,T] erase strengths; beta : [B,H,T] write strengths (device, in_dtype).
- *   Other arguments and errors as sfda_chunk_fwd, except C in {16, 32} (SFDA_ERR_CHUNK for
- *   64: the chunk's operands with R / G and the extra Gram block exceed one CU's LDS).
+ *   Other arguments, errors and the numerical range as sfda_chunk_fwd's float32 path:
+ *   every C runs 16-token chunks (the result does not depend on C).
  */
 sfda_status_t sfda_chunk_fwd_decoupled(const void* q, const void* k, const void* r, const void* v,
                                        const void* alpha, const void* theta, const void* eta,
@@ -238,8 +248,9 @@ sfda_status_t sfda_chunk_fwd_segmented(const void* q, const void* k, const void*
  *          leaving it (m x n) and two C x n blocks, complex float32.
  *   Sizes, C and dtypes as sfda_chunk_fwd; T == 0 writes dS0 = dS_T (or zeros).  The
  *   chunk length only fixes how the work is blocked (every C gives the same gradients up
- *   to rounding): C = 64 runs at chunk length 32, the largest whose gradient pass keeps a
- *   chunk's operands and a staged block of value columns in one CU's LDS, and the
+ *   to rounding): every C runs 16-token chunks, so that the numerical range is
+ *   sfda_chunk_fwd's (each aligned 16-token block decaying by at least 2^-126 per channel;
+ *   past it the gradients of that chunk and of the earlier ones are NaN), and the
  *   workspace function sizes for that.
  *   alpha must be nonzero wherever T > 0 (dalpha divides by it).
  */

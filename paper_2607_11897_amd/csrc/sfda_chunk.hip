@@ -790,10 +790,9 @@ static hipError_t launch_dec_t(const ChunkLaunch& L, hipStream_t st)
 {
     const ChunkArgs a = make_args(L);
     const dim3 grid(static_cast<unsigned>(static_cast<long>(L.B) * L.H * a.n_slices));
-    // C = 64 and 128 run at chunk length 32 (a 64-token chunk's operands with R / G and the
-    // extra Gram block need more LDS than a CU has; the result does not depend on C)
-    if (L.C == 16) hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 16, false, 3>), grid, dim3(scan_waves<16>() * 64), 0, st, a);
-    else hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 32, false, 3>), grid, dim3(scan_waves<32>() * 64), 0, st, a);
+    // every C runs 16-token chunks: the decay range of one chunk is then the plain
+    // forward's, and on MI355X it is also faster than 32 (the result does not depend on C)
+    hipLaunchKernelGGL((chunk_kernel<P, TIN, TOUT, 16, false, 3>), grid, dim3(scan_waves<16>() * 64), 0, st, a);
     return hipGetLastError();
 }
 
