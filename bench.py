@@ -25,8 +25,8 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--only chunk|decode]
        gated: the benchmarked shape through sfda_chunk_fwd_gated; bwd: sfda_chunk_bwd on the
        benchmarked shape and on the float32 workload B=4, H=8, T=2048; dec: the write-decoupled
        variant on the benchmarked batch, heads and length (C=64, run as 16-token chunks); f32: the float32
-       workload B=4, H=8, T=2048 against the fp32 matrix-core peak, one workgroup per head at
-       C = 16, 32, 64, value-column slices and segment-parallel)
+       workload B=4, H=8, T=2048 against the fp32 matrix-core peak: the plain launch,
+       value-column slices and segment-parallel)
 """
 from __future__ import annotations
 
@@ -50,6 +50,9 @@ KERNEL_SOURCES = ["paper_2607_11897_amd/csrc/sfda_chunk_bf16.hip", "paper_2607_1
                   "paper_2607_11897_amd/csrc/sfda_device.h"]
 FP32_MFMA_PEAK_TFLOPS = 157.3
 SETTLE_S = 0.3
+
+
+KERNEL_BLOCK = 16       # tokens per block of the bf16 chunk kernel's factorisation
 
 
 def kernel_hash() -> str:
@@ -178,8 +181,10 @@ def bench_chunk(args, stream):
     ms = stats["mean"]
     units = B * H * T
     bytes_alg = chunk_bytes_per_token_head(m, n, T, 2, 2) * units
-    useful, tile = chunk_flops_per_chunk_head(w.C, m, n)
-    nchunk = B * H * (T // w.C)
+    # the kernel evaluates 16-token blocks whatever C is (the result does not depend on C):
+    # its flops are those of 16-token chunks
+    useful, tile = chunk_flops_per_chunk_head(KERNEL_BLOCK, m, n)
+    nchunk = B * H * (T // KERNEL_BLOCK)
     sec = ms / 1e3
     achieved = bytes_alg / sec / 1e9
     traffic = load_traffic("chunk_fwd", w.name)
@@ -371,12 +376,15 @@ def fp32_forward(args):
     o = torch.empty((B, H, T, n, 2), dtype=torch.float32, device="cuda")
     S_T = torch.empty((B, H, m, n, 2), dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
-    useful, tile = chunk_flops_per_chunk_head(w.C, m, n)
-    nchunk = B * H * (T // w.C)
+    # the kernel evaluates 16-token blocks whatever C is (the result does not depend on C):
+    # its flops are those of 16-token chunks
+    useful, tile = chunk_flops_per_chunk_head(KERNEL_BLOCK, m, n)
+    nchunk = B * H * (T // KERNEL_BLOCK)
     bytes_alg = chunk_bytes_per_token_head(m, n, T, 4, 4) * B * H * T
     runs = []
-    for C, G, sl in ((64, None, None), (32, None, None), (16, None, None), (64, None, 16),
-                     (16, None, 16), (64, 4, None), (64, 8, None), (32, 8, None), (16, 8, None)):
+    # (every C runs 16-token chunks: slices and segments are the knobs that change the launch)
+    for C, G, sl in ((64, None, None), (64, None, 32), (64, None, 16), (64, None, 8),
+                     (64, 4, None), (64, 8, None), (64, 16, None)):
         ws = None if G is None else torch.empty(sfda.segmented_workspace_bytes(B, H, m, n, G),
                                                 dtype=torch.uint8, device="cuda")
 

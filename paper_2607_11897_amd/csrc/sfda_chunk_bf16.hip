@@ -26,17 +26,21 @@
 // magnitudes need block-local references (the paper's remark on log-decays and local
 // renormalisation inside chunks, App. C.4).
 //
-// Pipeline (512 threads = 8 waves, two per SIMD; one barrier per step):
+// Pipeline (512 threads = 8 waves, two per SIMD; two barriers per step):
 //   waves 0-3 (consumers) own 16 value columns each and hold their columns of the rotated
 //     state in MFMA accumulators for the whole scan; they walk the four blocks of step s:
 //       P = conj(K)G S,  O = conj(Q)G S,  Delta = N D_beta (conj(V) - P),  O += A Delta,
 //       S <- |D| S + (K Q)^T Delta      (|D| the block's decay magnitude per channel);
-//   waves 4-7 (producers) prepare step s + 1, one block each: the block's prefix and suffix
-//     decay products and phases (scans over the lane's four tokens and the wave's four token
-//     segments; phase offsets of the earlier blocks from LDS), the operands conj(Q)G,
-//     conj(K)G, K Q (bf16, to LDS), then the block's Gram matrices L, A on the matrix cores
-//     from its own rows (no barrier: one wave wrote them) and the inverse
-//     N = (I + D_beta L)^{-1} in fp32; then the scans of step s + 2.
+//     after the middle barrier of step s each also forms block `wave` of step s + 1's
+//     state-independent factors: the Gram matrices L and A on the matrix cores and the
+//     inverse N = (I + D_beta L)^{-1} in fp32, beside its last block of step s;
+//   waves 4-7 (producers) own one block of 16 tokens each.  Before the middle barrier they
+//     form step s + 1's operands conj(Q)G, conj(K)G, k / P and K Q (bf16, to LDS) from
+//     q, k requested a step earlier (a second register buffer; the gated variant keeps
+//     one) and request step s + 2's q, k; after it they run step s + 2's prefix and suffix
+//     decay products and phase sums (scans over a lane's four tokens and a wave's four
+//     token segments; the phase offsets of earlier blocks through LDS) and request step
+//     s + 3's alpha, theta.
 //   Operands live in two LDS sets (steps s and s + 1).
 //
 // Complex products.  A complex 16 x 16 result block is held as two MFMA accumulator tiles,
@@ -454,7 +458,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
 
         // The role test is wave-uniform and encloses each role's whole life (prologue, step
         // loop, epilogue), so each role keeps only its own registers live.  Both loops pass
-        // the same sequence of workgroup barriers: one per step plus the lead-in.
+        // the same sequence of workgroup barriers: two per step plus the lead-in.
         if (active) {
             const rsrc_t rs = make_rsrc(args.S0 ? args.S0 + 2 * base_mn : args.S0,
                                         args.S0 ? m * n * 8 : 0);
