@@ -199,7 +199,9 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
             th = ok ? args.tmax * tanhf(th) : 0.f;
         }
         sa += __logf(a);
-        sp += th;
+        // phase in revolutions, reduced to [0, 1) at every token, so that the sine and
+        // cosine below see a small argument whatever theta is
+        sp = __builtin_amdgcn_fractf(__builtin_fmaf(th, 0.15915494309189535f, sp));
         la[u] = sa;
         ph[u] = sp;
     }
@@ -236,8 +238,7 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
         // that the operand is NaN, so the chunk's outputs from here on and every later
         // state are NaN rather than silently wrong
         const float ei = A >= -87.3365447f ? __expf(-A) : __builtin_nanf("");
-        float sn, cs;
-        __sincosf(Ph, &sn, &cs);
+        const float sn = __builtin_amdgcn_sinf(Ph), cs = __builtin_amdgcn_cosf(Ph);   // Ph in revolutions
         const float gr = e * cs, gi = e * sn;        // g_t
         const float hr = ei * cs, hi = -ei * sn;     // 1 / g_t
         if constexpr (KEEP) gkeep[u] = make_float2(gr, gi);

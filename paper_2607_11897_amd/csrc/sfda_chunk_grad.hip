@@ -578,7 +578,7 @@ __global__ __launch_bounds__(GW * 64, C <= 16 ? 4 : 2) void grad_kernel(GradArgs
             for (int u = 0; u < SEG; ++u) {
                 const bool ok = t0 + seg * SEG + u < T && i < m;
                 sa += __logf(av[u] + (ok ? 0.f : 1.f));
-                sp2 += ph[u];
+                sp2 = __builtin_amdgcn_fractf(__builtin_fmaf(ph[u], 0.15915494309189535f, sp2));   // revolutions
                 la[u] = sa;
                 ph[u] = sp2;
             }
@@ -597,8 +597,7 @@ __global__ __launch_bounds__(GW * 64, C <= 16 ? 4 : 2) void grad_kernel(GradArgs
                 const float A = la[u] + oa;
                 const float e = __expf(A);
                 const float ei = A >= -87.3365447f ? __expf(-A) : __builtin_nanf("");
-                float sn, cs;
-                __sincosf(ph[u] + op2, &sn, &cs);
+                const float sn = __builtin_amdgcn_sinf(ph[u] + op2), cs = __builtin_amdgcn_cosf(ph[u] + op2);
                 gkeep[u] = make_float2(e * cs, e * sn);
                 gikeep[u] = make_float2(ei * cs, -ei * sn);
             }

@@ -115,6 +115,21 @@ def test_bwd_strong_decay(dtype, law):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_bwd_large_theta(dtype):
+    """theta ~ U(-50, 50): phase sums of hundreds of revolutions per chunk, reduced token by
+    token in the kernels."""
+    laws = I.Laws(alpha=("uniform", 0.9, 1.0), theta=("uniform", -50.0, 50.0),
+                  beta=("uniform", 0.0, 1.0), s0_scale=0.1)
+    w = I.Workload("bwd", 1, 2, 3 * 64 + 37, 64, 64, 64, dtype, laws, 35, 1e-4)
+    x = I.make_chunk_inputs(w)
+    dO, dS = I.make_cotangents(1, 2, w.T, 64, 64, dtype, seed=36)
+    say(dtype, "large theta")
+    got = run_bwd(x, dO, dS, 64, dtype)
+    ref = oracle_bwd(x, dO, dS)
+    check(got, ref, 1e-4 if dtype == "f32" else 2e-2, f"{dtype} large theta")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_bwd_decay_outside_range_returns_nan(dtype):
     """alpha = 0.001 on one channel for the 16 tokens 144..159 (one chunk of the backward,
     decaying by 1e-48) is outside the range: dS0 and dv of that chunk and of every earlier

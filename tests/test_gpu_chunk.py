@@ -105,6 +105,17 @@ def test_unit_and_tiny_decay_across_channels(dtype, s0):
           label=f"mixed {dtype} S0 {s0}")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_large_theta(dtype):
+    """theta ~ U(-50, 50) per token and channel: the phase sums reach hundreds of
+    revolutions within a chunk; the kernels reduce them to [0, 1) revolutions token by
+    token, so the rotations stay exact to rounding."""
+    laws = I.Laws(alpha=("uniform", 0.9, 1.0), theta=("uniform", -50.0, 50.0),
+                  beta=("uniform", 0.0, 1.0), s0_scale=0.1)
+    check(small(T=3 * 64 + 37, laws=laws, dtype=dtype), 64, 1e-4 if dtype == "f32" else 2e-2,
+          label=f"large theta {dtype}")
+
+
 @pytest.mark.parametrize("dtype,ok_until,nan_from", [("bf16", 128, 128), ("f32", 144, 156)])
 def test_decay_outside_range_returns_nan(dtype, ok_until, nan_from):
     """One channel decaying by 1e-48 over a whole 16-token block (alpha = 0.001, tokens
