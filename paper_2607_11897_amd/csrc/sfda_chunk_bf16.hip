@@ -138,8 +138,12 @@ __device__ __forceinline__ void cmma(CAcc& z, u32x4 a, const BPair& b) {
 
 constexpr u32 OOB = 0x80000000u;     // lane offset that lies past every resource's range
 
+// Every caller passes a wave-uniform size.  readfirstlane keeps it in a scalar register: a
+// size the compiler had placed in a vector register (a max() does that) turns each load
+// through the resource into a loop over the distinct descriptors of the wave.
 __device__ __forceinline__ rsrc_t make_rsrc(const void* base, int bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, __builtin_amdgcn_readfirstlane(bytes),
+                                             0x00020000);
 }
 __device__ __forceinline__ u32 ld16(rsrc_t r, u32 off) {
     return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
@@ -238,7 +242,6 @@ struct Smem {
         u32x4 kr[MP * RP / 16];  // k_t e^{-i phi_t} Q_t              [channel][token]
         u32x4 nd[NB * 64];       // N_p = (I + D_beta L_p)^{-1}, one 16 x 16 block per block p
         u32x4 aq[NB * 64];       // A_p, lower triangle with the diagonal
-        float beta[CP];
         float dm[NB][MP];        // |D_p|: decay magnitude over block p, per channel
         int bad[NB];             // block p lies outside the decay range
     };
@@ -247,6 +250,8 @@ struct Smem {
     float2 xs[NB][16][18];       // per producer wave: X of its block (fp32, padded)
     float tph[2][NB][MP];        // per block: theta / 2 pi summed over it, reduced to [0, 1)
     float2 rot[MP];              // e^{i phi} at the last token: the final state rotation
+    float beta[3][CP];           // beta of step s at s % 3: written by the scans of step s
+                                 // (two steps ahead), read by the factors and the steps
 };
 
 struct Args {
@@ -320,6 +325,12 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         const int o_row_bytes = args.o ? n * Out<TOUT>::BYTES : 0;
         CAcc Sa[4];          // rotated state, rows kb*16 + 4g + r, column jw
         u32 vv[NB][4];       // v of the step in flight (complex bf16), prefetched
+        // bf16 output: o of the step's blocks (complex bf16), stored together at the end of the
+        // step.  A vector memory counter covers loads and stores in issue order, so a store
+        // issued between a block's V prefetch and the next is waited for with that prefetch;
+        // stored at the end of the step, every V prefetch of the step is older than them.
+        constexpr bool OPACK = Out<TOUT>::BYTES == 4;
+        u32 opk[NB][4];
 
         auto load_v = [&](int st, int p) {
             const int t0 = st * CP + p * 16;
@@ -369,7 +380,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     for (int r = 0; r < 4; ++r) { Sa[kb].re[r] *= dr[r]; Sa[kb].im[r] *= dr[r]; }
                 }
                 // R = D_beta (conj(V) - P)
-                const float4 bt = *reinterpret_cast<const float4*>(&ss.beta[p * 16 + 4 * g]);
+                const float4 bt = *reinterpret_cast<const float4*>(&sm.beta[st % 3][p * 16 + 4 * g]);
                 const float btr[4] = {bt.x, bt.y, bt.z, bt.w};
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
@@ -377,7 +388,10 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     R.re[r] = btr[r] * (bf_lo(w) - R.re[r]);
                     R.im[r] = -btr[r] * (bf_hi(w) + R.im[r]);
                 }
-                if (st + 1 < nsteps) load_v(st + 1, p);     // this block's v is consumed
+                // this block's v is consumed: the next step's (past the last step an empty
+                // range; issued every step so that every path through the loop has the same
+                // loads in flight and the wait counts stay exact)
+                load_v(st + 1, p);
                 // Delta = N_p R
                 const u32x4 fn = *reinterpret_cast<const u32x4*>(S + OFF_ND + p * 1024 + blk_frag(c, g));
                 CAcc d;
@@ -387,15 +401,32 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 // O += A_p Delta; o = conj(O^*), rows past T and columns past the slice dropped
                 const u32x4 fa = *reinterpret_cast<const u32x4*>(S + OFF_AQ + p * 1024 + blk_frag(c, g));
                 cmma(O, fa, db);
-                const rsrc_t ro = make_rsrc(go + 2 * (base_tn + static_cast<long>(t0) * n),
-                                            max(T - t0, 0) * o_row_bytes);
+                if constexpr (OPACK) {
 #pragma unroll
-                for (int r = 0; r < 4; ++r) Out<TOUT>::store(ro, voff_o[r], O.re[r], -O.im[r]);
+                    for (int r = 0; r < 4; ++r) opk[p][r] = pack_bf16(O.re[r], -O.im[r]);
+                } else {
+                    const rsrc_t ro = make_rsrc(go + 2 * (base_tn + static_cast<long>(t0) * n),
+                                                max(T - t0, 0) * o_row_bytes);
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) Out<TOUT>::store(ro, voff_o[r], O.re[r], -O.im[r]);
+                }
                 // S += (K Q)^T Delta: rows = channels kb*16 + c, K = the block's tokens
 #pragma unroll
                 for (int kb = 0; kb < 4; ++kb) {
                     const u32x4 f = *reinterpret_cast<const u32x4*>(S + OFF_KR + rm_frag(kb * 16 + c, p * 4 + g));
                     cmma(Sa[kb], f, db);
+                }
+            }
+            if constexpr (OPACK) {
+                if (p1 == NB) {
+#pragma unroll
+                    for (int p = 0; p < NB; ++p) {
+                        const int t0 = st * CP + p * 16;
+                        const rsrc_t ro = make_rsrc(go + 2 * (base_tn + static_cast<long>(t0) * n),
+                                                    max(T - t0, 0) * o_row_bytes);
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) __builtin_amdgcn_raw_buffer_store_b32(opk[p][r], ro, voff_o[r], 0, 0);
+                    }
                 }
             }
         };
@@ -429,7 +460,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             }
             // X = -(D_beta L), zero on and above the diagonal, to the wave's scratch; each
             // lane then reads back one row
-            const float4 bt = *reinterpret_cast<const float4*>(&ss.beta[pw * 16 + 4 * g]);
+            const float4 bt = *reinterpret_cast<const float4*>(&sm.beta[st % 3][pw * 16 + 4 * g]);
             const float btr[4] = {bt.x, bt.y, bt.z, bt.w};
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
@@ -526,21 +557,22 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             poff4[u] = pc0 < m ? e * 4u : OOB;
         }
         uint2 pa[4], pt[4];               // alpha, theta of the 4 channels (bf16 pairs)
-        // q, k of the 4 channels (complex bf16) and beta of one step; two of them, so that a
-        // step's q and k are requested a whole step before their operands are formed (global
-        // loads take several thousand cycles under this load); the copy waits for loads issued
-        // a step earlier
-        struct QK { u32x4 q[4], k[4]; u32 beta; };
+        u32 pb;                           // beta of the block's tokens (lanes 0..15)
+        // q, k of the 4 channels (complex bf16) of one step; two of them, so that a step's q
+        // and k are requested a whole step before their operands are formed (global loads take
+        // several thousand cycles under this load); the copy waits for loads issued a step
+        // earlier
+        struct QK { u32x4 q[4], k[4]; };
         QK cur, nxt;
 
-        // alpha, theta of step st (consumed by the scan, a step before the rest)
-        auto load_at = [&](int st) {
+        // alpha, theta, beta of step st (consumed by the scan, a step before the rest)
+        auto load_at = [&](int st, auto wide_c) __attribute__((always_inline)) {
             const int t0 = st * CP;
             const long e0 = base_tm + static_cast<long>(t0) * m;
-            const int rows = T - t0;
+            const int rows = max(T - t0, 0);      // past the last step: an empty range
             const rsrc_t ra = make_rsrc(args.alpha + e0, rows * m * 2);
             const rsrc_t rt = make_rsrc(args.theta + e0, rows * m * 2);
-            if (wide) {
+            if constexpr (decltype(wide_c)::value) {
 #pragma unroll
                 for (int u = 0; u < 4; ++u) {
                     const u32x2 a = ld64(ra, poff2[u]), t = ld64(rt, poff2[u]);
@@ -562,15 +594,17 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     pt[u] = make_uint2(t4[0] | (t4[1] << 16), t4[2] | (t4[3] << 16));
                 }
             }
+            const rsrc_t rb = make_rsrc(args.beta + base_t + t0, rows * 2);
+            pb = ld16(rb, lane < 16 ? static_cast<u32>(pw * 16 + lane) * 2u : OOB);
         };
-        // q, k, beta of step st (beta: lanes 0..15 hold the block's 16 tokens)
-        auto load_qk = [&](int st, QK& b) {
+        // q, k of step st
+        auto load_qk = [&](int st, QK& b, auto wide_c) __attribute__((always_inline)) {
             const int t0 = st * CP;
             const long e0 = base_tm + static_cast<long>(t0) * m;
-            const int rows = T - t0;
+            const int rows = max(T - t0, 0);      // past the last step: an empty range
             const rsrc_t rq = make_rsrc(args.q + 2 * e0, rows * m * 4);
             const rsrc_t rk = make_rsrc(args.k + 2 * e0, rows * m * 4);
-            if (wide) {
+            if constexpr (decltype(wide_c)::value) {
 #pragma unroll
                 for (int u = 0; u < 4; ++u) {
                     b.q[u] = ld128(rq, poff4[u]);
@@ -587,8 +621,6 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                         b.k[u][k] = ld32(rk, ok ? e * 4u : OOB);
                     }
             }
-            const rsrc_t rb = make_rsrc(args.beta + base_t + t0, rows * 2);
-            b.beta = ld16(rb, lane < 16 ? static_cast<u32>(pw * 16 + lane) * 2u : OOB);
         };
 
         // Scans of one block per channel (three levels: the lane's 4 tokens, the wave's four
@@ -601,7 +633,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         float Pf[4][4], Qb[4][4], ph[4][4];   // [token u][channel k] of the lane
         float dtot[4], invd[4];               // block decay magnitude D and 1 / D per channel
         int oor = 0;                          // a channel of the block decays below 2^-126
-        auto pretot_body = [&](int st, auto padded) {
+        auto pretot_body = [&](int st, auto padded) __attribute__((always_inline)) {
             const bool s0 = tsg == 0, s01 = tsg < 2, s3 = tsg == 3, s23 = tsg >= 2;
             float tpk[4];
             bool low = false;
@@ -669,15 +701,20 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
 
         // scans of step st (inputs in pa, pt), the block's phase total to LDS.  Only a step
         // with padding (ragged tail, m < 64) needs the identity-token substitution.
-        auto pretot = [&](int st) {
+        auto pretot = [&](int st) __attribute__((always_inline)) {
             if ((st + 1) * CP <= T && m == MP) pretot_body(st, std::false_type{});
             else pretot_body(st, std::true_type{});
+            if (lane < 16) {
+                float bt = bf16_bits_to_f32(static_cast<uint16_t>(pb));
+                if constexpr (GATED) bt = st * CP + pw * 16 + lane < T ? sigmoid_f(bt) : 0.f;
+                sm.beta[st % 3][pw * 16 + lane] = bt;
+            }
         };
 
         float base[4] = {0.f, 0.f, 0.f, 0.f};   // phase (revolutions) before the step, per channel
 
         // operands of step st into set st & 1: conj(Q)G, conj(K)G, K Q and the Gram operand
-        auto produce = [&](int st, const QK& b) {
+        auto produce = [&](int st, const QK& b) __attribute__((always_inline)) {
             char* S = set_ptr(st & 1);
             Set& ss = sm.set[st & 1];
             float off[4];
@@ -750,40 +787,45 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 for (int w2 = 0; w2 < NB; ++w2) tot += sm.tph[st & 1][w2][pc0 + k];
                 base[k] = __builtin_amdgcn_fractf(tot);
             }
-            if (lane < 16) {
-                float bt = bf16_bits_to_f32(static_cast<uint16_t>(b.beta));
-                if constexpr (GATED) bt = st * CP + pw * 16 + lane < T ? sigmoid_f(bt) : 0.f;
-                ss.beta[pw * 16 + lane] = bt;
-            }
             if (tsg == 0) *reinterpret_cast<float4*>(&ss.dm[pw][pc0]) = make_float4(dtot[0], dtot[1], dtot[2], dtot[3]);
             if (lane == 0) ss.bad[pw] = oor;
         };
 
-        if (nsteps > 0) {
-            load_at(0);
-            load_qk(0, nxt);
-            pretot(0);
-            if (nsteps > 1) load_at(1);
-        }
-        __syncthreads();          // block phase totals of step 0
-        for (int st = -1; st < nsteps; ++st) {
-            // phase 1: the operands of step st + 1 (q, k requested a step ago), the next q, k.
-            // The gated variant's scans hold more registers: it keeps one buffer and requests
-            // the next q, k once the operands are formed.
-            if constexpr (GATED) {
-                if (st + 1 < nsteps) produce(st + 1, nxt);
-                if (st + 2 < nsteps) load_qk(st + 2, nxt);
-            } else {
-                if (st + 1 < nsteps) cur = nxt;
-                if (st + 2 < nsteps) load_qk(st + 2, nxt);
-                if (st + 1 < nsteps) produce(st + 1, cur);
+        // The step loop is instantiated once per load shape (4-channel vector loads, or one
+        // channel per load for m not a multiple of 4), so that every path through one
+        // instance issues the same loads and the compiler's wait counts stay exact.
+        auto run = [&](auto wide_c) __attribute__((always_inline)) {
+            if (nsteps > 0) {
+                load_at(0, wide_c);
+                load_qk(0, nxt, wide_c);
+                pretot(0);
+                if (nsteps > 1) load_at(1, wide_c);
             }
-            __syncthreads();
-            // phase 2: the scans of step st + 2, alpha and theta of the step after
-            if (st + 2 < nsteps) pretot(st + 2);
-            if (st + 3 < nsteps) load_at(st + 3);
-            __syncthreads();
-        }
+            __syncthreads();          // block phase totals of step 0
+            for (int st = -1; st < nsteps; ++st) {
+                // phase 1: the operands of step st + 1 (q, k requested a step ago), the next
+                // q, k.  The gated variant's scans hold more registers: it keeps one buffer and
+                // requests the next q, k once the operands are formed.  The loads are issued
+                // on every step (past the last step their ranges are empty): a path without
+                // them would make the wait counts at the loop head cover the younger alpha,
+                // theta and beta loads too.
+                if constexpr (GATED) {
+                    if (st + 1 < nsteps) produce(st + 1, nxt);
+                    load_qk(st + 2, nxt, wide_c);
+                } else {
+                    if (st + 1 < nsteps) cur = nxt;
+                    load_qk(st + 2, nxt, wide_c);
+                    if (st + 1 < nsteps) produce(st + 1, cur);
+                }
+                __syncthreads();
+                // phase 2: the scans of step st + 2, alpha, theta and beta of the step after
+                if (st + 2 < nsteps) pretot(st + 2);
+                load_at(st + 3, wide_c);
+                __syncthreads();
+            }
+        };
+        if (wide) run(std::true_type{});
+        else run(std::false_type{});
         // The compiler joins the two roles' control flow after the producer's exit, and the
         // wait-count analysis then treats the producer's last loads as in flight inside the
         // consumer loop; clearing them here keeps that loop from waiting on its own V loads.
