@@ -252,6 +252,8 @@ struct Smem {
     float2 rot[MP];              // e^{i phi} at the last token: the final state rotation
     float beta[3][CP];           // beta of step s at s % 3: written by the scans of step s
                                  // (two steps ahead), read by the factors and the steps
+    u32 ostage[2][NB][256];      // o of consumer waves 0, 1 per block (complex bf16, token-major
+                                 // 16 x 16), stored to global memory by waves 2, 3
 };
 
 struct Args {
@@ -331,6 +333,12 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         // stored at the end of the step, every V prefetch of the step is older than them.
         constexpr bool OPACK = Out<TOUT>::BYTES == 4;
         u32 opk[NB][4];
+        // A slice of exactly 32 columns leaves waves 2 and 3 without columns: then waves 0 and 1
+        // put each block's o into LDS and waves 2 and 3 store it, 16 bytes per lane (store
+        // instructions cost the issuing wave; these two waves have time to spare).
+        const bool staged = OPACK && scols == 32;                 // wave-uniform
+        const bool helper = staged && wave >= 2;
+        const int hw = wave - 2;                                 // the wave a helper stores for
 
         auto load_v = [&](int st, int p) {
             const int t0 = st * CP + p * 16;
@@ -402,8 +410,14 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 const u32x4 fa = *reinterpret_cast<const u32x4*>(S + OFF_AQ + p * 1024 + blk_frag(c, g));
                 cmma(O, fa, db);
                 if constexpr (OPACK) {
+                    if (staged) {
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) opk[p][r] = pack_bf16(O.re[r], -O.im[r]);
+                        for (int r = 0; r < 4; ++r)
+                            sm.ostage[wave][p][(4 * g + r) * 16 + c] = pack_bf16(O.re[r], -O.im[r]);
+                    } else {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) opk[p][r] = pack_bf16(O.re[r], -O.im[r]);
+                    }
                 } else {
                     const rsrc_t ro = make_rsrc(go + 2 * (base_tn + static_cast<long>(t0) * n),
                                                 max(T - t0, 0) * o_row_bytes);
@@ -418,7 +432,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 }
             }
             if constexpr (OPACK) {
-                if (p1 == NB) {
+                if (p1 == NB && !staged) {
 #pragma unroll
                     for (int p = 0; p < NB; ++p) {
                         const int t0 = st * CP + p * 16;
@@ -429,6 +443,17 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     }
                 }
             }
+        };
+
+        // a helper wave's store of block p of step s: lane L takes token L / 4, columns
+        // 4 (L % 4) .. 4 (L % 4) + 3 of wave hw's 16 (rows past T are dropped by the range)
+        auto hstore = [&](int s, int p) {
+            const int t0 = s * CP + p * 16;
+            const rsrc_t ro = make_rsrc(go + 2 * (base_tn + static_cast<long>(t0) * n),
+                                        max(T - t0, 0) * o_row_bytes);
+            const u32x4 w = *reinterpret_cast<const u32x4*>(&sm.ostage[hw][p][(lane >> 2) * 16 + 4 * (lane & 3)]);
+            const u32 off = static_cast<u32>((lane >> 2) * n + n0 + 16 * hw + 4 * (lane & 3)) * 4u;
+            __builtin_amdgcn_raw_buffer_store_b128(w, ro, off, 0, 0);
         };
 
         // block `wave` of step st: its Gram matrices L (strict lower) and A (with the diagonal)
@@ -512,12 +537,18 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         for (int st = -1; st < nsteps; ++st) {
             // phase 1: the first NB1 blocks of step st (the producers form step st + 1's operands)
             if (active && st >= 0) consume(st, 0, NB1);
+            if (helper && st >= 1) hstore(st - 1, NB - 1);
             __syncthreads();
             // phase 2: this wave's block of step st + 1 (Grams, inverse), the rest of step st
             if (st + 1 < nsteps) diag(st + 1);
             if (active && st >= 0) consume(st, NB1, NB);
+            if (helper && st >= 0) {
+#pragma unroll
+                for (int p = 0; p < NB1; ++p) hstore(st, p);
+            }
             __syncthreads();
         }
+        if (helper && nsteps > 0) hstore(nsteps - 1, NB - 1);
         if (active && args.S_T != nullptr) {
             // back from the rotated frame: S_T = diag(e^{i phi_T}) S
             const rsrc_t rs = make_rsrc(args.S_T + 2 * base_mn, m * n * 8);
