@@ -537,7 +537,10 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         for (int st = -1; st < nsteps; ++st) {
             // phase 1: the first NB1 blocks of step st (the producers form step st + 1's operands)
             if (active && st >= 0) consume(st, 0, NB1);
-            if (helper && st >= 1) hstore(st - 1, NB - 1);
+            if (helper && st >= 1) {                 // the previous step's last blocks
+#pragma unroll
+                for (int p = NB1; p < NB; ++p) hstore(st - 1, p);
+            }
             __syncthreads();
             // phase 2: this wave's block of step st + 1 (Grams, inverse), the rest of step st
             if (st + 1 < nsteps) diag(st + 1);
@@ -548,7 +551,10 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             }
             __syncthreads();
         }
-        if (helper && nsteps > 0) hstore(nsteps - 1, NB - 1);
+        if (helper && nsteps > 0) {
+#pragma unroll
+            for (int p = NB1; p < NB; ++p) hstore(nsteps - 1, p);
+        }
         if (active && args.S_T != nullptr) {
             // back from the rotated frame: S_T = diag(e^{i phi_T}) S
             const rsrc_t rs = make_rsrc(args.S_T + 2 * base_mn, m * n * 8);
