@@ -26,10 +26,12 @@
 //   W  U = T conj(V) (kept in registers), Wt = T (conj(K) * G) (to LDS)
 //   D  Delta = U - Wt S, O = (conj(Q) * G) S + tril(A) Delta, S = diag(g_C)(S + (K/G)^T Delta)
 //
-// Numerics: g_t is formed from fp32 running sums of log alpha and theta (local to the
-// chunk), so K / G grows like exp(-sum log alpha); the caller keeps the in-chunk decay
-// product above ~1e-30.  Accumulation and the state are fp32; with PREC_BF16 the matrix
-// products take bf16 operands (the solve always runs in fp32).
+// Numerics: g_t is formed from fp32 running sums of log alpha and of theta / 2 pi (local to
+// the chunk, the phase reduced to [0, 1) revolutions token by token), so K / G grows like
+// exp(-sum log alpha): the launchers run 16-token chunks, inside the float range while the
+// chunk's decay is at least 2^-126, and the load stage makes K / G NaN past that.
+// Accumulation and the state are fp32; with PREC_BF16 the matrix products take bf16
+// operands (the solve always runs in fp32).
 //
 // The same kernel runs the two scans of the backward: MODE 1 is the forward recording the
 // state entering each chunk and Delta; MODE 2 walks the chunks in reverse carrying dL/dS
