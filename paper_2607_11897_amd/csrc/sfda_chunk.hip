@@ -817,7 +817,6 @@ static hipError_t launch_scans_t(const ChunkLaunch& F, const ChunkLaunch& A, hip
     const dim3 grid(static_cast<unsigned>(nf + static_cast<long>(A.B) * A.H * aa.n_slices));
     switch (F.C) {
         case 16: hipLaunchKernelGGL((scan_pair_kernel<P, TIN, TOUT, 16>), grid, dim3(scan_waves<16>() * 64), 0, st, af, aa, nfwd); break;
-        case 32: hipLaunchKernelGGL((scan_pair_kernel<P, TIN, TOUT, 32>), grid, dim3(scan_waves<32>() * 64), 0, st, af, aa, nfwd); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -95,12 +95,13 @@ struct ChunkSmemDec : ChunkSmem<C> {
     float wb[C];                             // write strengths beta_t
 };
 
-// alpha, theta and beta of one thread's tokens, fetched a chunk ahead by a scan, as the
-// loaded words (a bf16 value is converted where it is used, so the fetch is not waited on
-// where it is issued)
+// alpha, theta, beta, q and k of one thread's tokens, fetched a chunk ahead by a scan, as
+// the loaded words (a bf16 value is converted where it is used, so the fetch is not waited
+// on where it is issued); q, k take one word per complex bf16 value, two per complex fp32
 template <int C>
 struct InPre {
     uint32_t a[C / 4], th[C / 4], b;
+    uint32_t q[C / 4][2], k[C / 4][2];
 };
 template <typename TIN> __device__ __forceinline__ uint32_t raw_word(const void* p, long e) {
     if constexpr (sizeof(TIN) == 2) return static_cast<const uint16_t*>(p)[e];
@@ -124,6 +125,14 @@ __device__ __forceinline__ void prefetch_inputs(const ChunkArgs& args, long bh, 
         const long e = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
         pf.a[u] = raw_word<TIN>(args.alpha, e);
         pf.th[u] = raw_word<TIN>(args.theta, e);
+        if constexpr (sizeof(TIN) == 2) {
+            pf.q[u][0] = static_cast<const uint32_t*>(args.q)[e];
+            pf.k[u][0] = static_cast<const uint32_t*>(args.k)[e];
+        } else {
+            const uint2 qw = static_cast<const uint2*>(args.q)[e], kw = static_cast<const uint2*>(args.k)[e];
+            pf.q[u][0] = qw.x; pf.q[u][1] = qw.y;
+            pf.k[u][0] = kw.x; pf.k[u][1] = kw.y;
+        }
     }
     pf.b = raw_word<TIN>(args.beta, bh * static_cast<long>(T) + min(t0 + (tid & (C - 1)), T - 1));
 }
@@ -164,14 +173,15 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
     float la[SEG], ph[SEG];
     float sa = 0.f, sp = 0.f;
     float2 qpre[PRE ? SEG : 1], kpre[PRE ? SEG : 1];
-    if constexpr (PRE) {
-        if (worker) {
+    if constexpr (PRE) {            // q, k from the chunk-ahead fetch
 #pragma unroll
-            for (int u = 0; u < SEG; ++u) {
-                const int t = t0 + seg * SEG + u;
-                const long e2 = base_tm + static_cast<long>(min(t, T - 1)) * m + min(i, m - 1);
-                qpre[u] = Elem<TIN>::load2(gq, e2);
-                kpre[u] = Elem<TIN>::load2(gk, e2);
+        for (int u = 0; u < SEG; ++u) {
+            if constexpr (sizeof(TIN) == 2) {
+                qpre[u] = make_float2(__uint_as_float(pre->q[u][0] << 16), __uint_as_float(pre->q[u][0] & 0xFFFF0000u));
+                kpre[u] = make_float2(__uint_as_float(pre->k[u][0] << 16), __uint_as_float(pre->k[u][0] & 0xFFFF0000u));
+            } else {
+                qpre[u] = make_float2(__uint_as_float(pre->q[u][0]), __uint_as_float(pre->q[u][1]));
+                kpre[u] = make_float2(__uint_as_float(pre->k[u][0]), __uint_as_float(pre->k[u][1]));
             }
         }
     }

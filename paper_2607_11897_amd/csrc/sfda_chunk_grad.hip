@@ -28,8 +28,8 @@
 // product accumulates over the blocks in registers, so the pass waits on global memory
 // once per block instead of once per product; products over tokens read the decay-scaled
 // operands from LDS.  The C x C gradients G_L' and G_A share one LDS block (G_L' strict
-// lower, G_A^T upper with the diagonal).  C = 16 and 32 (the chunk's LDS and the staged
-// block together stay within one CU's 160 KB).
+// lower, G_A^T upper with the diagonal).  The library launches it at C = 16 (the chunk length
+// of the whole backward).
 #include <type_traits>
 
 #include "sfda_chunk_common.h"
@@ -691,7 +691,6 @@ static hipError_t launch_grad_t(const GradLaunch& L, hipStream_t st)
     const dim3 grid(static_cast<unsigned>(static_cast<long>(L.B) * L.H * nchunks));
     switch (L.C) {
         case 16: hipLaunchKernelGGL((grad_kernel<P, TIN, TOUT, 16>), grid, dim3(GW * 64), 0, st, a); break;
-        case 32: hipLaunchKernelGGL((grad_kernel<P, TIN, TOUT, 32>), grid, dim3(GW * 64), 0, st, a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
