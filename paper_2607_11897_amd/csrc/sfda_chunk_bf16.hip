@@ -333,9 +333,10 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         // stored at the end of the step, every V prefetch of the step is older than them.
         constexpr bool OPACK = Out<TOUT>::BYTES == 4;
         u32 opk[NB][4];
-        // A slice of exactly 32 columns leaves waves 2 and 3 without columns: then waves 0 and 1
-        // put each block's o into LDS and waves 2 and 3 store it, 16 bytes per lane (store
-        // instructions cost the issuing wave; these two waves have time to spare).
+        // A slice of exactly 32 columns leaves waves 2 and 3 without columns: then they do the
+        // global memory traffic of waves 0 and 1 through an LDS slot per block, 16 bytes per
+        // lane: load V into it before the block, store the o that waves 0 and 1 put into it
+        // after (memory instructions cost the issuing wave; these two have time to spare).
         const bool staged = OPACK && scols == 32;                 // wave-uniform
         const bool helper = staged && wave >= 2;
         const int hw = wave - 2;                                 // the wave a helper stores for
@@ -387,9 +388,13 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
 #pragma unroll
                     for (int r = 0; r < 4; ++r) { Sa[kb].re[r] *= dr[r]; Sa[kb].im[r] *= dr[r]; }
                 }
-                // R = D_beta (conj(V) - P)
+                // R = D_beta (conj(V) - P); staged: V of the block from the staging slot
                 const float4 bt = *reinterpret_cast<const float4*>(&sm.beta[st % 3][p * 16 + 4 * g]);
                 const float btr[4] = {bt.x, bt.y, bt.z, bt.w};
+                if (staged) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) vv[p][r] = sm.ostage[wave][p][(4 * g + r) * 16 + c];
+                }
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const u32 w = vv[p][r];
@@ -399,7 +404,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 // this block's v is consumed: the next step's (past the last step an empty
                 // range; issued every step so that every path through the loop has the same
                 // loads in flight and the wait counts stay exact)
-                load_v(st + 1, p);
+                if (!staged) load_v(st + 1, p);
                 // Delta = N_p R
                 const u32x4 fn = *reinterpret_cast<const u32x4*>(S + OFF_ND + p * 1024 + blk_frag(c, g));
                 CAcc d;
@@ -454,6 +459,19 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             const u32x4 w = *reinterpret_cast<const u32x4*>(&sm.ostage[hw][p][(lane >> 2) * 16 + 4 * (lane & 3)]);
             const u32 off = static_cast<u32>((lane >> 2) * n + n0 + 16 * hw + 4 * (lane & 3)) * 4u;
             __builtin_amdgcn_raw_buffer_store_b128(w, ro, off, 0, 0);
+        };
+        // ... and its load of wave hw's V for block p of step s (the same lane layout), put into
+        // the block's slot once the slot's o has been stored: the slot then holds V until
+        // wave hw reads it at the start of the block, and o after the block
+        u32x4 hv[NB];
+        auto hload = [&](int s, int p) {
+            const int t0 = s * CP + p * 16;
+            const rsrc_t rv = make_rsrc(args.v + 2 * (base_tn + static_cast<long>(t0) * n),
+                                        max(T - t0, 0) * v_row_bytes);
+            hv[p] = ld128(rv, static_cast<u32>((lane >> 2) * n + n0 + 16 * hw + 4 * (lane & 3)) * 4u);
+        };
+        auto hput = [&](int p) {
+            *reinterpret_cast<u32x4*>(&sm.ostage[hw][p][(lane >> 2) * 16 + 4 * (lane & 3)]) = hv[p];
         };
 
         // block `wave` of step st: its Gram matrices L (strict lower) and A (with the diagonal)
@@ -528,7 +546,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     Sa[kb].re[r] = __uint_as_float(x.x);
                     Sa[kb].im[r] = __uint_as_float(x.y);
                 }
-            if (nsteps > 0) {
+            if (nsteps > 0 && !staged) {
 #pragma unroll
                 for (int p = 0; p < NB; ++p) load_v(0, p);
             }
@@ -536,18 +554,32 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         __syncthreads();          // matches the producers' lead-in barrier
         for (int st = -1; st < nsteps; ++st) {
             // phase 1: the first NB1 blocks of step st (the producers form step st + 1's operands)
-            if (active && st >= 0) consume(st, 0, NB1);
-            if (helper && st >= 1) {                 // the previous step's last blocks
+            if (helper) {                            // V of the next step's first blocks
 #pragma unroll
-                for (int p = NB1; p < NB; ++p) hstore(st - 1, p);
+                for (int p = 0; p < NB1; ++p) hload(st + 1, p);
+            }
+            if (active && st >= 0) consume(st, 0, NB1);
+            if (helper) {                            // the previous step's last blocks: o out, V in
+#pragma unroll
+                for (int p = NB1; p < NB; ++p) {
+                    if (st >= 1) hstore(st - 1, p);
+                    if (st >= 0) hput(p);
+                }
             }
             __syncthreads();
             // phase 2: this wave's block of step st + 1 (Grams, inverse), the rest of step st
+            if (helper) {                            // V of the next step's last blocks
+#pragma unroll
+                for (int p = NB1; p < NB; ++p) hload(st + 1, p);
+            }
             if (st + 1 < nsteps) diag(st + 1);
             if (active && st >= 0) consume(st, NB1, NB);
-            if (helper && st >= 0) {
+            if (helper) {                            // this step's first blocks: o out, V in
 #pragma unroll
-                for (int p = 0; p < NB1; ++p) hstore(st, p);
+                for (int p = 0; p < NB1; ++p) {
+                    if (st >= 0) hstore(st, p);
+                    hput(p);
+                }
             }
             __syncthreads();
         }
