@@ -33,6 +33,10 @@
 // Accumulation and the state are fp32; with PREC_BF16 the matrix products take bf16
 // operands (the solve always runs in fp32).
 //
+// The forward at 16-token chunks (every launch of MODE 0) runs these stages split by role
+// instead (chunk_scan_pipe below): four waves prepare chunk c + 1 in a second LDS set while
+// the other four run chunk c's state-dependent stage.
+//
 // The same kernel runs the two scans of the backward: MODE 1 is the forward recording the
 // state entering each chunk and Delta; MODE 2 walks the chunks in reverse carrying dL/dS
 // (the adjoint of the chunk map, adjoint_chunk below) and records it with G_F.
@@ -726,6 +730,325 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
     }
 }
 
+// ---------------------------------------------------------------- pipelined forward scan
+// The forward for 16-token chunks with the work split by role: waves 4-7 prepare chunk c + 1
+// (load stage, Gram products, inverse and Wt = T (conj(K) G), into a second LDS set) while
+// waves 0-3, which own the value columns and keep the state, run the state-dependent stage
+// of chunk c between the same barriers:
+//   column waves:     -       | Delta   | O       | S update | U of c + 1 |  -
+//   preparing waves:  sums of c + 1 | operands | Gram | inverse | Wt tiles | Wt to LDS
+// (the column waves pass the load stage's inner barrier first, so the running sums of the
+// next chunk do not wait for Delta).  The stage functions take a thread index per role: the
+// preparing waves pass theirs less 256 (the first 256 "threads"), the column waves theirs
+// plus 256 (past the workers, so they only take part in the stages' barriers).
+template <int P, typename TIN, typename TOUT, bool GATED>
+__device__ __forceinline__ void chunk_scan_pipe(ChunkSmem<16> (&sms)[2], const ChunkArgs& args, unsigned block, long heads)
+{
+    constexpr int C = 16;
+    constexpr int NC = 4;                         // column waves (0..3); preparing waves 4..7
+    constexpr int CBW = 2;                        // column blocks per column wave: w, w + 4
+    constexpr int SEG = C / 4;
+    constexpr int LDG = ChunkSmem<C>::LDG;
+    using SM = ChunkSmem<C>;
+
+    const TIN* __restrict__ gv = static_cast<const TIN*>(args.v);
+    TOUT* __restrict__ go = static_cast<TOUT*>(args.o);
+    const int T = args.T, m = args.m, n = args.n;
+    long bh;
+    int sl;
+    head_slice(block, args.n_slices, heads, bh, sl);
+    const int n0 = sl * args.slice;
+    const int ncb = (min(args.slice, n - n0) + 7) / 8;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const bool cols = wave < NC;                  // wave-uniform role
+    const int rtid = cols ? tid + 256 : tid - 256;   // thread index for the stage functions
+    const int pwave = wave - NC;                  // preparing wave 0..3
+    const int c = lane & 15;
+    const int g = lane >> 4;
+    const int qp = lane & 1;
+    const long base_tn = bh * static_cast<long>(T) * n;
+    const long base_mn = bh * static_cast<long>(m) * n;
+    const int nchunks = (T + C - 1) / C;
+
+    // ---------------------------------------------------------------- state (column waves)
+    f32x4 Sacc[CBW][MP / 16];
+    if (cols) {
+        const rsrc_t rs = buf(args.S0 ? args.S0 + 2 * base_mn : args.S0, args.S0 ? static_cast<long>(m) * n * 8 : 0);
+#pragma unroll
+        for (int w = 0; w < CBW; ++w) {
+            const int cb = wave + NC * w;
+            const int j = n0 + cb * 8 + (c >> 1);
+            const bool jok = cb < ncb && j < n;
+#pragma unroll
+            for (int kb = 0; kb < MP / 16; ++kb)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int i = kb * 16 + 4 * g + r;
+                    Sacc[w][kb][r] = ld_f32(rs, jok ? static_cast<uint32_t>(((i * n + j) * 2 + qp) * 4) : OOR);
+                }
+        }
+    }
+
+    InPre<C> pf;
+    if (nchunks > 0) prefetch_inputs<TIN, C, true>(args, bh, 0, rtid, pf);
+
+    // ---------------------------------------------------------------- stage pieces
+    float2 vf[CBW][4];                            // column waves: conj(V) fragments of the next chunk
+    auto load_v = [&](int ch) __attribute__((always_inline)) {
+        const int t0 = ch * C;
+        const long vbytes = gv ? static_cast<long>(min(C, T - t0)) * n * 2 * sizeof(TIN) : 0;
+        const rsrc_t rv = buf(gv ? gv + 2 * (base_tn + static_cast<long>(t0) * n) : gv, vbytes);
+#pragma unroll
+        for (int w = 0; w < CBW; ++w) {
+            const int cb = wave + NC * w;
+            const int j = n0 + cb * 8 + (c >> 1);
+            const bool jok = cb < ncb && j < n;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int tl = 4 * g + r;
+                vf[w][r] = ld_cplx<TIN>(rv, jok ? static_cast<uint32_t>((tl * n + j) * 2 * sizeof(TIN)) : OOR);
+            }
+        }
+    };
+    // load stage of chunk ch (every thread: it holds a barrier; the preparing waves work),
+    // then the chunk-ahead fetch of the next one
+    auto stage_L = [&](SM& sm, int ch) __attribute__((always_inline)) {
+        float2 gkeep[SEG];
+        stage_load<TIN, C, GATED, false, false, SM, true, true>(sm, args, bh, ch * C, rtid, gkeep, &pf);
+        if (ch + 1 < nchunks) prefetch_inputs<TIN, C, true>(args, bh, (ch + 1) * C, rtid, pf);
+    };
+    // L' and A, one 16 x 8 tile per preparing wave
+    auto stage_G = [&](SM& sm) __attribute__((always_inline)) { stage_gram<P, C, true, false, SM, 4>(sm, rtid); };
+    // N = (I + D_beta L')^{-1} on the first preparing wave, written over L'
+    auto stage_S = [&](SM& sm) __attribute__((always_inline)) {
+        if (pwave == 0) {
+            const int i = lane & 15, cg = lane >> 4;
+            const float bi = sm.beta[i];
+            float2 xrow[16];
+#pragma unroll
+            for (int s2 = 0; s2 < 16; ++s2) {
+                const float2 l = sm.g2[i * LDG + s2];
+                xrow[s2] = s2 < i ? make_float2(-bi * l.x, -bi * l.y) : make_float2(0.f, 0.f);
+            }
+            float nr[4], ni[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) { nr[k] = i == 4 * k + cg ? 1.f : 0.f; ni[k] = 0.f; }
+            subst_steps(nr, ni, xrow, std::make_integer_sequence<int, 15>{});
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                if (4 * k + cg < i) sm.g2[i * LDG + 4 * k + cg] = make_float2(nr[k], ni[k]);
+        }
+    };
+    // A fragment of T = N D_beta (rows c, K = the chunk's tokens)
+    auto tfrag = [&](SM& sm) __attribute__((always_inline)) {
+        Frag8 a;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int j = 4 * g + r;
+            float2 nvv = sm.g2[c * LDG + j];
+            nvv = j < c ? nvv : make_float2(j == c ? 1.f : 0.f, 0.f);
+            const float bj = sm.beta[j];
+            a.v[2 * r] = nvv.x * bj;
+            a.v[2 * r + 1] = nvv.y * bj;
+        }
+        return a;
+    };
+    f32x4 U[CBW];                 // column waves: U = T conj(V), then Delta
+    auto stage_U = [&](SM& sm) __attribute__((always_inline)) {
+        const Frag8 ta = tfrag(sm);
+#pragma unroll
+        for (int w = 0; w < CBW; ++w) {
+            Frag8 bv;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) bpair(bv, r, vf[w][r].x, -vf[w][r].y, qp);
+            U[w] = zero4();
+            if (wave + NC * w < ncb) mma<P>(U[w], ta, bv);
+        }
+    };
+    // preparing waves: Wt = T (conj(K) G), two 16 x 8 tiles per wave, written over conj(K) G
+    // after a barrier
+    f32x4 wres[2];
+    auto stage_W1 = [&](SM& sm) __attribute__((always_inline)) {
+        const Frag8 ta = tfrag(sm);
+#pragma unroll
+        for (int it = 0; it < 2; ++it) {
+            const int icol = (pwave + 4 * it) * 8 + (c >> 1);
+            Frag8 b;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float2 y = sm.kg[(4 * g + r) * LDX + icol];
+                bpair(b, r, y.x, y.y, qp);
+            }
+            wres[it] = zero4();
+            mma<P>(wres[it], ta, b);
+        }
+    };
+    auto stage_W2 = [&](SM& sm) __attribute__((always_inline)) {
+        float* kgf = reinterpret_cast<float*>(sm.kg);
+#pragma unroll
+        for (int it = 0; it < 2; ++it) {
+            const int icol = (pwave + 4 * it) * 8 + (c >> 1);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) kgf[2 * ((4 * g + r) * LDX + icol) + qp] = wres[it][r];
+        }
+    };
+    static_assert(2 * MP / 16 == 2 * 4, "two Wt tiles per preparing wave");
+
+    // ---------------------------------------------------------------- prologue: first chunk
+    if (nchunks > 0) {
+        if (cols) load_v(0);
+        stage_L(sms[0], 0);
+        __syncthreads();
+        if (!cols) stage_G(sms[0]);
+        __syncthreads();
+        if (!cols) stage_S(sms[0]);
+        __syncthreads();
+        if (cols) stage_U(sms[0]);
+        else stage_W1(sms[0]);
+        __syncthreads();
+        if (!cols) stage_W2(sms[0]);
+        __syncthreads();
+    }
+
+    for (int ch = 0; ch < nchunks; ++ch) {
+        SM& cur = sms[ch & 1];
+        SM& nx = sms[(ch + 1) & 1];
+        const bool more = ch + 1 < nchunks;
+        const int t0 = ch * C;
+
+        // ---- Delta = U - Wt S (column waves) | the next chunk's load stage
+        if (more) stage_L(nx, ch + 1);
+        else __syncthreads();                     // the load stage's barrier
+        if (cols) {
+#pragma unroll
+            for (int w = 0; w < CBW; ++w) {
+                if (wave + NC * w >= ncb) continue;
+                f32x4 pw = zero4();
+#pragma unroll
+                for (int kb = 0; kb < MP / 16; ++kb) {
+                    Frag8 a;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const float2 x = cur.kg[c * LDX + kb * 16 + 4 * g + r];
+                        a.v[2 * r] = x.x;
+                        a.v[2 * r + 1] = x.y;
+                    }
+                    // (the state's and Delta's B fragments are re-formed where they are
+                    // used: a few row moves instead of registers held across barriers)
+                    mma<P>(pw, a, bfrag_from_acc(Sacc[w][kb], qp));
+                }
+                U[w] = U[w] - pw;
+            }
+            if (more) load_v(ch + 1);
+        }
+        __syncthreads();
+
+        // ---- O^* = conj(Q)G S + tril(A) Delta (column waves) | the next chunk's Gram products
+        if (cols) {
+#pragma unroll
+            for (int w = 0; w < CBW; ++w) {
+                const int cb = wave + NC * w;
+                if (cb >= ncb) continue;
+                const int j = n0 + cb * 8 + (c >> 1);
+                f32x4 acc = zero4();
+#pragma unroll
+                for (int kb = 0; kb < MP / 16; ++kb) {
+                    Frag8 a;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const float2 x = cur.qg[c * LDX + kb * 16 + 4 * g + r];
+                        a.v[2 * r] = x.x;
+                        a.v[2 * r + 1] = x.y;
+                    }
+                    mma<P>(acc, a, bfrag_from_acc(Sacc[w][kb], qp));
+                }
+                Frag8 a;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int jt = 4 * g + r;
+                    const float2 lo_p = pin(cur.g2[jt * LDG + c]), dg_p = pin(cur.g2[c * LDG + c]);
+                    const float2 x = masked(jt <= c, jt < c ? lo_p : dg_p);   // A[c][jt] (stored transposed)
+                    a.v[2 * r] = x.x;
+                    a.v[2 * r + 1] = x.y;
+                }
+                mma<P>(acc, a, bfrag_from_acc(U[w], qp));
+                if (j < n && go != nullptr) {     // o == NULL: no output
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int t = t0 + 4 * g + r;
+                        if (t < T)
+                            Elem<TOUT>::store(go, 2 * (base_tn + static_cast<long>(t) * n + j) + qp,
+                                              qp ? -acc[r] : acc[r]);
+                    }
+                }
+            }
+        } else if (more) {
+            stage_G(nx);
+        }
+        __syncthreads();
+
+        // ---- S = diag(g_C) S + diag(g_C) (K/G)^T Delta (column waves) | the next inverse
+        if (cols) {
+#pragma unroll
+            for (int w = 0; w < CBW; ++w) {
+                if (wave + NC * w >= ncb) continue;
+                const Frag8 db = bfrag_from_acc(U[w], qp);
+#pragma unroll
+                for (int kb = 0; kb < MP / 16; ++kb) {
+                    const int irow = kb * 16 + c;
+                    const float2 gcr = cur.gc[irow];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const float2 gg = cur.gc[kb * 16 + 4 * g + r];
+                        const float own = Sacc[w][kb][r];
+                        const float oth = partner(own);
+                        Sacc[w][kb][r] = qp ? (gg.x * own + gg.y * oth) : (gg.x * own - gg.y * oth);
+                    }
+                    Frag8 a;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const float2 x = cur.ki[(4 * g + r) * LDX + irow];
+                        a.v[2 * r] = x.x * gcr.x - x.y * gcr.y;
+                        a.v[2 * r + 1] = x.x * gcr.y + x.y * gcr.x;
+                    }
+                    mma<P>(Sacc[w][kb], a, db);
+                }
+            }
+        } else if (more) {
+            stage_S(nx);
+        }
+        __syncthreads();
+
+        // ---- U of the next chunk (column waves) | its Wt
+        if (more) {
+            if (cols) stage_U(nx);
+            else stage_W1(nx);
+        }
+        __syncthreads();
+        if (more && !cols) stage_W2(nx);
+        __syncthreads();
+    }
+
+    // ---------------------------------------------------------------- final state
+    if (cols && args.S_T != nullptr) {
+#pragma unroll
+        for (int w = 0; w < CBW; ++w) {
+            const int cb = wave + NC * w;
+            const int j = n0 + cb * 8 + (c >> 1);
+            if (cb >= ncb || j >= n) continue;
+#pragma unroll
+            for (int kb = 0; kb < MP / 16; ++kb)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int i = kb * 16 + 4 * g + r;
+                    if (i < m) args.S_T[2 * (base_mn + static_cast<long>(i) * n + j) + qp] = Sacc[w][kb][r];
+                }
+        }
+    }
+}
+
 // waves per workgroup: two per SIMD where the registers allow it (at C = 64 a second wave
 // per SIMD spills heavily), one otherwise
 template <int C> constexpr int scan_waves() { return C == 64 ? 4 : 8; }
@@ -734,8 +1057,13 @@ template <int P, typename TIN, typename TOUT, int C, bool GATED, int MODE>
 __global__ __launch_bounds__(scan_waves<C>() * 64, 1) void chunk_kernel(ChunkArgs args)
 {
     using SM = std::conditional_t<MODE == 3, ChunkSmemDec<C>, ChunkSmem<C>>;
-    __shared__ SM sm;
-    chunk_scan<P, TIN, TOUT, C, GATED, MODE, SM, scan_waves<C>()>(sm, args, blockIdx.x, gridDim.x / args.n_slices);
+    if constexpr (C == 16 && MODE == 0) {
+        __shared__ SM sms[2];
+        chunk_scan_pipe<P, TIN, TOUT, GATED>(sms, args, blockIdx.x, gridDim.x / args.n_slices);
+    } else {
+        __shared__ SM sm;
+        chunk_scan<P, TIN, TOUT, C, GATED, MODE, SM, scan_waves<C>()>(sm, args, blockIdx.x, gridDim.x / args.n_slices);
+    }
 }
 
 // The backward's two scans in one launch: the first nfwd workgroups run the recording
