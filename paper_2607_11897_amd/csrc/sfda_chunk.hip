@@ -290,6 +290,11 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
                 }
         }
     }
+    // The wait-count analysis joins the loop's entry with its back edge, so the state's
+    // loads above would count as in flight at every later use of the state registers (each
+    // record store in the loop would then wait for an older memory operation); waiting for
+    // them once here clears that.
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
 
     // eight-wave scans fetch alpha, theta and beta a chunk ahead (their registers fit there)
     constexpr bool PRE = NW > 4;
@@ -790,6 +795,7 @@ __device__ __forceinline__ void chunk_scan_pipe(ChunkSmem<16> (&sms)[2], const C
                 }
         }
     }
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): as in chunk_scan
 
     InPre<C> pf;
     if (nchunks > 0) prefetch_inputs<TIN, C, true>(args, bh, 0, rtid, pf);
