@@ -33,9 +33,9 @@
 // Accumulation and the state are fp32; with PREC_BF16 the matrix products take bf16
 // operands (the solve always runs in fp32).
 //
-// The forward at 16-token chunks (every launch of MODE 0) runs these stages split by role
-// instead (chunk_scan_pipe below): four waves prepare chunk c + 1 in a second LDS set while
-// the other four run chunk c's state-dependent stage.
+// The forward and the write-decoupled forward (MODE 0 and 3, always at 16-token chunks) run
+// these stages split by role instead (chunk_scan_pipe below): four waves prepare chunk c + 1
+// in a second LDS set while the other four run chunk c's state-dependent stage.
 //
 // The same kernel runs the two scans of the backward: MODE 1 is the forward recording the
 // state entering each chunk and Delta; MODE 2 walks the chunks in reverse carrying dL/dS
@@ -745,16 +745,18 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
 // (the column waves pass the load stage's inner barrier first, so the running sums of the
 // next chunk do not wait for Delta).  The stage functions take a thread index per role: the
 // preparing waves pass theirs less 256 (the first 256 "threads"), the column waves theirs
-// plus 256 (past the workers, so they only take part in the stages' barriers).
-template <int P, typename TIN, typename TOUT, bool GATED>
-__device__ __forceinline__ void chunk_scan_pipe(ChunkSmem<16> (&sms)[2], const ChunkArgs& args, unsigned block, long heads)
+// plus 256 (past the workers, so they only take part in the stages' barriers).  MODE 3 is
+// the write-decoupled forward (as in chunk_scan: R / G, the k-r and q-r Gram blocks and the
+// write rows Delta_r = D_beta conj(V) join the same stages).
+template <int P, typename TIN, typename TOUT, bool GATED, int MODE, typename SM>
+__device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& args, unsigned block, long heads)
 {
+    static_assert(MODE == 0 || MODE == 3, "the forward and the write-decoupled forward");
     constexpr int C = 16;
     constexpr int NC = 4;                         // column waves (0..3); preparing waves 4..7
     constexpr int CBW = 2;                        // column blocks per column wave: w, w + 4
     constexpr int SEG = C / 4;
     constexpr int LDG = ChunkSmem<C>::LDG;
-    using SM = ChunkSmem<C>;
 
     const TIN* __restrict__ gv = static_cast<const TIN*>(args.v);
     TOUT* __restrict__ go = static_cast<TOUT*>(args.o);
@@ -822,11 +824,14 @@ __device__ __forceinline__ void chunk_scan_pipe(ChunkSmem<16> (&sms)[2], const C
     // then the chunk-ahead fetch of the next one
     auto stage_L = [&](SM& sm, int ch) __attribute__((always_inline)) {
         float2 gkeep[SEG];
-        stage_load<TIN, C, GATED, false, false, SM, true, true>(sm, args, bh, ch * C, rtid, gkeep, &pf);
+        stage_load<TIN, C, GATED, false, MODE == 3, SM, true, true>(sm, args, bh, ch * C, rtid, gkeep, &pf);
         if (ch + 1 < nchunks) prefetch_inputs<TIN, C, true>(args, bh, (ch + 1) * C, rtid, pf);
     };
-    // L' and A, one 16 x 8 tile per preparing wave
-    auto stage_G = [&](SM& sm) __attribute__((always_inline)) { stage_gram<P, C, true, false, SM, 4>(sm, rtid); };
+    // L' and A, one 16 x 8 tile per preparing wave (MODE 3: then L'_kr and A_qr)
+    auto stage_G = [&](SM& sm) __attribute__((always_inline)) {
+        stage_gram<P, C, true, false, SM, 4>(sm, rtid);
+        if constexpr (MODE == 3) stage_gram<P, C, true, true, SM, 4>(sm, rtid);
+    };
     // N = (I + D_beta L')^{-1} on the first preparing wave, written over L'
     auto stage_S = [&](SM& sm) __attribute__((always_inline)) {
         if (pwave == 0) {
@@ -861,14 +866,37 @@ __device__ __forceinline__ void chunk_scan_pipe(ChunkSmem<16> (&sms)[2], const C
         }
         return a;
     };
-    f32x4 U[CBW];                 // column waves: U = T conj(V), then Delta
+    f32x4 U[CBW];                 // column waves: U = T conj(V) (MODE 3: U' = T L'_kr Delta_r), then Delta
+    Frag8 bvr[CBW];               // MODE 3: the write rows Delta_r = D_beta conj(V)
     auto stage_U = [&](SM& sm) __attribute__((always_inline)) {
         const Frag8 ta = tfrag(sm);
+        Frag8 a3;
+        if constexpr (MODE == 3) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int jt = 4 * g + r;
+                const float2 x = masked(jt < c, pin(sm.g3[c * LDG + jt]));   // L'_kr
+                a3.v[2 * r] = x.x;
+                a3.v[2 * r + 1] = x.y;
+            }
+        }
 #pragma unroll
         for (int w = 0; w < CBW; ++w) {
             Frag8 bv;
+            if constexpr (MODE == 3) {
+                // Delta_r, then Y = L'_kr Delta_r takes conj(V)'s place
 #pragma unroll
-            for (int r = 0; r < 4; ++r) bpair(bv, r, vf[w][r].x, -vf[w][r].y, qp);
+                for (int r = 0; r < 4; ++r) {
+                    const float bw = sm.wb[4 * g + r];
+                    bpair(bvr[w], r, bw * vf[w][r].x, -bw * vf[w][r].y, qp);
+                }
+                f32x4 y = zero4();
+                if (wave + NC * w < ncb) mma<P>(y, a3, bvr[w]);
+                bv = bfrag_from_acc(y, qp);
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) bpair(bv, r, vf[w][r].x, -vf[w][r].y, qp);
+            }
             U[w] = zero4();
             if (wave + NC * w < ncb) mma<P>(U[w], ta, bv);
         }
@@ -945,7 +973,8 @@ __device__ __forceinline__ void chunk_scan_pipe(ChunkSmem<16> (&sms)[2], const C
                     // used: a few row moves instead of registers held across barriers)
                     mma<P>(pw, a, bfrag_from_acc(Sacc[w][kb], qp));
                 }
-                U[w] = U[w] - pw;
+                if constexpr (MODE == 3) U[w] = -U[w] - pw;          // Delta_k = -(U' + Wt S)
+                else U[w] = U[w] - pw;
             }
             if (more) load_v(ch + 1);
         }
@@ -980,6 +1009,17 @@ __device__ __forceinline__ void chunk_scan_pipe(ChunkSmem<16> (&sms)[2], const C
                     a.v[2 * r + 1] = x.y;
                 }
                 mma<P>(acc, a, bfrag_from_acc(U[w], qp));
+                if constexpr (MODE == 3) {            // + A_qr Delta_r
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int jt = 4 * g + r;
+                        const float2 lo_p = pin(cur.g3[jt * LDG + c]), dg_p = pin(cur.g3[c * LDG + c]);
+                        const float2 x = masked(jt <= c, jt < c ? lo_p : dg_p);
+                        a.v[2 * r] = x.x;
+                        a.v[2 * r + 1] = x.y;
+                    }
+                    mma<P>(acc, a, bvr[w]);
+                }
                 if (j < n && go != nullptr) {     // o == NULL: no output
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
@@ -1020,6 +1060,15 @@ __device__ __forceinline__ void chunk_scan_pipe(ChunkSmem<16> (&sms)[2], const C
                         a.v[2 * r + 1] = x.x * gcr.y + x.y * gcr.x;
                     }
                     mma<P>(Sacc[w][kb], a, db);
+                    if constexpr (MODE == 3) {            // + diag(g_C) (R/G)^T Delta_r
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const float2 x = cur.ri[(4 * g + r) * LDX + irow];
+                            a.v[2 * r] = x.x * gcr.x - x.y * gcr.y;
+                            a.v[2 * r + 1] = x.x * gcr.y + x.y * gcr.x;
+                        }
+                        mma<P>(Sacc[w][kb], a, bvr[w]);
+                    }
                 }
             }
         } else if (more) {
@@ -1063,9 +1112,9 @@ template <int P, typename TIN, typename TOUT, int C, bool GATED, int MODE>
 __global__ __launch_bounds__(scan_waves<C>() * 64, 1) void chunk_kernel(ChunkArgs args)
 {
     using SM = std::conditional_t<MODE == 3, ChunkSmemDec<C>, ChunkSmem<C>>;
-    if constexpr (C == 16 && MODE == 0) {
+    if constexpr (C == 16 && (MODE == 0 || MODE == 3)) {
         __shared__ SM sms[2];
-        chunk_scan_pipe<P, TIN, TOUT, GATED>(sms, args, blockIdx.x, gridDim.x / args.n_slices);
+        chunk_scan_pipe<P, TIN, TOUT, GATED, MODE, SM>(sms, args, blockIdx.x, gridDim.x / args.n_slices);
     } else {
         __shared__ SM sm;
         chunk_scan<P, TIN, TOUT, C, GATED, MODE, SM, scan_waves<C>()>(sm, args, blockIdx.x, gridDim.x / args.n_slices);
