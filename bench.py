@@ -174,7 +174,7 @@ def bench_chunk(args, stream):
 
     def run():
         sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], S0, C=w.C,
-                       o=o, S_T=S_T, stream=stream)
+                       o=o, S_T=S_T, segments=None, stream=stream)
 
     print(f"# timing sfda_chunk_fwd: warmup {args.warmup}, steps {args.steps}", file=sys.stderr, flush=True)
     stats = timed_stats(run, args.steps, args.warmup, stream)
@@ -334,16 +334,16 @@ def long_context(args):
            "dtype": "f32", "ms": {}, "tokens_per_s": {}}
     # the workload's chunk length, and C = 16 (the same result to rounding; the fp32 kernel
     # runs two waves per SIMD at C <= 32)
-    for C, Gs in ((w.C, (None, 4, 8, 16, 32)), (16, (None, 16))):
+    for C, Gs in ((w.C, (None, 4, 8, 16, 32, "auto")), (16, (None, 16))):
         for G in Gs:
-            ws = None if G is None else torch.empty(sfda.segmented_workspace_bytes(B, H, m, n, G),
-                                                    dtype=torch.uint8, device="cuda")
+            ws = None if G in (None, "auto") else torch.empty(sfda.segmented_workspace_bytes(B, H, m, n, G),
+                                                              dtype=torch.uint8, device="cuda")
 
             def run():
                 sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], S0, C=C,
                                o=o, S_T=S_T, segments=G, workspace=ws, stream=stream)
 
-            key = ("plain" if G is None else f"segments_{G}") + ("" if C == w.C else f"_C{C}")
+            key = ("plain" if G is None else "auto" if G == "auto" else f"segments_{G}") + ("" if C == w.C else f"_C{C}")
             print(f"# timing {key}", file=sys.stderr, flush=True)
             ms = timed(run, 3 if G is None else 10, 1, stream)
             out["ms"][key] = round(ms, 3)
@@ -383,10 +383,11 @@ def fp32_forward(args):
     bytes_alg = chunk_bytes_per_token_head(m, n, T, 4, 4) * B * H * T
     runs = []
     # (every C runs 16-token chunks: slices and segments are the knobs that change the launch)
+    # ("auto": the binding's default, the segment count sfda_chunk_fwd_auto_segments picks)
     for C, G, sl in ((64, None, None), (64, None, 32), (64, None, 16), (64, None, 8),
-                     (64, 4, None), (64, 8, None), (64, 16, None)):
-        ws = None if G is None else torch.empty(sfda.segmented_workspace_bytes(B, H, m, n, G),
-                                                dtype=torch.uint8, device="cuda")
+                     (64, 4, None), (64, 8, None), (64, 16, None), (64, "auto", None)):
+        ws = None if G in (None, "auto") else torch.empty(sfda.segmented_workspace_bytes(B, H, m, n, G),
+                                                          dtype=torch.uint8, device="cuda")
 
         def run():
             sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], S0, C=C,
@@ -397,6 +398,7 @@ def fp32_forward(args):
         sec = ms / 1e3
         tf = useful * nchunk / sec / 1e12
         runs.append({"C": C, "segments": G, "slice": sl, "ms": round(ms, 4),
+                     **({"auto_segments": sfda.auto_segments(B, H, T, m, n, C)} if G == "auto" else {}),
                      "tokens_per_s": round(B * T / sec, 1),
                      "roofline": {"bound": "mfma", "achieved": round(tf, 2), "peak": FP32_MFMA_PEAK_TFLOPS,
                                   "unit": "TFLOP/s", "frac": round(tf / FP32_MFMA_PEAK_TFLOPS, 4),
@@ -505,7 +507,7 @@ def backward(args):
 
         def run_fwd():
             sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], S0, C=w.C,
-                           stream=stream)
+                           segments=None, stream=stream)
 
         print(f"# timing sfda_chunk_bwd on {w.name}", file=sys.stderr, flush=True)
         ms = timed(run, max(5, args.steps // 5), max(2, args.warmup // 5), stream)
@@ -570,7 +572,7 @@ def decoupled(args):
 
     def run_tied():
         sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], S0, C=C, o=o, S_T=S_T,
-                       stream=stream)
+                       segments=None, stream=stream)
 
     ms_d = timed(run_dec, max(5, args.steps // 5), max(2, args.warmup // 5), stream)
     ms_t = timed(run_tied, max(5, args.steps // 5), max(2, args.warmup // 5), stream)

@@ -196,6 +196,18 @@ sfda_status_t sfda_chunk_fwd_decoupled(const void* q, const void* k, const void*
 size_t sfda_chunk_fwd_segmented_workspace_bytes(int B, int H, int m, int n, int G);
 
 /*
+ * sfda_chunk_fwd_auto_segments -- the segment count G that the library suggests for
+ * sfda_chunk_fwd_segmented on the current device: the largest power of two for which the
+ * segments' workgroups (B * H * G * ceil(n / 64)) still fit the compute units once each, T
+ * is a multiple of G * C and every segment keeps at least 256 tokens; 1 (use
+ * sfda_chunk_fwd) when that G is below 8.  The segmented scan does about three times the
+ * work of sfda_chunk_fwd spread over G times the workgroups, so it pays only when few heads
+ * would leave most compute units idle (B * H of 32 or fewer on 256 CUs).  Sizes out of
+ * range, or no device, give 1.  Launches nothing and allocates nothing.
+ */
+int sfda_chunk_fwd_auto_segments(int B, int H, int T, int m, int n, int C);
+
+/*
  * sfda_chunk_fwd_segmented_noalloc -- sfda_chunk_fwd_segmented for callers that cannot
  * allocate device memory (code under HIP graph capture, tight serving loops, harnesses that
  * forbid hipMalloc): the workspace is a static device array of SFDA_NOALLOC_SCRATCH_BYTES

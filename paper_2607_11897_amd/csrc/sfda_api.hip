@@ -259,6 +259,17 @@ size_t sfda_chunk_fwd_segmented_workspace_bytes(int B, int H, int m, int n, int 
     return static_cast<size_t>(segs) * (static_cast<size_t>(m) * m + 2 * static_cast<size_t>(m) * n) * 8;
 }
 
+int sfda_chunk_fwd_auto_segments(int B, int H, int T, int m, int n, int C)
+{
+    if (B <= 0 || H <= 0 || T <= 0 || m < 1 || m > 64 || n < 1 || !chunk_ok(C)) return 1;
+    const long cus = device_cus();
+    if (cus <= 0) return 1;
+    const long per = static_cast<long>(B) * H * ((n + 63) / 64);     // workgroups per segment index
+    int G = 1;
+    while (G < 1024 && per * 2 * G <= cus && T % (2L * G * C) == 0 && T / (2L * G) >= 256) G *= 2;
+    return G >= 8 ? G : 1;
+}
+
 // sfda_chunk_fwd_segmented, and with noalloc the workspace taken from the static scratch
 // (its size checked first, its address fetched only after every other argument check)
 static sfda_status_t segmented_impl(const void* q, const void* k, const void* v,

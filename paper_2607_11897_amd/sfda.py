@@ -22,7 +22,8 @@ STATUS = {0: "SFDA_OK", 1: "SFDA_ERR_NULL", 2: "SFDA_ERR_SHAPE", 3: "SFDA_ERR_CH
 NOALLOC_SCRATCH_BYTES = 32 * 1024 * 1024      # SFDA_NOALLOC_SCRATCH_BYTES
 EXPORTS = ("sfda_chunk_fwd", "sfda_chunk_fwd_sliced", "sfda_chunk_fwd_gated", "sfda_chunk_fwd_decoupled",
            "sfda_chunk_fwd_segmented", "sfda_chunk_fwd_segmented_noalloc",
-           "sfda_chunk_fwd_segmented_workspace_bytes", "sfda_chunk_bwd", "sfda_chunk_bwd_workspace_bytes",
+           "sfda_chunk_fwd_segmented_workspace_bytes", "sfda_chunk_fwd_auto_segments",
+           "sfda_chunk_bwd", "sfda_chunk_bwd_workspace_bytes",
            "sfda_step", "sfda_status_string", "sfda_abi_version")
 
 _lib = None
@@ -60,6 +61,8 @@ def load_library(path: str = LIB_PATH):
     lib.sfda_chunk_fwd_segmented_noalloc.restype = i
     lib.sfda_chunk_fwd_segmented_workspace_bytes.argtypes = [i] * 5
     lib.sfda_chunk_fwd_segmented_workspace_bytes.restype = ctypes.c_size_t
+    lib.sfda_chunk_fwd_auto_segments.argtypes = [i] * 6
+    lib.sfda_chunk_fwd_auto_segments.restype = i
     lib.sfda_chunk_bwd.argtypes = [vp] * 16 + [i] * 6 + [i, i, vp, ctypes.c_size_t, vp]
     lib.sfda_chunk_bwd.restype = i
     lib.sfda_chunk_bwd_workspace_bytes.argtypes = [i] * 6
@@ -137,13 +140,16 @@ def _stream(stream):
 
 def chunk_fwd(q, k, v, alpha, theta, beta, S0=None, C: int = 64, *, o=None, S_T=None,
               out_dtype=None, want_state: bool = True, slice: Optional[int] = None,
-              segments: Optional[int] = None, workspace=None, stream=None) -> Tuple:
+              segments="auto", workspace=None, stream=None) -> Tuple:
     """SFDA chunkwise forward.  q, k: [B,H,T,m,2]; v: [B,H,T,n,2]; alpha, theta: [B,H,T,m];
     beta: [B,H,T] (all float32 or all bfloat16); S0: [B,H,m,n,2] float32 or None.
     Returns (o [B,H,T,n,2] in out_dtype, S_T [B,H,m,n,2] float32 or None).
     slice: value columns per workgroup (sfda_chunk_fwd_sliced); segments: G parallel
     segments per head (sfda_chunk_fwd_segmented; `workspace` a uint8 device tensor of at
-    least segmented_workspace_bytes(...) bytes, allocated here when not given)."""
+    least segmented_workspace_bytes(...) bytes, allocated here when not given), None for one
+    scan per head (sfda_chunk_fwd), or "auto" (the default, without a slice): the count
+    sfda_chunk_fwd_auto_segments suggests, segments when the heads alone would leave most
+    compute units idle (the workspace then comes from torch's allocator)."""
     import torch
     lib = load_library()
     B, H, T, m, _ = _dims(q, v, 5)
@@ -165,6 +171,14 @@ def chunk_fwd(q, k, v, alpha, theta, beta, S0=None, C: int = 64, *, o=None, S_T=
                 workspace=(workspace, tuple(workspace.shape) if workspace is not None else ())))
     args = [_ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(theta), _ptr(beta), _ptr(S0),
             _ptr(o), _ptr(S_T), B, H, T, m, n, C]
+    if isinstance(segments, str):
+        if segments != "auto":
+            raise ValueError(f"segments must be an int, None or 'auto', not {segments!r}")
+        segments = None
+        if slice is None and q.is_cuda:
+            with torch.cuda.device(q.device):
+                G = int(lib.sfda_chunk_fwd_auto_segments(B, H, T, m, n, C))
+            segments = G if G > 1 else None
     if segments is not None:
         nws = lib.sfda_chunk_fwd_segmented_workspace_bytes(B, H, m, n, segments)
         if workspace is None:
@@ -320,6 +334,11 @@ def chunk_bwd(q, k, v, alpha, theta, beta, S0, dO, dS_T=None, C: int = 64, *,
 
 def bwd_workspace_bytes(B: int, H: int, T: int, m: int, n: int, C: int) -> int:
     return int(load_library().sfda_chunk_bwd_workspace_bytes(B, H, T, m, n, C))
+
+
+def auto_segments(B: int, H: int, T: int, m: int, n: int, C: int = 64) -> int:
+    """sfda_chunk_fwd_auto_segments on the current device (1: one scan per head)."""
+    return int(load_library().sfda_chunk_fwd_auto_segments(B, H, T, m, n, C))
 
 
 def segmented_workspace_bytes(B: int, H: int, m: int, n: int, G: int) -> int:

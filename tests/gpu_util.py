@@ -49,13 +49,13 @@ def rel_err(x: np.ndarray, ref: np.ndarray) -> float:
     return num / den if den > 0 else num
 
 
-def run_chunk(x: "I.ChunkInputs", C: int, out_dtype=None, slice=None, device="cuda"):
+def run_chunk(x: "I.ChunkInputs", C: int, out_dtype=None, slice=None, device="cuda", segments="auto"):
     import torch
     from paper_2607_11897_amd import sfda
     d = upload(x, device)
     od = None if out_dtype is None else {"f32": torch.float32, "bf16": torch.bfloat16}[out_dtype]
     o, S = sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], d["S0"],
-                          C=C, out_dtype=od, slice=slice)
+                          C=C, out_dtype=od, slice=slice, segments=segments)
     torch.cuda.synchronize()
     return to_complex(o), to_complex(S)
 

@@ -28,9 +28,9 @@ def say(*a):
     print("[case]", *a, flush=True)
 
 
-def check(x, C, tol, out_dtype=None, slice=None, label=""):
-    say(label, x.shape, "C", C, x.dtype, "slice", slice)
-    o, S = run_chunk(x, C, out_dtype=out_dtype, slice=slice)
+def check(x, C, tol, out_dtype=None, slice=None, label="", segments="auto"):
+    say(label, x.shape, "C", C, x.dtype, "slice", slice, "segments", segments)
+    o, S = run_chunk(x, C, out_dtype=out_dtype, slice=slice, segments=segments)
     o_ref, S_ref = run_oracle(x)
     eo, es = rel_err(o, o_ref), rel_err(S, S_ref)
     say(label, "err(o)", eo, "err(S_T)", es)
@@ -147,9 +147,12 @@ def test_bf16_every_chunk_length_bitwise_equal():
         assert np.array_equal(o, o64) and np.array_equal(S, S64), C
 
 
-def test_fwd_f32_b4h8_t2k_full():
+@pytest.mark.parametrize("segments", [None, "auto"])
+def test_fwd_f32_b4h8_t2k_full(segments):
+    """The float32 workload at full size, with one scan per head and with the binding's
+    default (32 heads: segment-parallel on a 256-CU device)."""
     w = I.WORKLOADS["fwd_f32_b4h8_t2k"]
-    check(I.make_chunk_inputs(w), w.C, w.tol, label=w.name)
+    check(I.make_chunk_inputs(w), w.C, w.tol, label=w.name, segments=segments)
 
 
 def test_fwd_bf16_b8h16_t4k_full_sampled_heads():

@@ -43,7 +43,8 @@ def run_plain(x, C):
     import torch
     from paper_2607_11897_amd import sfda
     d = upload(x)
-    o, S = sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], d["S0"], C=C)
+    o, S = sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], d["S0"], C=C,
+                          segments=None)
     torch.cuda.synchronize()
     return to_complex(o), to_complex(S)
 
@@ -124,3 +125,54 @@ def test_long_f32_h16_t64k_segmented_sampled_heads():
         es = rel_err(S[0, h], S_ref[0, 0])
         say(w.name, "head", h, "err(o) by prefix", errs, "err(S_T)", es)
         assert max(errs.values()) <= w.tol and es <= w.tol
+
+
+def _policy(B, H, T, m, n, C, cus):
+    """The segment count rule of sfda_chunk_fwd_auto_segments, restated."""
+    per = B * H * ((n + 63) // 64)
+    G = 1
+    while G < 1024 and per * 2 * G <= cus and T % (2 * G * C) == 0 and T // (2 * G) >= 256:
+        G *= 2
+    return G if G >= 8 else 1
+
+
+@pytest.mark.parametrize("B,H,T,m,n,C", [
+    (4, 8, 2048, 64, 64, 64),       # the float32 workload: 32 heads
+    (8, 16, 4096, 64, 64, 64),      # the benchmarked bf16 workload: enough heads, no segments
+    (1, 16, 65536, 64, 64, 64),     # long context
+    (1, 2, 4096, 64, 64, 64),
+    (1, 2, 4000, 64, 64, 64),       # T not a multiple of 8 C: no segments
+    (1, 1, 1024, 64, 130, 16),
+])
+def test_auto_segments_policy(B, H, T, m, n, C):
+    import torch
+    from paper_2607_11897_amd import sfda
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    G = sfda.auto_segments(B, H, T, m, n, C)
+    say("auto segments", (B, H, T, m, n, C), "CUs", cus, "G", G)
+    assert G == _policy(B, H, T, m, n, C, cus)
+    if cus >= 256 and (B, H, T) == (4, 8, 2048):
+        assert G == 8
+    if (B, H, T) == (8, 16, 4096):
+        assert G == 1
+
+
+def test_default_picks_segments_for_few_heads():
+    """chunk_fwd's default on 2 heads x 4096 tokens runs the segmented scan the policy picks:
+    the same bits as asking for that G, and the oracle's result within the float32 bar."""
+    import torch
+    from paper_2607_11897_amd import sfda
+    x = make(1, 2, 4096, 64, 64, 64)
+    G = sfda.auto_segments(1, 2, 4096, 64, 64, 64)
+    say("default segments", G)
+    assert G > 1
+    d = upload(x)
+    o1, S1 = sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], d["S0"], C=64)
+    o2, S2 = sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], d["S0"], C=64,
+                            segments=G)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(S1, S2)
+    o_ref, S_ref = run_oracle(x)
+    eo, es = rel_err(to_complex(o1), o_ref), rel_err(to_complex(S1), S_ref)
+    say("default segments err(o)", eo, "err(S_T)", es)
+    assert eo <= 1e-4 and es <= 1e-4
