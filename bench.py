@@ -15,8 +15,9 @@ Also reported on the same JSON line:
                 intervals between HIP events recorded on the launch stream
   cpu_baseline  the CPU oracle (complex128 recurrence) on a bounded sample of the workload,
                 on every host thread and on one thread, with the CPU model
-The decode step is timed first; its untimed settle phase (about 0.3 s of decode steps)
-brings the GPU to steady clocks before the chunk kernel's warm-up and timed launches.
+Each kernel runs an untimed settle phase (about 0.3 s of launches) before its W warm-up
+and K timed launches: the GPU's clocks drop while the host generates the next workload's
+inputs, and a short run (the driver's 20 steps after 5) would otherwise time the ramp.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--only chunk|decode]
        [--no-cpu-baseline] [--mode copy|rmw|long|gated|bwd|dec|f32]   (copy: a plain device copy, for counter
@@ -176,7 +177,9 @@ def bench_chunk(args, stream):
         sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], S0, C=w.C,
                        o=o, S_T=S_T, segments=None, stream=stream)
 
-    print(f"# timing sfda_chunk_fwd: warmup {args.warmup}, steps {args.steps}", file=sys.stderr, flush=True)
+    print(f"# timing sfda_chunk_fwd: {SETTLE_S} s of untimed launches, warmup {args.warmup}, "
+          f"steps {args.steps}", file=sys.stderr, flush=True)
+    settle_clocks(run, SETTLE_S, stream)
     stats = timed_stats(run, args.steps, args.warmup, stream)
     ms = stats["mean"]
     units = B * H * T
@@ -683,8 +686,6 @@ def main():
         out["decode"] = bench_decode(args, stream)
         print(json.dumps(out), flush=True)
         return
-    # the decode step runs first: its untimed settle phase brings the GPU to steady clocks
-    # before the chunk kernel's W warm-up and K timed launches
     if args.only is None:
         out["decode"] = bench_decode(args, stream)
     r = bench_chunk(args, stream)
