@@ -339,7 +339,7 @@ def long_context(args):
     # runs two waves per SIMD at C <= 32)
     for C, Gs in ((w.C, (None, 4, 8, 16, 32, "auto")), (16, (None, 16))):
         for G in Gs:
-            ws = None if G in (None, "auto") else torch.empty(sfda.segmented_workspace_bytes(B, H, m, n, G),
+            ws = None if G in (None, "auto") else torch.empty(sfda.segmented_workspace_bytes(B, H, T, m, n, G),
                                                               dtype=torch.uint8, device="cuda")
 
             def run():
@@ -389,7 +389,7 @@ def fp32_forward(args):
     # ("auto": the binding's default, the segment count sfda_chunk_fwd_auto_segments picks)
     for C, G, sl in ((64, None, None), (64, None, 32), (64, None, 16), (64, None, 8),
                      (64, 4, None), (64, 8, None), (64, 16, None), (64, "auto", None)):
-        ws = None if G in (None, "auto") else torch.empty(sfda.segmented_workspace_bytes(B, H, m, n, G),
+        ws = None if G in (None, "auto") else torch.empty(sfda.segmented_workspace_bytes(B, H, T, m, n, G),
                                                           dtype=torch.uint8, device="cuda")
 
         def run():

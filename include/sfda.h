@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define SFDA_ABI_VERSION 2
+#define SFDA_ABI_VERSION 3
 
 /* Element types and status codes are plain ints (the names below are their values), so
  * any value a caller passes is well defined: an unknown dtype is SFDA_ERR_DTYPE, an unknown
@@ -177,35 +177,40 @@ sfda_status_t sfda_chunk_fwd_decoupled(const void* q, const void* k, const void*
  * sequences, where one workgroup per head leaves most of the GPU idle).  It uses the
  * exact affine law of a stretch of tokens (Thm 4.4: S_end = P S_in + B, P the product of
  * the stretch's transitions, B its write from the zero state) composed along the segments
- * (Lemma A.2, the boundary-state scan of Thm 6.1 at segment granularity): every segment's
- * P_g (final state from S0 = I with v = 0) and B_g (final state from S0 = 0) come from
- * the chunk kernel, a fold gives S_in[g + 1] = P_g S_in[g] + B_g and S_T = S_in[G], and
- * a last chunk pass writes o from the exact incoming states.  About three times the work
- * of sfda_chunk_fwd, spread over G times as many workgroups; results agree with it to
- * rounding.
+ * (Lemma A.2, the boundary-state scan of Thm 6.1 at segment granularity): chunk passes give
+ * every segment's P_g (final state from S0 = I with v = 0) and B_g (final state from
+ * S0 = 0), and a fold gives S_in[g + 1] = P_g S_in[g] + B_g and S_T = S_in[G].  With
+ * float32 inputs the same two passes also give the readouts X_t = P_t^* q_t and the
+ * zero-state outputs o0_t, and a join writes o_t = o0_t + S_in^* X_t (the same law token by
+ * token; a bfloat16 o is then rounded twice); with bfloat16 inputs a third pass writes o
+ * from the exact incoming states.  Two or three times the scan work of sfda_chunk_fwd,
+ * spread over G times as many workgroups; results agree with it to rounding.
  *   Arguments and errors as sfda_chunk_fwd, plus:
  *   G >= 1 with T a multiple of G * C (SFDA_ERR_SHAPE otherwise; T == 0 is as
  *   sfda_chunk_fwd).
  *   workspace : device memory of at least sfda_chunk_fwd_segmented_workspace_bytes(B, H,
- *               m, n, G) bytes (SFDA_ERR_SHAPE if smaller, SFDA_ERR_NULL if NULL),
- *               16-byte aligned, not overlapping any other argument (SFDA_ERR_ALIAS);
- *               no initial contents needed.  Holds, per segment, P_g (m x m), B_g and
- *               the incoming state (m x n), complex float32.
+ *               T, m, n, G, in_dtype) bytes (SFDA_ERR_SHAPE if smaller, SFDA_ERR_NULL if
+ *               NULL), 16-byte aligned, not overlapping any other argument
+ *               (SFDA_ERR_ALIAS); no initial contents needed.  Holds, per segment, P_g
+ *               (m x m), B_g and the incoming state (m x n), and with float32 inputs per
+ *               token X_t (m), complex float32 (0 for sizes or a dtype out of range).
  *   S_T == S0 (in place) is allowed.
  */
-size_t sfda_chunk_fwd_segmented_workspace_bytes(int B, int H, int m, int n, int G);
+size_t sfda_chunk_fwd_segmented_workspace_bytes(int B, int H, int T, int m, int n, int G,
+                                                sfda_dtype_t in_dtype);
 
 /*
  * sfda_chunk_fwd_auto_segments -- the segment count G that the library suggests for
- * sfda_chunk_fwd_segmented on the current device: the largest power of two for which the
- * segments' workgroups (B * H * G * ceil(n / 64)) still fit the compute units once each, T
- * is a multiple of G * C and every segment keeps at least 256 tokens; 1 (use
- * sfda_chunk_fwd) when that G is below 8.  The segmented scan does about three times the
- * work of sfda_chunk_fwd spread over G times the workgroups, so it pays only when few heads
- * would leave most compute units idle (B * H of 32 or fewer on 256 CUs).  Sizes out of
- * range, or no device, give 1.  Launches nothing and allocates nothing.
+ * sfda_chunk_fwd_segmented on the current device and input dtype: the largest power of two
+ * for which the segments' workgroups (B * H * G * ceil(n / 64)) still fit the compute units
+ * once each, T is a multiple of G * C and every segment keeps at least 256 tokens; 1 (use
+ * sfda_chunk_fwd) when that G is below 4 for float32 inputs or below 8 for bfloat16 ones.
+ * The segmented scan does two (float32) or three (bfloat16) times the scan work of
+ * sfda_chunk_fwd spread over G times the workgroups, so it pays only when few heads would
+ * leave most compute units idle.  Sizes or a dtype out of range, or no device, give 1.
+ * Launches nothing and allocates nothing.
  */
-int sfda_chunk_fwd_auto_segments(int B, int H, int T, int m, int n, int C);
+int sfda_chunk_fwd_auto_segments(int B, int H, int T, int m, int n, int C, sfda_dtype_t in_dtype);
 
 /*
  * sfda_chunk_fwd_segmented_noalloc -- sfda_chunk_fwd_segmented for callers that cannot

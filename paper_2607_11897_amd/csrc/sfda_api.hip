@@ -252,22 +252,28 @@ sfda_status_t sfda_chunk_fwd_decoupled(const void* q, const void* k, const void*
     return e == hipSuccess ? SFDA_OK : SFDA_ERR_HIP;
 }
 
-size_t sfda_chunk_fwd_segmented_workspace_bytes(int B, int H, int m, int n, int G)
+size_t sfda_chunk_fwd_segmented_workspace_bytes(int B, int H, int T, int m, int n, int G,
+                                                sfda_dtype_t in_dtype)
 {
-    if (B <= 0 || H <= 0 || m < 1 || m > 64 || n < 1 || G < 1) return 0;
-    const long segs = static_cast<long>(B) * H * G;
-    return static_cast<size_t>(segs) * (static_cast<size_t>(m) * m + 2 * static_cast<size_t>(m) * n) * 8;
+    if (B <= 0 || H <= 0 || T < 0 || m < 1 || m > 64 || n < 1 || G < 1 || !dtype_ok(in_dtype)) return 0;
+    const size_t segs = static_cast<size_t>(B) * H * G, heads = static_cast<size_t>(B) * H;
+    // per segment P_g (m x m), B_g and S_in (m x n); with float32 inputs per head and token
+    // X_t (m)
+    const size_t xt = in_dtype == SFDA_F32 ? heads * static_cast<size_t>(T) * m : 0;
+    return (segs * (static_cast<size_t>(m) * m + 2 * static_cast<size_t>(m) * n) + xt) * 8;
 }
 
-int sfda_chunk_fwd_auto_segments(int B, int H, int T, int m, int n, int C)
+int sfda_chunk_fwd_auto_segments(int B, int H, int T, int m, int n, int C, sfda_dtype_t in_dtype)
 {
-    if (B <= 0 || H <= 0 || T <= 0 || m < 1 || m > 64 || n < 1 || !chunk_ok(C)) return 1;
+    if (B <= 0 || H <= 0 || T <= 0 || m < 1 || m > 64 || n < 1 || !chunk_ok(C) || !dtype_ok(in_dtype))
+        return 1;
     const long cus = device_cus();
     if (cus <= 0) return 1;
     const long per = static_cast<long>(B) * H * ((n + 63) / 64);     // workgroups per segment index
     int G = 1;
     while (G < 1024 && per * 2 * G <= cus && T % (2L * G * C) == 0 && T / (2L * G) >= 256) G *= 2;
-    return G >= 8 ? G : 1;
+    // the segmented scan repeats the scan work twice (float32) or three times (bfloat16)
+    return G >= (in_dtype == SFDA_F32 ? 4 : 8) ? G : 1;
 }
 
 // sfda_chunk_fwd_segmented, and with noalloc the workspace taken from the static scratch
@@ -290,7 +296,7 @@ static sfda_status_t segmented_impl(const void* q, const void* k, const void* v,
     const long BH = static_cast<long>(B) * H;
     if (BH * G > 0x7FFFFFFFL) return SFDA_ERR_SHAPE;
     if (noalloc) {
-        if (sfda_chunk_fwd_segmented_workspace_bytes(B, H, m, n, G) > SFDA_NOALLOC_SCRATCH_BYTES)
+        if (sfda_chunk_fwd_segmented_workspace_bytes(B, H, T, m, n, G, in_dtype) > SFDA_NOALLOC_SCRATCH_BYTES)
             return SFDA_ERR_SCRATCH;
         const sfda_status_t st0 = chunk_fwd_impl(q, k, v, alpha, theta, beta, S0, o, S_T, B, H, T,
                                                  m, n, C, in_dtype, out_dtype, stream, slice_n,
@@ -302,7 +308,7 @@ static sfda_status_t segmented_impl(const void* q, const void* k, const void* v,
     }
     if (!workspace) return SFDA_ERR_NULL;
     if (!aligned16(workspace)) return SFDA_ERR_ALIGN;
-    const size_t need = sfda_chunk_fwd_segmented_workspace_bytes(B, H, m, n, G);
+    const size_t need = sfda_chunk_fwd_segmented_workspace_bytes(B, H, T, m, n, G, in_dtype);
     if (workspace_bytes < need) return SFDA_ERR_SHAPE;
     // validate the buffers the way sfda_chunk_fwd does (nothing is launched on error)
     {
@@ -326,24 +332,39 @@ static sfda_status_t segmented_impl(const void* q, const void* k, const void* v,
     float* P = static_cast<float*>(workspace);                      // [segs][m][m]
     float* Bs = P + segs * m * m * 2;                               // [segs][m][n]
     float* Sin = Bs + segs * static_cast<long>(m) * n * 2;          // [segs][m][n]
+    float* X = Sin + segs * static_cast<long>(m) * n * 2;           // [segs][T / G][m], float32 inputs
     // [B, H, T, .] with T = G * Ts is [B*H*G, Ts, .]: each segment runs as a head
+    const int Ts = T / G;
+    // float32 inputs: the outputs come from the zero-state pass and a join (o0 + S_in^* X),
+    // cheaper than a third pass of the latency-bound float32 scan; bfloat16 inputs: a third
+    // pass of the pipelined kernel from the incoming states (cheaper than writing X in
+    // float32 and the join)
+    const bool join = in_dtype == SFDA_F32 && o != nullptr;
     sfda::ChunkLaunch L;
     L.q = q; L.k = k; L.alpha = alpha; L.theta = theta; L.beta = beta;
-    L.B = static_cast<int>(segs); L.H = 1; L.T = T / G; L.m = m; L.C = C;
+    L.B = static_cast<int>(segs); L.H = 1; L.T = Ts; L.m = m; L.C = C;
     L.in_bf16 = in_dtype == SFDA_BF16;
-    L.out_bf16 = out_dtype == SFDA_BF16;
-    // P_g: S0 = I, v = 0 (in place on the identity), no output
+    // P_g (and with the join X_t = P_t^* q_t, the m-column float32 output): S0 = I, v = 0,
+    // in place on the identity
     if (sfda::launch_identity(P, segs, m, st) != hipSuccess) return SFDA_ERR_HIP;
-    L.v = nullptr; L.S0 = P; L.S_T = P; L.o = nullptr; L.n = m; L.slice = ((m + 7) / 8) * 8;
+    L.v = nullptr; L.S0 = P; L.S_T = P; L.o = join ? X : nullptr; L.out_bf16 = false;
+    L.n = m; L.slice = ((m + 7) / 8) * 8;
     if (sfda::launch_chunk(L, st) != hipSuccess) return SFDA_ERR_HIP;
-    // B_g: S0 = 0, no output
-    L.v = v; L.S0 = nullptr; L.S_T = Bs; L.o = nullptr; L.n = n; L.slice = slice_n;
+    // B_g (and with the join the zero-state outputs o0, into o)
+    L.v = v; L.S0 = nullptr; L.S_T = Bs; L.o = join ? o : nullptr; L.out_bf16 = out_dtype == SFDA_BF16;
+    L.n = n; L.slice = slice_n;
     if (sfda::launch_chunk(L, st) != hipSuccess) return SFDA_ERR_HIP;
     // incoming states and S_T
     if (sfda::launch_fold(P, Bs, Sin, S0, S_T, BH, G, m, n, st) != hipSuccess) return SFDA_ERR_HIP;
-    // outputs from the exact incoming states
-    L.S0 = Sin; L.S_T = nullptr; L.o = o;
-    if (sfda::launch_chunk(L, st) != hipSuccess) return SFDA_ERR_HIP;
+    if (join) {
+        // o = o0 + S_in^* X (the affine law of each segment, token by token)
+        if (sfda::launch_join(X, Sin, o, out_dtype == SFDA_BF16, segs, Ts, m, n, st) != hipSuccess)
+            return SFDA_ERR_HIP;
+    } else {
+        // outputs from the exact incoming states
+        L.S0 = Sin; L.S_T = nullptr; L.o = o;
+        if (sfda::launch_chunk(L, st) != hipSuccess) return SFDA_ERR_HIP;
+    }
     return SFDA_OK;
 }
 

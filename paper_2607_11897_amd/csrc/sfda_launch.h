@@ -65,8 +65,11 @@ hipError_t launch_chunk_decoupled(const ChunkLaunch& L, hipStream_t st);   // C 
 // reverse adjoint scan (A) in one launch, then the per-chunk gradient pass
 hipError_t launch_bwd_scans(const ChunkLaunch& F, const ChunkLaunch& A, hipStream_t st);
 hipError_t launch_chunk_grad(const GradLaunch& L, hipStream_t st);
-// segment-parallel scan: identity fill and the fold of the segments' affine maps
+// segment-parallel scan: identity fill, the fold of the segments' affine maps and the join of
+// the outputs (o += S_in^* X)
 hipError_t launch_identity(float* P, long count, int m, hipStream_t st);
+hipError_t launch_join(const float* X, const float* Sin, void* o, bool out_bf16, long segs,
+                       int Ts, int m, int n, hipStream_t st);
 hipError_t launch_fold(const float* P, const float* Bs, float* Sin, const float* S0, float* S_T,
                        long heads, int G, int m, int n, hipStream_t st);
 

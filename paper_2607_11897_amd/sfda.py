@@ -59,9 +59,9 @@ def load_library(path: str = LIB_PATH):
     lib.sfda_chunk_fwd_segmented.restype = i
     lib.sfda_chunk_fwd_segmented_noalloc.argtypes = [vp] * 9 + [i] * 7 + [i, i, vp]
     lib.sfda_chunk_fwd_segmented_noalloc.restype = i
-    lib.sfda_chunk_fwd_segmented_workspace_bytes.argtypes = [i] * 5
+    lib.sfda_chunk_fwd_segmented_workspace_bytes.argtypes = [i] * 7
     lib.sfda_chunk_fwd_segmented_workspace_bytes.restype = ctypes.c_size_t
-    lib.sfda_chunk_fwd_auto_segments.argtypes = [i] * 6
+    lib.sfda_chunk_fwd_auto_segments.argtypes = [i] * 7
     lib.sfda_chunk_fwd_auto_segments.restype = i
     lib.sfda_chunk_bwd.argtypes = [vp] * 16 + [i] * 6 + [i, i, vp, ctypes.c_size_t, vp]
     lib.sfda_chunk_bwd.restype = i
@@ -177,10 +177,10 @@ def chunk_fwd(q, k, v, alpha, theta, beta, S0=None, C: int = 64, *, o=None, S_T=
         segments = None
         if slice is None and q.is_cuda:
             with torch.cuda.device(q.device):
-                G = int(lib.sfda_chunk_fwd_auto_segments(B, H, T, m, n, C))
+                G = int(lib.sfda_chunk_fwd_auto_segments(B, H, T, m, n, C, in_code))
             segments = G if G > 1 else None
     if segments is not None:
-        nws = lib.sfda_chunk_fwd_segmented_workspace_bytes(B, H, m, n, segments)
+        nws = lib.sfda_chunk_fwd_segmented_workspace_bytes(B, H, T, m, n, segments, in_code)
         if workspace is None:
             workspace = torch.empty(max(nws, 1), dtype=torch.uint8, device=q.device)
         st = lib.sfda_chunk_fwd_segmented(*args, segments, in_code, _dtype_code(o), _ptr(workspace),
@@ -336,13 +336,17 @@ def bwd_workspace_bytes(B: int, H: int, T: int, m: int, n: int, C: int) -> int:
     return int(load_library().sfda_chunk_bwd_workspace_bytes(B, H, T, m, n, C))
 
 
-def auto_segments(B: int, H: int, T: int, m: int, n: int, C: int = 64) -> int:
-    """sfda_chunk_fwd_auto_segments on the current device (1: one scan per head)."""
-    return int(load_library().sfda_chunk_fwd_auto_segments(B, H, T, m, n, C))
+def auto_segments(B: int, H: int, T: int, m: int, n: int, C: int = 64, dtype: str = "f32") -> int:
+    """sfda_chunk_fwd_auto_segments on the current device (1: one scan per head); dtype: the
+    inputs' ("f32" or "bf16")."""
+    code = {"f32": SFDA_F32, "bf16": SFDA_BF16}[dtype]
+    return int(load_library().sfda_chunk_fwd_auto_segments(B, H, T, m, n, C, code))
 
 
-def segmented_workspace_bytes(B: int, H: int, m: int, n: int, G: int) -> int:
-    return int(load_library().sfda_chunk_fwd_segmented_workspace_bytes(B, H, m, n, G))
+def segmented_workspace_bytes(B: int, H: int, T: int, m: int, n: int, G: int, dtype: str = "f32") -> int:
+    """Workspace of sfda_chunk_fwd_segmented; dtype: the inputs' ("f32" or "bf16")."""
+    code = {"f32": SFDA_F32, "bf16": SFDA_BF16}[dtype]
+    return int(load_library().sfda_chunk_fwd_segmented_workspace_bytes(B, H, T, m, n, G, code))
 
 
 def step(q, k, v, alpha, theta, beta, S, *, o=None, out_dtype=None, stream=None):

@@ -37,7 +37,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_abi_version_and_status_strings(lib):
-    assert lib.sfda_abi_version() == 2
+    assert lib.sfda_abi_version() == 3
     for s in range(9):
         assert len(lib.sfda_status_string(s)) > 0
     assert lib.sfda_status_string(99) == b"unknown status"
@@ -88,10 +88,16 @@ def seg(lib, T=64, G=2, C=16, ws=A * 20, nws=1 << 40, q=P[0], B=1, H=1, m=8, n=8
 
 
 def test_segmented_workspace_size(lib):
-    # per segment: P_g (m x m) + B_g and the incoming state (m x n), complex float32
-    assert lib.sfda_chunk_fwd_segmented_workspace_bytes(2, 3, 64, 48, 4) == 24 * (64 * 64 + 2 * 64 * 48) * 8
-    assert lib.sfda_chunk_fwd_segmented_workspace_bytes(1, 1, 65, 8, 1) == 0
-    assert lib.sfda_chunk_fwd_segmented_workspace_bytes(1, 1, 8, 8, 0) == 0
+    # per segment: P_g (m x m) + B_g and the incoming state (m x n); per head and token X_t
+    # (m)
+    # (float32 inputs), complex float32
+    assert lib.sfda_chunk_fwd_segmented_workspace_bytes(2, 3, 256, 64, 48, 4, 0) == \
+        (24 * (64 * 64 + 2 * 64 * 48) + 6 * 256 * 64) * 8
+    assert lib.sfda_chunk_fwd_segmented_workspace_bytes(2, 3, 256, 64, 48, 4, 1) == 24 * (64 * 64 + 2 * 64 * 48) * 8
+    assert lib.sfda_chunk_fwd_segmented_workspace_bytes(1, 1, 64, 65, 8, 1, 0) == 0
+    assert lib.sfda_chunk_fwd_segmented_workspace_bytes(1, 1, 64, 8, 8, 0, 0) == 0
+    assert lib.sfda_chunk_fwd_segmented_workspace_bytes(1, 1, -1, 8, 8, 1, 0) == 0
+    assert lib.sfda_chunk_fwd_segmented_workspace_bytes(1, 1, 64, 8, 8, 1, 2) == 0
 
 
 def noalloc(lib, T=64, G=2, C=16, q=P[0], B=1, H=1, m=8, n=8, din=0):
@@ -107,7 +113,7 @@ def test_noalloc_argument_errors(lib):
     assert noalloc(lib, C=8) == 3 and noalloc(lib, din=3) == 4
     assert noalloc(lib, B=0, q=None) == 0
     # 64 heads x 8 segments x (64 x 64 + 2 x 64 x 64) complex float32 = 48 MiB > 32 MiB
-    assert lib.sfda_chunk_fwd_segmented_workspace_bytes(1, 64, 64, 64, 8) > (32 << 20)
+    assert lib.sfda_chunk_fwd_segmented_workspace_bytes(1, 64, 8 * 16, 64, 64, 8, 0) > (32 << 20)
     assert noalloc(lib, T=8 * 16, G=8, H=64, m=64, n=64) == 8
     assert lib.sfda_status_string(8).startswith(b"the call needs more workspace")
 

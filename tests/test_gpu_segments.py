@@ -127,30 +127,32 @@ def test_long_f32_h16_t64k_segmented_sampled_heads():
         assert max(errs.values()) <= w.tol and es <= w.tol
 
 
-def _policy(B, H, T, m, n, C, cus):
+def _policy(B, H, T, m, n, C, cus, dtype):
     """The segment count rule of sfda_chunk_fwd_auto_segments, restated."""
     per = B * H * ((n + 63) // 64)
     G = 1
     while G < 1024 and per * 2 * G <= cus and T % (2 * G * C) == 0 and T // (2 * G) >= 256:
         G *= 2
-    return G if G >= 8 else 1
+    return G if G >= (4 if dtype == "f32" else 8) else 1
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("B,H,T,m,n,C", [
     (4, 8, 2048, 64, 64, 64),       # the float32 workload: 32 heads
     (8, 16, 4096, 64, 64, 64),      # the benchmarked bf16 workload: enough heads, no segments
     (1, 16, 65536, 64, 64, 64),     # long context
+    (4, 16, 4096, 64, 64, 64),      # 64 heads: G = 4, segments for float32 only
     (1, 2, 4096, 64, 64, 64),
     (1, 2, 4000, 64, 64, 64),       # T not a multiple of 8 C: no segments
     (1, 1, 1024, 64, 130, 16),
 ])
-def test_auto_segments_policy(B, H, T, m, n, C):
+def test_auto_segments_policy(B, H, T, m, n, C, dtype):
     import torch
     from paper_2607_11897_amd import sfda
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    G = sfda.auto_segments(B, H, T, m, n, C)
-    say("auto segments", (B, H, T, m, n, C), "CUs", cus, "G", G)
-    assert G == _policy(B, H, T, m, n, C, cus)
+    G = sfda.auto_segments(B, H, T, m, n, C, dtype)
+    say("auto segments", (B, H, T, m, n, C), dtype, "CUs", cus, "G", G)
+    assert G == _policy(B, H, T, m, n, C, cus, dtype)
     if cus >= 256 and (B, H, T) == (4, 8, 2048):
         assert G == 8
     if (B, H, T) == (8, 16, 4096):
