@@ -20,7 +20,8 @@ namespace seg {
 
 constexpr int NT = 256;
 constexpr int MP = 64;      // state rows (m <= 64)
-constexpr int CB = 16;      // value columns per workgroup in the fold
+constexpr int CB = 8;       // value columns per workgroup in the fold
+constexpr int CPT = CB / 4; // of them per thread
 
 // P[s] = I (m x m complex), s < count
 __global__ __launch_bounds__(NT) void identity_kernel(float* P, long count, int m)
@@ -52,16 +53,16 @@ __global__ __launch_bounds__(NT) void fold_kernel(const float* __restrict__ P,
     const int j0 = static_cast<int>(blockIdx.x - h * ncb) * CB;
     const int tid = threadIdx.x;
     const int i = tid >> 2;             // state row
-    const int jq = (tid & 3) * 4;       // first of this thread's 4 columns in the block
+    const int jq = (tid & 3) * CPT;     // first of this thread's CPT columns in the block
     const long mn = static_cast<long>(m) * n;
     const float2* P2 = reinterpret_cast<const float2*>(P);
     const float2* B2 = reinterpret_cast<const float2*>(Bs);
     float2* Sin2 = reinterpret_cast<float2*>(Sin);
 
     auto col_ok = [&](int c) { return j0 + jq + c < n; };
-    float2 s[4];
+    float2 s[CPT];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
+    for (int c = 0; c < CPT; ++c) {
         s[c] = make_float2(0.f, 0.f);
         if (S0 != nullptr && i < m && col_ok(c))
             s[c] = reinterpret_cast<const float2*>(S0)[h * mn + static_cast<long>(i) * n + j0 + jq + c];
@@ -86,7 +87,7 @@ __global__ __launch_bounds__(NT) void fold_kernel(const float* __restrict__ P,
         // the state entering segment gi
         if (i < m) {
 #pragma unroll
-            for (int c = 0; c < 4; ++c)
+            for (int c = 0; c < CPT; ++c)
                 if (col_ok(c)) Sin2[seg * mn + static_cast<long>(i) * n + j0 + jq + c] = s[c];
         }
 #pragma unroll
@@ -97,21 +98,21 @@ __global__ __launch_bounds__(NT) void fold_kernel(const float* __restrict__ P,
         __syncthreads();
         if (gi + 1 < G) fetch_p(seg + 1);
         // row i of P_gi S + B_gi
-        float2 acc[4];
+        float2 acc[CPT];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) acc[c] = make_float2(0.f, 0.f);
+        for (int c = 0; c < CPT; ++c) acc[c] = make_float2(0.f, 0.f);
         if (i < m) {
             for (int l = 0; l < m; ++l) {
                 const float2 p = Ps[i][l];
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
+                for (int c = 0; c < CPT; ++c) {
                     const float2 x = S[l][jq + c];
                     acc[c].x = __builtin_fmaf(p.x, x.x, __builtin_fmaf(-p.y, x.y, acc[c].x));
                     acc[c].y = __builtin_fmaf(p.x, x.y, __builtin_fmaf(p.y, x.x, acc[c].y));
                 }
             }
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
+            for (int c = 0; c < CPT; ++c) {
                 if (!col_ok(c)) continue;
                 const float2 b = B2[seg * mn + static_cast<long>(i) * n + j0 + jq + c];
                 acc[c].x += b.x;
@@ -120,7 +121,7 @@ __global__ __launch_bounds__(NT) void fold_kernel(const float* __restrict__ P,
         }
         __syncthreads();                // every row of S and of P_gi read
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
+        for (int c = 0; c < CPT; ++c) {
             s[c] = acc[c];
             S[i][jq + c] = acc[c];
         }
@@ -128,7 +129,7 @@ __global__ __launch_bounds__(NT) void fold_kernel(const float* __restrict__ P,
     }
     if (S_T != nullptr && i < m) {
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
+        for (int c = 0; c < CPT; ++c)
             if (col_ok(c)) reinterpret_cast<float2*>(S_T)[h * mn + static_cast<long>(i) * n + j0 + jq + c] = s[c];
     }
 }
