@@ -13,6 +13,7 @@ Also reported on the same JSON line:
   decode        the sfda_step kernel on the state [512, 32, 64, 64] complex fp32 (HBM-bound)
   launch_ms     mean (= ms_per_step), median, minimum and maximum of the K per-launch
                 intervals between HIP events recorded on the launch stream
+  launch_ms_c128  the same statistics for the same call with C = 128 (K launches after W)
   cpu_baseline  the CPU oracle (complex128 recurrence) on a bounded sample of the workload,
                 on every host thread and on one thread, with the CPU model
 Each kernel runs an untimed settle phase (about 0.3 s of launches) before its W warm-up
@@ -182,6 +183,14 @@ def bench_chunk(args, stream):
     settle_clocks(run, SETTLE_S, stream)
     stats = timed_stats(run, args.steps, args.warmup, stream)
     ms = stats["mean"]
+
+    # the same launch with C = 128 (the kernel's 16-token blocking does not depend on C, and
+    # neither does the result: Thm 6.1), reported beside the C = 64 line
+    def run128():
+        sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], S0, C=128,
+                       o=o, S_T=S_T, segments=None, stream=stream)
+
+    stats128 = timed_stats(run128, args.steps, args.warmup, stream)
     units = B * H * T
     bytes_alg = chunk_bytes_per_token_head(m, n, T, 2, 2) * units
     # the kernel evaluates 16-token blocks whatever C is (the result does not depend on C):
@@ -195,6 +204,7 @@ def bench_chunk(args, stream):
     return dict(
         w=w, ms=ms, tokens_per_s=B * T / sec, x=x,
         launch_ms={k: round(v, 4) for k, v in stats.items()},
+        launch_ms_c128={k: round(v, 4) for k, v in stats128.items()},
         roofline={"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                   "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                   "traffic": traffic,
@@ -698,6 +708,7 @@ def main():
         "config": {"workload": w.name, "B": w.B, "H": w.H, "T": w.T, "d_k": 2 * w.m, "d_v": 2 * w.n,
                    "m_complex": w.m, "n_complex": w.n, "C": w.C, "state": "fp32", "accum": "fp32"},
         "launch_ms": r["launch_ms"],
+        "launch_ms_c128": r["launch_ms_c128"],
         "roofline": r["roofline"],
     }
     if "decode" in out:
