@@ -301,6 +301,28 @@ sfda_status_t sfda_step(const void* q, const void* k, const void* v,
 /* Static, human-readable text for a status code. */
 const char* sfda_status_string(sfda_status_t s);
 
+/*
+ * sfda_chunk_solve_monitor -- the conditioning watch that Prop. 6.4 asks for (its bound
+ * ||M||_2 <= 1 / (1 - eta) holds when ||L||_2 <= eta < 1, which the gates do not enforce):
+ * for every 16-token block of every head (the blocking of the chunk kernels), the
+ * triangular solve that forms N = (I + D_beta L')^{-1} is repeated exactly as the float32
+ * path's kernels do it (same load stage, Gram products and substitution; with bfloat16
+ * inputs the Gram products take bfloat16 operands, as in the backward's scans), and
+ *   residual[b, h, blk] = max_ij |((I + D_beta L') N - I)_ij|   (on the L' it used)
+ *   lnorm[b, h, blk]    = ||D_beta L'||_F   (an upper bound of the spectral norm)
+ * are written, float32, [B, H, ceil(T / 16)].  L'[t, j] = k_t^* diag(g_t / g_j) k_j for j < t
+ * inside the block (the chunk relations of Thm 4.2).  A block outside the decay range of
+ * sfda_chunk_fwd gives NaN.
+ *   k, alpha, theta, beta: as sfda_chunk_fwd's (device, in_dtype); residual, lnorm: device
+ *   float32 (either may be NULL, not both; SFDA_ERR_NULL), 16-byte aligned, not
+ *   overlapping the inputs or each other (SFDA_ERR_ALIAS).  Sizes as sfda_chunk_fwd (m in
+ *   1..64); B, H or T == 0 is a no-op.
+ */
+sfda_status_t sfda_chunk_solve_monitor(const void* k, const void* alpha, const void* theta,
+                                       const void* beta, float* residual, float* lnorm, int B,
+                                       int H, int T, int m, sfda_dtype_t in_dtype,
+                                       sfda_stream_t stream);
+
 /* SFDA_ABI_VERSION of the built library. */
 int sfda_abi_version(void);
 

@@ -486,6 +486,39 @@ sfda_status_t sfda_chunk_bwd(const void* q, const void* k, const void* v, const 
     return SFDA_OK;
 }
 
+sfda_status_t sfda_chunk_solve_monitor(const void* k, const void* alpha, const void* theta,
+                                       const void* beta, float* residual, float* lnorm, int B,
+                                       int H, int T, int m, sfda_dtype_t in_dtype,
+                                       sfda_stream_t stream)
+{
+    if (!dtype_ok(in_dtype)) return SFDA_ERR_DTYPE;
+    if (B < 0 || H < 0 || T < 0 || m < 1 || m > 64) return SFDA_ERR_SHAPE;
+    const long BH = static_cast<long>(B) * H, nb = (static_cast<long>(T) + 15) / 16;
+    if (BH * nb > 0x7FFFFFFFL) return SFDA_ERR_SHAPE;
+    if (BH == 0 || T == 0) return SFDA_OK;
+    if (!k || !alpha || !theta || !beta || (!residual && !lnorm)) return SFDA_ERR_NULL;
+    const void* ptrs[] = {k, alpha, theta, beta, residual, lnorm};
+    for (const void* p : ptrs)
+        if (p && !aligned16(p)) return SFDA_ERR_ALIGN;
+    const long ei = esize(in_dtype), BHT = BH * T;
+    const Range ins[] = {range_of(k, BHT * m * 2 * ei), range_of(alpha, BHT * m * ei),
+                         range_of(theta, BHT * m * ei), range_of(beta, BHT * ei)};
+    const Range outs[] = {range_of(residual, BH * nb * 4), range_of(lnorm, BH * nb * 4)};
+    for (const Range& o : outs)
+        for (const Range& r : ins)
+            if (overlap(o, r)) return SFDA_ERR_ALIAS;
+    if (overlap(outs[0], outs[1])) return SFDA_ERR_ALIAS;
+    sfda::ChunkLaunch L;
+    L.q = k; L.k = k; L.v = nullptr; L.alpha = alpha; L.theta = theta; L.beta = beta;
+    L.S0 = nullptr; L.o = nullptr; L.S_T = nullptr;
+    L.B = B; L.H = H; L.T = T; L.m = m; L.n = 8; L.C = 16; L.slice = 8;
+    L.in_bf16 = in_dtype == SFDA_BF16;
+    L.out_bf16 = false;
+    if (sfda::launch_solve_monitor(L, residual, lnorm, static_cast<hipStream_t>(stream)) != hipSuccess)
+        return SFDA_ERR_HIP;
+    return SFDA_OK;
+}
+
 sfda_status_t sfda_step(const void* q, const void* k, const void* v, const void* alpha,
                         const void* theta, const void* beta, float* S, void* o, int B, int H,
                         int m, int n, sfda_dtype_t in_dtype, sfda_dtype_t out_dtype,

@@ -1205,6 +1205,101 @@ static hipError_t launch_scans_t(const ChunkLaunch& F, const ChunkLaunch& A, hip
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- solve monitor
+// The triangular solve of every 16-token block checked on its own (Prop 6.4 asks for the
+// conditioning of the WY factors to be watched through ||L|| and solve residuals): one
+// workgroup (four waves) per (head, block) forms the block's operands and L' with the
+// scans' load and Gram stages, the inverse N = (I + D_beta L')^{-1} with their row-per-lane
+// substitution, and writes max_ij |((I + D_beta L') N - I)_ij| (the substitution's
+// residual, on the same L' it used) and ||D_beta L'||_F (an upper bound of the spectral norm
+// that Prop 6.4's bound 1 / (1 - eta) needs below 1).  A block outside the decay range
+// gives NaN in both, as the scans' outputs do.
+template <int P, typename TIN>
+__global__ __launch_bounds__(NTHR) void solve_monitor_kernel(ChunkArgs args, float* residual, float* lnorm)
+{
+    constexpr int C = 16;
+    constexpr int LDG = ChunkSmem<C>::LDG;
+    __shared__ ChunkSmem<C> sm;
+    __shared__ float2 Nb[C][C + 1];
+    const int nb = (args.T + C - 1) / C;
+    const long bh = blockIdx.x / nb;
+    const int blk = static_cast<int>(blockIdx.x - bh * nb);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    {
+        float2 gkeep[C / 4];
+        stage_load<TIN, C, false>(sm, args, bh, blk * C, tid, gkeep);
+    }
+    __syncthreads();
+    stage_gram<P, C, false>(sm, tid);                // L' (strict lower of g2)
+    __syncthreads();
+    const int i = lane & 15, cg = lane >> 4;         // row i, columns cg, cg + 4, cg + 8, cg + 12
+    float2 xrow[16];                                 // row i of X = -D_beta L'
+    float nr[4], ni[4];                              // row i of N
+    float fro = 0.f;
+    if (wave == 0) {
+        const float bi = sm.beta[i];
+#pragma unroll
+        for (int s2 = 0; s2 < 16; ++s2) {
+            const float2 l = sm.g2[i * LDG + s2];
+            xrow[s2] = s2 < i ? make_float2(-bi * l.x, -bi * l.y) : make_float2(0.f, 0.f);
+            fro = __builtin_fmaf(xrow[s2].x, xrow[s2].x, __builtin_fmaf(xrow[s2].y, xrow[s2].y, fro));
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) { nr[k] = i == 4 * k + cg ? 1.f : 0.f; ni[k] = 0.f; }
+        subst_steps(nr, ni, xrow, std::make_integer_sequence<int, 15>{});
+#pragma unroll
+        for (int k = 0; k < 4; ++k) Nb[i][4 * k + cg] = make_float2(nr[k], ni[k]);
+    }
+    __syncthreads();
+    if (wave == 0) {
+        // R[i][j] = N[i][j] - sum_{s < i} X[i][s] N[s][j] - [i == j]
+        float rmax = 0.f;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int j = 4 * k + cg;
+            float rr = nr[k] - (i == j ? 1.f : 0.f), ri = ni[k];
+#pragma unroll
+            for (int s2 = 0; s2 < 15; ++s2) {
+                if (s2 >= i) continue;
+                const float2 x = xrow[s2], nv = Nb[s2][j];
+                rr -= x.x * nv.x - x.y * nv.y;
+                ri -= x.x * nv.y + x.y * nv.x;
+            }
+            const float a = __builtin_sqrtf(rr * rr + ri * ri);
+            rmax = a > rmax || a != a ? a : rmax;     // (NaN propagates)
+        }
+        fro = cg == 0 ? fro : 0.f;                    // one lane per row holds the row's sum
+#pragma unroll
+        for (int sh = 1; sh < 64; sh <<= 1) {
+            const float o = __shfl_xor(rmax, sh);
+            rmax = o > rmax || o != o ? o : rmax;
+            fro += __shfl_xor(fro, sh);
+        }
+        if (lane == 0) {
+            const long e = bh * nb + blk;
+            if (residual) residual[e] = rmax;
+            if (lnorm) lnorm[e] = __builtin_sqrtf(fro);
+        }
+    }
+}
+
+template <int P, typename TIN>
+static hipError_t launch_monitor_t(const ChunkLaunch& L, float* residual, float* lnorm, hipStream_t st)
+{
+    ChunkArgs a = make_args(L);
+    a.q = a.k;                      // the load stage also forms conj(Q) G; unused here
+    const long nb = (L.T + 15) / 16;
+    const dim3 grid(static_cast<unsigned>(static_cast<long>(L.B) * L.H * nb));
+    hipLaunchKernelGGL((solve_monitor_kernel<P, TIN>), grid, dim3(NTHR), 0, st, a, residual, lnorm);
+    return hipGetLastError();
+}
+
+hipError_t launch_solve_monitor(const ChunkLaunch& L, float* residual, float* lnorm, hipStream_t st)
+{
+    return L.in_bf16 ? launch_monitor_t<PREC_BF16, uint16_t>(L, residual, lnorm, st)
+                     : launch_monitor_t<PREC_F32, float>(L, residual, lnorm, st);
+}
+
 hipError_t launch_bwd_scans(const ChunkLaunch& F, const ChunkLaunch& A, hipStream_t st)
 {
     if (F.in_bf16)

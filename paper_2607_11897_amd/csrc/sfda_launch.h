@@ -65,6 +65,8 @@ hipError_t launch_chunk_decoupled(const ChunkLaunch& L, hipStream_t st);   // C 
 // reverse adjoint scan (A) in one launch, then the per-chunk gradient pass
 hipError_t launch_bwd_scans(const ChunkLaunch& F, const ChunkLaunch& A, hipStream_t st);
 hipError_t launch_chunk_grad(const GradLaunch& L, hipStream_t st);
+// per 16-token block: the triangular solve's residual and ||D_beta L'||_F ([B, H, ceil(T / 16)])
+hipError_t launch_solve_monitor(const ChunkLaunch& L, float* residual, float* lnorm, hipStream_t st);
 // segment-parallel scan: identity fill, the fold of the segments' affine maps and the join of
 // the outputs (o += S_in^* X)
 hipError_t launch_identity(float* P, long count, int m, hipStream_t st);

@@ -23,7 +23,7 @@ NOALLOC_SCRATCH_BYTES = 32 * 1024 * 1024      # SFDA_NOALLOC_SCRATCH_BYTES
 EXPORTS = ("sfda_chunk_fwd", "sfda_chunk_fwd_sliced", "sfda_chunk_fwd_gated", "sfda_chunk_fwd_decoupled",
            "sfda_chunk_fwd_segmented", "sfda_chunk_fwd_segmented_noalloc",
            "sfda_chunk_fwd_segmented_workspace_bytes", "sfda_chunk_fwd_auto_segments",
-           "sfda_chunk_bwd", "sfda_chunk_bwd_workspace_bytes",
+           "sfda_chunk_bwd", "sfda_chunk_bwd_workspace_bytes", "sfda_chunk_solve_monitor",
            "sfda_step", "sfda_status_string", "sfda_abi_version")
 
 _lib = None
@@ -62,6 +62,8 @@ def load_library(path: str = LIB_PATH):
     lib.sfda_chunk_fwd_segmented_workspace_bytes.argtypes = [i] * 7
     lib.sfda_chunk_fwd_segmented_workspace_bytes.restype = ctypes.c_size_t
     lib.sfda_chunk_fwd_auto_segments.argtypes = [i] * 7
+    lib.sfda_chunk_solve_monitor.argtypes = [vp] * 6 + [i] * 5 + [vp]
+    lib.sfda_chunk_solve_monitor.restype = i
     lib.sfda_chunk_fwd_auto_segments.restype = i
     lib.sfda_chunk_bwd.argtypes = [vp] * 16 + [i] * 6 + [i, i, vp, ctypes.c_size_t, vp]
     lib.sfda_chunk_bwd.restype = i
@@ -334,6 +336,32 @@ def chunk_bwd(q, k, v, alpha, theta, beta, S0, dO, dS_T=None, C: int = 64, *,
 
 def bwd_workspace_bytes(B: int, H: int, T: int, m: int, n: int, C: int) -> int:
     return int(load_library().sfda_chunk_bwd_workspace_bytes(B, H, T, m, n, C))
+
+
+def chunk_solve_monitor(k, alpha, theta, beta, stream=None) -> Tuple:
+    """The triangular solve of every 16-token block checked on its own
+    (sfda_chunk_solve_monitor): returns (residual, lnorm), float32 [B, H, ceil(T / 16)],
+    the max-abs entry of (I + D_beta L') N - I and ||D_beta L'||_F.  k: [B,H,T,m,2];
+    alpha, theta: [B,H,T,m]; beta: [B,H,T] (float32 or bfloat16)."""
+    import torch
+    lib = load_library()
+    if k.dim() != 5 or k.shape[-1] != 2:
+        raise ValueError(f"k must be [B,H,T,m,2], not {tuple(k.shape)}")
+    B, H, T, m = k.shape[0], k.shape[1], k.shape[2], k.shape[3]
+    code = _dtype_code(k)
+    for t in (alpha, theta, beta):
+        if t.dtype != k.dtype:
+            raise TypeError("k, alpha, theta, beta must share one dtype")
+    _check(dict(k=(k, (B, H, T, m, 2)), alpha=(alpha, (B, H, T, m)), theta=(theta, (B, H, T, m)),
+                beta=(beta, (B, H, T))))
+    nb = (T + 15) // 16
+    residual = torch.empty((B, H, nb), dtype=torch.float32, device=k.device)
+    lnorm = torch.empty((B, H, nb), dtype=torch.float32, device=k.device)
+    st = lib.sfda_chunk_solve_monitor(_ptr(k), _ptr(alpha), _ptr(theta), _ptr(beta), _ptr(residual),
+                                      _ptr(lnorm), B, H, T, m, code, _stream(stream))
+    if st != 0:
+        raise SfdaError(st, "sfda_chunk_solve_monitor")
+    return residual, lnorm
 
 
 def auto_segments(B: int, H: int, T: int, m: int, n: int, C: int = 64, dtype: str = "f32") -> int:

@@ -299,3 +299,17 @@ def test_binding_checks_state_and_output_dtypes(lib):
     with pytest.raises(TypeError, match="unsupported dtype"):
         sfda.step(q[:, :, 0], k[:, :, 0], v[:, :, 0], a[:, :, 0], th[:, :, 0], b[:, :, 0],
                   torch.zeros(B, H, m, n, 2), o=torch.zeros(B, H, n, 2, dtype=torch.float16))
+
+
+def monitor(lib, k=P[1], a=P[3], th=P[4], b=P[5], res=P[6], ln=P[7], B=1, H=1, T=32, m=8, din=0):
+    return lib.sfda_chunk_solve_monitor(k, a, th, b, res, ln, B, H, T, m, din, None)
+
+
+def test_solve_monitor_argument_errors(lib):
+    assert monitor(lib, din=2) == 4
+    assert monitor(lib, m=0) == 2 and monitor(lib, m=65) == 2 and monitor(lib, T=-1) == 2
+    assert monitor(lib, k=None) == 1 and monitor(lib, res=None, ln=None) == 1
+    assert monitor(lib, k=P[1] + 4) == 5
+    assert monitor(lib, res=P[1]) == 6            # over k
+    assert monitor(lib, ln=P[6]) == 6             # over residual
+    assert monitor(lib, B=0, k=None) == 0 and monitor(lib, T=0, k=None) == 0
