@@ -9,6 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsfda.so")
+POISON_LIB = os.path.join(HERE, "libsfda_poison.so")
 SOURCES = ["sfda_api.hip", "sfda_chunk.hip", "sfda_chunk_grad.hip", "sfda_chunk_bf16.hip", "sfda_segments.hip",
            "sfda_step.hip"]
 ARCH = "gfx950"
@@ -20,9 +21,12 @@ SANITIZE_FLAGS = ["-Xarch_host", "-fsanitize=address,undefined", "-Xarch_host", 
                   "-Xarch_host", "-fno-sanitize-recover=undefined"]
 
 
-def build(verbose: bool = True, sanitize: bool = False, out: str = LIB) -> str:
+def build(verbose: bool = True, sanitize: bool = False, out: str = LIB, poison: bool = False) -> str:
     """Compile every HIP source for gfx950 into one shared library (always recompiles).
-    sanitize adds ASan/UBSan instrumentation of the host code; out is the library path."""
+    sanitize adds ASan/UBSan instrumentation of the host code; poison builds the LDS-poison
+    debug variant (SFDA_LDS_POISON: the kernels fill their LDS operand areas with NaN
+    before each chunk or step rewrites them, so a stale read shows up as NaN); out is the
+    library path."""
     cmd = [
         "hipcc", f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
         "-Wall", "-Wno-unused-variable",
@@ -30,7 +34,8 @@ def build(verbose: bool = True, sanitize: bool = False, out: str = LIB) -> str:
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
         "-I", os.path.join(ROOT, "include"),
         "-o", out + ".tmp",
-    ] + (SANITIZE_FLAGS if sanitize else []) + [os.path.join(CSRC, s) for s in SOURCES]
+    ] + (SANITIZE_FLAGS if sanitize else []) + (["-DSFDA_LDS_POISON"] if poison else []) + \
+        [os.path.join(CSRC, s) for s in SOURCES]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

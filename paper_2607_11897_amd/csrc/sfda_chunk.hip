@@ -304,6 +304,12 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
     for (int it_ch = 0; it_ch < nchunks; ++it_ch) {
         const int ch = MODE == 2 ? nchunks - 1 - it_ch : it_ch;
         const int t0 = ch * C;
+#ifdef SFDA_LDS_POISON
+        // every LDS operand is rewritten by this chunk's stages before it is read
+        __syncthreads();
+        lds_poison(&sm, sizeof(SM), tid, NW * 64);
+        __syncthreads();
+#endif
         // MODE 2: this wave's dL/do entries of the chunk, requested first so that they arrive
         // during the load, Gram and inverse stages (tokens past T lie past the chunk's rows)
         typename RawC<TOUT>::W dor[CBW][NRB][4];
@@ -951,6 +957,12 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
         SM& nx = sms[(ch + 1) & 1];
         const bool more = ch + 1 < nchunks;
         const int t0 = ch * C;
+#ifdef SFDA_LDS_POISON
+        // the next chunk's set (last read in the previous iteration) is rewritten before it
+        // is read
+        if (more) lds_poison(&nx, sizeof(SM), tid, 512);
+        __syncthreads();
+#endif
 
         // ---- Delta = U - Wt S (column waves) | the next chunk's load stage
         if (more) stage_L(nx, ch + 1);

@@ -303,6 +303,16 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
     const long base_t = bh * static_cast<long>(T);
 
     auto set_ptr = [&](int s) -> char* { return reinterpret_cast<char*>(&sm.set[s]); };
+#ifdef SFDA_LDS_POISON
+    // at the top of step st, by every wave: the operand set of step st + 1 (last read in step
+    // st - 1), k / P and the inverse's scratch are rewritten before they are read
+    auto poison_next = [&](int st) {
+        lds_poison(&sm.set[(st + 1) & 1], sizeof(Set), tid, NTH);
+        lds_poison(sm.kd, sizeof(sm.kd), tid, NTH);
+        lds_poison(sm.xs, sizeof(sm.xs), tid, NTH);
+        __syncthreads();
+    };
+#endif
     constexpr int OFF_QB = offsetof(Set, qb), OFF_KB = offsetof(Set, kb), OFF_KR = offsetof(Set, kr);
     constexpr int OFF_ND = offsetof(Set, nd), OFF_AQ = offsetof(Set, aq);
 
@@ -553,6 +563,9 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
         }
         __syncthreads();          // matches the producers' lead-in barrier
         for (int st = -1; st < nsteps; ++st) {
+#ifdef SFDA_LDS_POISON
+            poison_next(st);
+#endif
             // phase 1: the first NB1 blocks of step st (the producers form step st + 1's operands)
             if (helper) {                            // V of the next step's first blocks
 #pragma unroll
@@ -872,6 +885,9 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
             }
             __syncthreads();          // block phase totals of step 0
             for (int st = -1; st < nsteps; ++st) {
+#ifdef SFDA_LDS_POISON
+                poison_next(st);
+#endif
                 // phase 1: the operands of step st + 1 (q, k requested a step ago), the next
                 // q, k.  The gated variant's scans hold more registers: it keeps one buffer and
                 // requests the next q, k once the operands are formed.  The loads are issued

@@ -173,6 +173,11 @@ __global__ __launch_bounds__(GW * 64, C <= 16 ? 4 : 2) void grad_kernel(GradArgs
     static_assert(NR >= 1 && NB % 16 == 0 && NB / 8 <= GW, "staging shape");
     __shared__ GradSmem<P, C> gs;
     ChunkSmem<C>& sm = gs.ch;
+#ifdef SFDA_LDS_POISON
+    // every LDS entry this workgroup reads is written by it first
+    lds_poison(&gs, sizeof(gs), threadIdx.x, GW * 64);
+    __syncthreads();
+#endif
 
     const ChunkArgs& args = A.in;
     const int T = args.T, m = args.m, n = args.n;

@@ -104,6 +104,14 @@ __device__ __forceinline__ float partner(float x) {
 
 struct Frag8 { float v[8]; };
 
+// LDS-poison debug build (SFDA_LDS_POISON): fill `bytes` of LDS with all-ones words (NaN as
+// float32 and as a bf16 pair), threads tid = 0 .. nthr - 1 together; the caller synchronises
+// before and after
+__device__ __forceinline__ void lds_poison(void* p, int bytes, int tid, int nthr) {
+    uint32_t* w = static_cast<uint32_t*>(p);
+    for (int e = tid; e < bytes / 4; e += nthr) w[e] = 0xFFFFFFFFu;
+}
+
 // B fragment entries for one complex value y of Y at (i, j), for output column part q:
 // q = 0 (real column): (Re y, -Im y); q = 1 (imaginary column): (Im y, Re y).
 __device__ __forceinline__ void bpair(Frag8& f, int r, float yr, float yi, int q) {

@@ -7,6 +7,7 @@ bfloat16.  torch is used for device memory and streams only.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 from typing import Optional, Tuple
@@ -34,6 +35,20 @@ class SfdaError(RuntimeError):
         self.status = status
         msg = load_library().sfda_status_string(status).decode()
         super().__init__(f"{where}: {STATUS.get(status, status)} ({msg})")
+
+
+@contextlib.contextmanager
+def library(path: str):
+    """Run the binding against another build of the library at `path` (the LDS-poison
+    debug build in its test) for the duration of a with-block, then go back to the one
+    loaded before.  Nothing may be in flight on the device when the block ends."""
+    global _lib
+    saved = _lib
+    _lib = None
+    try:
+        yield load_library(path)
+    finally:
+        _lib = saved
 
 
 def load_library(path: str = LIB_PATH):
