@@ -225,7 +225,7 @@ sfda_status_t sfda_chunk_fwd_decoupled(const void* q, const void* k, const void*
                                        sfda_dtype_t in_dtype, sfda_dtype_t out_dtype,
                                        sfda_stream_t stream)
 {
-    const int slice = n <= 64 ? ((n + 7) / 8) * 8 : 64;
+    const int slice = auto_slice(static_cast<long>(B) * H, n);
     // the shared checks, with the erase strengths in beta's place
     const sfda_status_t st0 = chunk_fwd_impl(q, k, v, alpha, theta, eta, S0, o, S_T, B, H, T, m, n,
                                              C, in_dtype, out_dtype, stream, slice, nullptr, 0,
