@@ -183,8 +183,10 @@ sfda_status_t sfda_chunk_fwd_decoupled(const void* q, const void* k, const void*
  * float32 inputs the same two passes also give the readouts X_t = P_t^* q_t and the
  * zero-state outputs o0_t, and a join writes o_t = o0_t + S_in^* X_t (the same law token by
  * token; a bfloat16 o is then rounded twice); with bfloat16 inputs a third pass writes o
- * from the exact incoming states.  Two or three times the scan work of sfda_chunk_fwd,
- * spread over G times as many workgroups; results agree with it to rounding.
+ * from the exact incoming states.  With float32 inputs and n <= 64 the two passes run as
+ * one scan per segment (one copy of the chunk factors, twice the columns).  Up to two
+ * (float32) or three (bfloat16) times the scan work of sfda_chunk_fwd, spread over G times
+ * as many workgroups; results agree with it to rounding.
  *   Arguments and errors as sfda_chunk_fwd, plus:
  *   G >= 1 with T a multiple of G * C (SFDA_ERR_SHAPE otherwise; T == 0 is as
  *   sfda_chunk_fwd).

@@ -344,16 +344,24 @@ static sfda_status_t segmented_impl(const void* q, const void* k, const void* v,
     L.q = q; L.k = k; L.alpha = alpha; L.theta = theta; L.beta = beta;
     L.B = static_cast<int>(segs); L.H = 1; L.T = Ts; L.m = m; L.C = C;
     L.in_bf16 = in_dtype == SFDA_BF16;
-    // P_g (and with the join X_t = P_t^* q_t, the m-column float32 output): S0 = I, v = 0,
-    // in place on the identity
-    if (sfda::launch_identity(P, segs, m, st) != hipSuccess) return SFDA_ERR_HIP;
-    L.v = nullptr; L.S0 = P; L.S_T = P; L.o = join ? X : nullptr; L.out_bf16 = false;
-    L.n = m; L.slice = ((m + 7) / 8) * 8;
-    if (sfda::launch_chunk(L, st) != hipSuccess) return SFDA_ERR_HIP;
-    // B_g (and with the join the zero-state outputs o0, into o)
-    L.v = v; L.S0 = nullptr; L.S_T = Bs; L.o = join ? o : nullptr; L.out_bf16 = out_dtype == SFDA_BF16;
-    L.n = n; L.slice = slice_n;
-    if (sfda::launch_chunk(L, st) != hipSuccess) return SFDA_ERR_HIP;
+    if (join && n <= 64) {
+        // P_g and B_g in one scan per segment (one copy of the chunk factors): the transfer
+        // columns from I_m with X_t = P_t^* q_t, the value columns from zero with o0 into o
+        L.v = v; L.S0 = nullptr; L.S_T = Bs; L.o = o; L.out_bf16 = out_dtype == SFDA_BF16;
+        L.n = n; L.slice = slice_n; L.xo = X; L.pend = P;
+        if (sfda::launch_chunk_segment(L, st) != hipSuccess) return SFDA_ERR_HIP;
+    } else {
+        // P_g (and with the join X_t = P_t^* q_t, the m-column float32 output): S0 = I,
+        // v = 0, in place on the identity
+        if (sfda::launch_identity(P, segs, m, st) != hipSuccess) return SFDA_ERR_HIP;
+        L.v = nullptr; L.S0 = P; L.S_T = P; L.o = join ? X : nullptr; L.out_bf16 = false;
+        L.n = m; L.slice = ((m + 7) / 8) * 8;
+        if (sfda::launch_chunk(L, st) != hipSuccess) return SFDA_ERR_HIP;
+        // B_g (and with the join the zero-state outputs o0, into o)
+        L.v = v; L.S0 = nullptr; L.S_T = Bs; L.o = join ? o : nullptr; L.out_bf16 = out_dtype == SFDA_BF16;
+        L.n = n; L.slice = slice_n;
+        if (sfda::launch_chunk(L, st) != hipSuccess) return SFDA_ERR_HIP;
+    }
     // incoming states and S_T
     if (sfda::launch_fold(P, Bs, Sin, S0, S_T, BH, G, m, n, st) != hipSuccess) return SFDA_ERR_HIP;
     if (join) {

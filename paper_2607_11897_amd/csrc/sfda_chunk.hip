@@ -35,7 +35,10 @@
 //
 // The forward and the write-decoupled forward (MODE 0 and 3, always at 16-token chunks) run
 // these stages split by role instead (chunk_scan_pipe below): four waves prepare chunk c + 1
-// in a second LDS set while the other four run chunk c's state-dependent stage.
+// in a second LDS set while the other four run chunk c's state-dependent stage.  MODE 4 is the
+// forward of a sequence segment for the segment-parallel scan: beside the value columns
+// scanned from a zero state it scans the m columns of the segment's homogeneous transfer
+// P_t (entering state I, no values), with one copy of the state-independent stages.
 //
 // The same kernel runs the two scans of the backward: MODE 1 is the forward recording the
 // state entering each chunk and Delta; MODE 2 walks the chunks in reverse carrying dL/dS
@@ -757,10 +760,14 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
 template <int P, typename TIN, typename TOUT, bool GATED, int MODE, typename SM>
 __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& args, unsigned block, long heads)
 {
-    static_assert(MODE == 0 || MODE == 3, "the forward and the write-decoupled forward");
+    static_assert(MODE == 0 || MODE == 3 || MODE == 4, "the forward, the write-decoupled forward, the segment forward");
     constexpr int C = 16;
     constexpr int NC = 4;                         // column waves (0..3); preparing waves 4..7
-    constexpr int CBW = 2;                        // column blocks per column wave: w, w + 4
+    // MODE 4 (segment forward) holds two column sets: slots 0, 1 scan the transfer P_t
+    // (columns of I_m, no values; outputs X_t = P_t^* q_t to args.xo, the last P_t to
+    // args.pend), slots 2, 3 the value columns from a zero state
+    constexpr bool SEGF = MODE == 4;
+    constexpr int CBW = SEGF ? 4 : 2;             // column blocks per column wave: w, w + 4 (per set)
     constexpr int SEG = C / 4;
     constexpr int LDG = ChunkSmem<C>::LDG;
 
@@ -784,6 +791,12 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
     const long base_tn = bh * static_cast<long>(T) * n;
     const long base_mn = bh * static_cast<long>(m) * n;
     const int nchunks = (T + C - 1) / C;
+    // column slot w: its set (value columns, or MODE 4's transfer columns), block and column
+    // (all folded to constants or simple expressions once the loops over w are unrolled)
+    auto vset = [&](int w) { return !SEGF || w >= 2; };
+    auto cblk = [&](int w) { return wave + NC * (SEGF ? (w & 1) : w); };
+    auto active = [&](int w) { return cblk(w) < (vset(w) ? ncb : (m + 7) / 8); };
+    auto colj = [&](int w) { return (vset(w) ? n0 : 0) + cblk(w) * 8 + (c >> 1); };
 
     // ---------------------------------------------------------------- state (column waves)
     f32x4 Sacc[CBW][MP / 16];
@@ -791,9 +804,16 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
         const rsrc_t rs = buf(args.S0 ? args.S0 + 2 * base_mn : args.S0, args.S0 ? static_cast<long>(m) * n * 8 : 0);
 #pragma unroll
         for (int w = 0; w < CBW; ++w) {
-            const int cb = wave + NC * w;
-            const int j = n0 + cb * 8 + (c >> 1);
-            const bool jok = cb < ncb && j < n;
+            const int j = colj(w);
+            if (!vset(w)) {                       // the transfer columns start from I_m
+#pragma unroll
+                for (int kb = 0; kb < MP / 16; ++kb)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        Sacc[w][kb][r] = qp == 0 && kb * 16 + 4 * g + r == j ? 1.f : 0.f;
+                continue;
+            }
+            const bool jok = active(w) && j < n;
 #pragma unroll
             for (int kb = 0; kb < MP / 16; ++kb)
 #pragma unroll
@@ -816,9 +836,9 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
         const rsrc_t rv = buf(gv ? gv + 2 * (base_tn + static_cast<long>(t0) * n) : gv, vbytes);
 #pragma unroll
         for (int w = 0; w < CBW; ++w) {
-            const int cb = wave + NC * w;
-            const int j = n0 + cb * 8 + (c >> 1);
-            const bool jok = cb < ncb && j < n;
+            if (!vset(w)) continue;               // the transfer columns have no values
+            const int j = colj(w);
+            const bool jok = active(w) && j < n;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int tl = 4 * g + r;
@@ -897,14 +917,16 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
                     bpair(bvr[w], r, bw * vf[w][r].x, -bw * vf[w][r].y, qp);
                 }
                 f32x4 y = zero4();
-                if (wave + NC * w < ncb) mma<P>(y, a3, bvr[w]);
+                if (active(w)) mma<P>(y, a3, bvr[w]);
                 bv = bfrag_from_acc(y, qp);
             } else {
+                U[w] = zero4();
+                if (!vset(w)) continue;           // transfer columns: U = 0
 #pragma unroll
                 for (int r = 0; r < 4; ++r) bpair(bv, r, vf[w][r].x, -vf[w][r].y, qp);
             }
             U[w] = zero4();
-            if (wave + NC * w < ncb) mma<P>(U[w], ta, bv);
+            if (active(w)) mma<P>(U[w], ta, bv);
         }
     };
     // preparing waves: Wt = T (conj(K) G), two 16 x 8 tiles per wave, written over conj(K) G
@@ -970,7 +992,7 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
         if (cols) {
 #pragma unroll
             for (int w = 0; w < CBW; ++w) {
-                if (wave + NC * w >= ncb) continue;
+                if (!active(w)) continue;
                 f32x4 pw = zero4();
 #pragma unroll
                 for (int kb = 0; kb < MP / 16; ++kb) {
@@ -996,9 +1018,8 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
         if (cols) {
 #pragma unroll
             for (int w = 0; w < CBW; ++w) {
-                const int cb = wave + NC * w;
-                if (cb >= ncb) continue;
-                const int j = n0 + cb * 8 + (c >> 1);
+                if (!active(w)) continue;
+                const int j = colj(w);
                 f32x4 acc = zero4();
 #pragma unroll
                 for (int kb = 0; kb < MP / 16; ++kb) {
@@ -1032,7 +1053,16 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
                     }
                     mma<P>(acc, a, bvr[w]);
                 }
-                if (j < n && go != nullptr) {     // o == NULL: no output
+                if (!vset(w)) {                   // X_t = P_t^* q_t, [heads][T][m] complex fp32
+                    if (j < m && args.xo != nullptr) {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const int t = t0 + 4 * g + r;
+                            if (t < T)
+                                args.xo[2 * ((bh * T + t) * m + j) + qp] = qp ? -acc[r] : acc[r];
+                        }
+                    }
+                } else if (j < n && go != nullptr) {     // o == NULL: no output
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
                         const int t = t0 + 4 * g + r;
@@ -1051,7 +1081,7 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
         if (cols) {
 #pragma unroll
             for (int w = 0; w < CBW; ++w) {
-                if (wave + NC * w >= ncb) continue;
+                if (!active(w)) continue;
                 const Frag8 db = bfrag_from_acc(U[w], qp);
 #pragma unroll
                 for (int kb = 0; kb < MP / 16; ++kb) {
@@ -1099,18 +1129,20 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
     }
 
     // ---------------------------------------------------------------- final state
-    if (cols && args.S_T != nullptr) {
+    if (cols) {
 #pragma unroll
         for (int w = 0; w < CBW; ++w) {
-            const int cb = wave + NC * w;
-            const int j = n0 + cb * 8 + (c >> 1);
-            if (cb >= ncb || j >= n) continue;
+            const int j = colj(w);
+            // the value columns' S_T [heads][m][n]; MODE 4's last transfer P [heads][m][m]
+            float* dst = vset(w) ? args.S_T : args.pend;
+            const int w_n = vset(w) ? n : m;
+            if (dst == nullptr || !active(w) || j >= w_n) continue;
 #pragma unroll
             for (int kb = 0; kb < MP / 16; ++kb)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int i = kb * 16 + 4 * g + r;
-                    if (i < m) args.S_T[2 * (base_mn + static_cast<long>(i) * n + j) + qp] = Sacc[w][kb][r];
+                    if (i < m) dst[2 * ((bh * m + i) * static_cast<long>(w_n) + j) + qp] = Sacc[w][kb][r];
                 }
         }
     }
@@ -1124,7 +1156,7 @@ template <int P, typename TIN, typename TOUT, int C, bool GATED, int MODE>
 __global__ __launch_bounds__(scan_waves<C>() * 64, 1) void chunk_kernel(ChunkArgs args)
 {
     using SM = std::conditional_t<MODE == 3, ChunkSmemDec<C>, ChunkSmem<C>>;
-    if constexpr (C == 16 && (MODE == 0 || MODE == 3)) {
+    if constexpr (C == 16 && (MODE == 0 || MODE == 3 || MODE == 4)) {
         __shared__ SM sms[2];
         chunk_scan_pipe<P, TIN, TOUT, GATED, MODE, SM>(sms, args, blockIdx.x, gridDim.x / args.n_slices);
     } else {
@@ -1156,6 +1188,7 @@ static ChunkArgs make_args(const ChunkLaunch& L)
     a.amin = L.alpha_min; a.aspan = L.alpha_max - L.alpha_min; a.tmax = L.theta_max; a.eps = L.eps;
     a.ck_state = L.ck_state; a.ck_rows = L.ck_rows; a.dO = L.dO; a.dv = L.dv;
     a.r = L.r; a.wbeta = L.wbeta;
+    a.xo = L.xo; a.pend = L.pend;
     return a;
 }
 
@@ -1180,6 +1213,20 @@ hipError_t launch_chunk(const ChunkLaunch& L, hipStream_t st)
     if (L.in_bf16) return launch_chunk_bf16(L, st);
     return L.out_bf16 ? launch_chunk_t<PREC_F32, float, uint16_t>(L, st)
                       : launch_chunk_t<PREC_F32, float, float>(L, st);
+}
+
+// the segment forward of the segment-parallel scan (float32 inputs, one slice of at most 64
+// value columns): the transfer and the zero-state scan of a segment in one workgroup
+hipError_t launch_chunk_segment(const ChunkLaunch& L, hipStream_t st)
+{
+    if (L.in_bf16 || L.gated || L.n > 64 || L.slice < L.n) return hipErrorInvalidValue;
+    const ChunkArgs a = make_args(L);
+    const dim3 grid(static_cast<unsigned>(static_cast<long>(L.B) * L.H));
+    if (L.out_bf16)
+        hipLaunchKernelGGL((chunk_kernel<PREC_F32, float, uint16_t, 16, false, 4>), grid, dim3(scan_waves<16>() * 64), 0, st, a);
+    else
+        hipLaunchKernelGGL((chunk_kernel<PREC_F32, float, float, 16, false, 4>), grid, dim3(scan_waves<16>() * 64), 0, st, a);
+    return hipGetLastError();
 }
 
 template <int P, typename TIN, typename TOUT>

@@ -69,6 +69,10 @@ struct ChunkArgs {
     // [B,H,T] (beta then holds the erase strengths eta)
     const void* r;
     const void* wbeta;
+    // segment forward (MODE 4): the transfer columns' outputs X_t = P_t^* q_t
+    // [heads][T][m] and last transfer P [heads][m][m], complex fp32 (either may be null)
+    float* xo;
+    float* pend;
 };
 
 __device__ __forceinline__ float sigmoid_acc(float x) { return 1.f / (1.f + expf(-x)); }

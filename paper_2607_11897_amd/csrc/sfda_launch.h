@@ -39,6 +39,11 @@ struct ChunkLaunch {
     // strengths wbeta; beta holds the erase strengths
     const void* r = nullptr;
     const void* wbeta = nullptr;
+    // segment forward (launch_chunk_segment): beside the value columns (from S0 = 0 when
+    // S0 is null) the m columns of the homogeneous transfer from I_m, with outputs
+    // X_t = P_t^* q_t [heads][T][m] and the last transfer [heads][m][m] (complex fp32)
+    float* xo = nullptr;
+    float* pend = nullptr;
 };
 
 // per-chunk gradient pass of the backward (one workgroup per head and chunk)
@@ -61,6 +66,7 @@ hipError_t launch_step(const StepLaunch& L, hipStream_t st);
 hipError_t launch_chunk(const ChunkLaunch& L, hipStream_t st);
 hipError_t launch_chunk_bf16(const ChunkLaunch& L, hipStream_t st);   // bf16 inputs
 hipError_t launch_chunk_decoupled(const ChunkLaunch& L, hipStream_t st);   // C = 16 or 32
+hipError_t launch_chunk_segment(const ChunkLaunch& L, hipStream_t st);
 // backward: the forward scan recording states and Delta (F; none when F.T == 0) and the
 // reverse adjoint scan (A) in one launch, then the per-chunk gradient pass
 hipError_t launch_bwd_scans(const ChunkLaunch& F, const ChunkLaunch& A, hipStream_t st);

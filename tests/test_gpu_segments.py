@@ -77,6 +77,26 @@ def test_segmented_f32(B, H, T, m, n, C, G):
     assert eo <= 1e-4 and es <= 1e-4
 
 
+@pytest.mark.parametrize("m,n,G", [(64, 40, 4), (21, 64, 2)])
+def test_segmented_f32_in_bf16_out(m, n, G):
+    """float32 inputs, bfloat16 output: the segment scans store o0 in bfloat16 and the join
+    adds S_in^* X in float32 before rounding once more; o within the bf16 bar, S_T (float32)
+    within 1e-4."""
+    import torch
+    from paper_2607_11897_amd import sfda
+    x = make(2, 1, 256, m, n, 16, seed=17)
+    say("f32 -> bf16", (2, 1, 256, m, n), "G", G)
+    d = upload(x)
+    o, S = sfda.chunk_fwd(d["q"], d["k"], d["v"], d["alpha"], d["theta"], d["beta"], d["S0"], C=16,
+                          segments=G, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    o, S = to_complex(o), to_complex(S)
+    o_ref, S_ref = run_oracle(x)
+    eo, es = rel_err(o, o_ref), rel_err(S, S_ref)
+    say("err(o)", eo, "err(S_T)", es)
+    assert eo <= 2e-2 and es <= 1e-4
+
+
 def test_segmented_zero_state_and_in_place():
     x = make(1, 2, 128, 64, 64, 16, zero_state=True)
     o, S = run(x, 16, 4)
