@@ -36,8 +36,8 @@
 //     inverse N = (I + D_beta L)^{-1} in fp32, beside its last block of step s;
 //   waves 4-7 (producers) own one block of 16 tokens each.  Before the middle barrier they
 //     form step s + 1's operands conj(Q)G, conj(K)G, k / P and K Q (bf16, to LDS) from
-//     q, k requested a step earlier (a second register buffer; the gated variant keeps
-//     one) and request step s + 2's q, k; after it they run step s + 2's prefix and suffix
+//     q, k requested a step earlier (a second register buffer) and request step s + 2's
+//     q, k; after it they run step s + 2's prefix and suffix
 //     decay products and phase sums (scans over a lane's four tokens and a wave's four
 //     token segments; the phase offsets of earlier blocks through LDS) and request step
 //     s + 3's alpha, theta.
@@ -889,19 +889,14 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 poison_next(st);
 #endif
                 // phase 1: the operands of step st + 1 (q, k requested a step ago), the next
-                // q, k.  The gated variant's scans hold more registers: it keeps one buffer and
-                // requests the next q, k once the operands are formed.  The loads are issued
-                // on every step (past the last step their ranges are empty): a path without
-                // them would make the wait counts at the loop head cover the younger alpha,
-                // theta and beta loads too.
-                if constexpr (GATED) {
-                    if (st + 1 < nsteps) produce(st + 1, nxt);
-                    load_qk(st + 2, nxt, wide_c);
-                } else {
-                    if (st + 1 < nsteps) cur = nxt;
-                    load_qk(st + 2, nxt, wide_c);
-                    if (st + 1 < nsteps) produce(st + 1, cur);
-                }
+                // q, k.  The loads are issued on every step (past the last step their ranges
+                // are empty): a path without them would make the wait counts at the loop head
+                // cover the younger alpha, theta and beta loads too.  (The gated variant's
+                // scans hold more registers; with the second buffer a few are spilled, which
+                // costs less than requesting q, k only once the operands are formed.)
+                if (st + 1 < nsteps) cur = nxt;
+                load_qk(st + 2, nxt, wide_c);
+                if (st + 1 < nsteps) produce(st + 1, cur);
                 __syncthreads();
                 // phase 2: the scans of step st + 2, alpha, theta and beta of the step after
                 if (st + 2 < nsteps) pretot(st + 2);
