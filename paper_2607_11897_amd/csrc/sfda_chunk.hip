@@ -303,7 +303,7 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
     constexpr bool PRE = NW > 4;
     InPre<C> pf;
     if constexpr (PRE)
-        if (nchunks > 0) prefetch_inputs<TIN, C, true>(args, bh, (MODE == 2 ? nchunks - 1 : 0) * C, tid, pf);
+        if (nchunks > 0) prefetch_inputs<TIN, C, true, MODE == 3>(args, bh, (MODE == 2 ? nchunks - 1 : 0) * C, tid, pf);
     for (int it_ch = 0; it_ch < nchunks; ++it_ch) {
         const int ch = MODE == 2 ? nchunks - 1 - it_ch : it_ch;
         const int t0 = ch * C;
@@ -378,7 +378,7 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
         }
         if constexpr (PRE)
             if (it_ch + 1 < nchunks)
-                prefetch_inputs<TIN, C, true>(args, bh, (MODE == 2 ? ch - 1 : ch + 1) * C, tid, pf);
+                prefetch_inputs<TIN, C, true, MODE == 3>(args, bh, (MODE == 2 ? ch - 1 : ch + 1) * C, tid, pf);
         __syncthreads();
 
         // ============================================================ G: L' and A
@@ -826,7 +826,7 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
     __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): as in chunk_scan
 
     InPre<C> pf;
-    if (nchunks > 0) prefetch_inputs<TIN, C, true>(args, bh, 0, rtid, pf);
+    if (nchunks > 0) prefetch_inputs<TIN, C, true, MODE == 3>(args, bh, 0, rtid, pf);
 
     // ---------------------------------------------------------------- stage pieces
     float2 vf[CBW][4];                            // column waves: conj(V) fragments of the next chunk
@@ -851,15 +851,17 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
     auto stage_L = [&](SM& sm, int ch) __attribute__((always_inline)) {
         float2 gkeep[SEG];
         stage_load<TIN, C, GATED, false, MODE == 3, SM, true, true>(sm, args, bh, ch * C, rtid, gkeep, &pf);
-        if (ch + 1 < nchunks) prefetch_inputs<TIN, C, true>(args, bh, (ch + 1) * C, rtid, pf);
+        if (ch + 1 < nchunks) prefetch_inputs<TIN, C, true, MODE == 3>(args, bh, (ch + 1) * C, rtid, pf);
     };
-    // L' and A, one 16 x 8 tile per preparing wave (MODE 3: then L'_kr and A_qr)
+    // L' and A, one 16 x 8 tile per preparing wave
     auto stage_G = [&](SM& sm) __attribute__((always_inline)) {
         stage_gram<P, C, true, false, SM, 4>(sm, rtid);
-        if constexpr (MODE == 3) stage_gram<P, C, true, true, SM, 4>(sm, rtid);
     };
-    // N = (I + D_beta L')^{-1} on the first preparing wave, written over L'
+    // N = (I + D_beta L')^{-1} on the first preparing wave, written over L'; MODE 3: L'_kr
+    // and A_qr (not needed by the inverse) on the other three meanwhile
     auto stage_S = [&](SM& sm) __attribute__((always_inline)) {
+        if constexpr (MODE == 3)
+            if (pwave > 0) stage_gram<P, C, true, true, SM, 3>(sm, rtid - 64);
         if (pwave == 0) {
             const int i = lane & 15, cg = lane >> 4;
             const float bi = sm.beta[i];

@@ -101,11 +101,13 @@ struct ChunkSmemDec : ChunkSmem<C> {
 
 // alpha, theta, beta, q and k of one thread's tokens, fetched a chunk ahead by a scan, as
 // the loaded words (a bf16 value is converted where it is used, so the fetch is not waited
-// on where it is issued); q, k take one word per complex bf16 value, two per complex fp32
+// on where it is issued); q, k take one word per complex bf16 value, two per complex fp32.
+// The write-decoupled forward also fetches the write directions r and write strengths.
 template <int C>
 struct InPre {
     uint32_t a[C / 4], th[C / 4], b;
     uint32_t q[C / 4][2], k[C / 4][2];
+    uint32_t r[C / 4][2], wb;
 };
 template <typename TIN> __device__ __forceinline__ uint32_t raw_word(const void* p, long e) {
     if constexpr (sizeof(TIN) == 2) return static_cast<const uint16_t*>(p)[e];
@@ -115,7 +117,7 @@ template <typename TIN> __device__ __forceinline__ float word_f(uint32_t w) {
     return __uint_as_float(sizeof(TIN) == 2 ? w << 16 : w);
 }
 
-template <typename TIN, int C, bool WIDE>
+template <typename TIN, int C, bool WIDE, bool DEC = false>
 __device__ __forceinline__ void prefetch_inputs(const ChunkArgs& args, long bh, int t0, int tid, InPre<C>& pf)
 {
     constexpr int SEG = C / 4;
@@ -137,8 +139,18 @@ __device__ __forceinline__ void prefetch_inputs(const ChunkArgs& args, long bh, 
             pf.q[u][0] = qw.x; pf.q[u][1] = qw.y;
             pf.k[u][0] = kw.x; pf.k[u][1] = kw.y;
         }
+        if constexpr (DEC) {
+            if constexpr (sizeof(TIN) == 2) {
+                pf.r[u][0] = static_cast<const uint32_t*>(args.r)[e];
+            } else {
+                const uint2 rw = static_cast<const uint2*>(args.r)[e];
+                pf.r[u][0] = rw.x; pf.r[u][1] = rw.y;
+            }
+        }
     }
-    pf.b = raw_word<TIN>(args.beta, bh * static_cast<long>(T) + min(t0 + (tid & (C - 1)), T - 1));
+    const long eb = bh * static_cast<long>(T) + min(t0 + (tid & (C - 1)), T - 1);
+    pf.b = raw_word<TIN>(args.beta, eb);
+    if constexpr (DEC) pf.wb = raw_word<TIN>(args.wbeta, eb);
 }
 
 // ----------------------------------------------------------------- load stage
@@ -230,7 +242,9 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
         if constexpr (GATED) bv = sigmoid_acc(bv);
         if (tid < C) sm.beta[tid] = masked(tb < T, bv);
         if constexpr (DEC) {
-            const float wv = Elem<TIN>::load(static_cast<const TIN*>(args.wbeta), bh * static_cast<long>(T) + min(tb, T - 1));
+            float wv;
+            if constexpr (PRE) wv = word_f<TIN>(pre->wb);
+            else wv = Elem<TIN>::load(static_cast<const TIN*>(args.wbeta), bh * static_cast<long>(T) + min(tb, T - 1));
             if (tid < C) sm.wb[tid] = masked(tb < T, wv);
         }
     }
@@ -281,7 +295,16 @@ __device__ __forceinline__ void stage_load(SM& sm, const ChunkArgs& args, long b
         sm.kg[tl * LDX + i] = make_float2(kk.x * gr + kk.y * gi, kk.x * gi - kk.y * gr);
         sm.ki[tl * LDX + i] = make_float2(kk.x * hr - kk.y * hi, kk.x * hi + kk.y * hr);
         if constexpr (DEC) {
-            const float2 rr = masked(ok, Elem<TIN>::load2(static_cast<const TIN*>(args.r), e2));
+            float2 rr;
+            if constexpr (PRE) {
+                if constexpr (sizeof(TIN) == 2)
+                    rr = make_float2(__uint_as_float(pre->r[u][0] << 16), __uint_as_float(pre->r[u][0] & 0xFFFF0000u));
+                else
+                    rr = make_float2(__uint_as_float(pre->r[u][0]), __uint_as_float(pre->r[u][1]));
+            } else {
+                rr = Elem<TIN>::load2(static_cast<const TIN*>(args.r), e2);
+            }
+            rr = masked(ok, rr);
             sm.ri[tl * LDX + i] = make_float2(rr.x * hr - rr.y * hi, rr.x * hi + rr.y * hr);
         }
         if (tl == C - 1) sm.gc[i] = make_float2(gr, gi);
