@@ -61,24 +61,27 @@ template <int K>
 __device__ __forceinline__ float row_bcast(float x) {
     return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x150 + K, 0xF, 0xF, false));
 }
-template <int S>
+// SLOTS: the slots k this lane's wave carries (bit k); two waves can share one inverse, one
+// taking slots {0, 3}, the other {1, 2} (18 of the 36 slot steps each)
+template <int S, int SLOTS>
 __device__ __forceinline__ void subst_step(float (&nr)[4], float (&ni)[4], const float2 (&xrow)[16])
 {
     const float xr = xrow[S].x, xi = xrow[S].y;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-        if (4 * k > S) continue;
+        if (4 * k > S || !((SLOTS >> k) & 1)) continue;
         const float pr = row_bcast<S>(nr[k]), pi = row_bcast<S>(ni[k]);
         nr[k] = __builtin_fmaf(xr, pr, __builtin_fmaf(-xi, pi, nr[k]));
         ni[k] = __builtin_fmaf(xr, pi, __builtin_fmaf(xi, pr, ni[k]));
     }
 }
-template <int... S>
+template <int SLOTS = 0xF, int... S>
 __device__ __forceinline__ void subst_steps(float (&nr)[4], float (&ni)[4], const float2 (&xrow)[16],
                                             std::integer_sequence<int, S...>)
 {
-    (subst_step<S>(nr, ni, xrow), ...);
+    (subst_step<S, SLOTS>(nr, ni, xrow), ...);
 }
+constexpr int SLOTS_A = 0x9, SLOTS_B = 0x6;     // the two halves of a shared inverse
 
 // a complex element as loaded (bf16 pair word or fp32 pair), converted where it is used
 template <typename T> struct RawC;
@@ -387,24 +390,37 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
         __syncthreads();
 
         // ============================================================ S: N = (I + D_beta L')^{-1}
-        if (wave < NRB) {
-            // diagonal block p = wave (the substitution above): lane (i, cg) reads row i of
-            // L' and writes row i of N over it (one wave's LDS accesses run in order)
-            const int p = wave, i = lane & 15, cg = lane >> 4;
-            const float bi = sm.beta[p * 16 + i];
+        // diagonal block p (the substitution above): lane (i, cg) reads row i of L' and writes
+        // row i of N over it.  With a wave to spare per block, two waves share each block's
+        // slots and both read L' before either writes (a barrier between); otherwise one wave
+        // per block (its LDS accesses run in order)
+        constexpr bool SPLIT = 2 * NRB <= NW;
+        {
+            const int p = SPLIT ? wave >> 1 : wave, i = lane & 15, cg = lane >> 4;
+            const bool inv = wave < (SPLIT ? 2 * NRB : NRB);
             float2 xrow[16];
-#pragma unroll
-            for (int s2 = 0; s2 < 16; ++s2) {
-                const float2 l = sm.g2[(p * 16 + i) * LDG + p * 16 + s2];
-                xrow[s2] = s2 < i ? make_float2(-bi * l.x, -bi * l.y) : make_float2(0.f, 0.f);
-            }
             float nr[4], ni[4];
+            if (inv) {
+                const float bi = sm.beta[p * 16 + i];
 #pragma unroll
-            for (int k = 0; k < 4; ++k) { nr[k] = i == 4 * k + cg ? 1.f : 0.f; ni[k] = 0.f; }
-            subst_steps(nr, ni, xrow, std::make_integer_sequence<int, 15>{});
+                for (int s2 = 0; s2 < 16; ++s2) {
+                    const float2 l = sm.g2[(p * 16 + i) * LDG + p * 16 + s2];
+                    xrow[s2] = s2 < i ? make_float2(-bi * l.x, -bi * l.y) : make_float2(0.f, 0.f);
+                }
 #pragma unroll
-            for (int k = 0; k < 4; ++k)
-                if (4 * k + cg < i) sm.g2[(p * 16 + i) * LDG + p * 16 + 4 * k + cg] = make_float2(nr[k], ni[k]);
+                for (int k = 0; k < 4; ++k) { nr[k] = i == 4 * k + cg ? 1.f : 0.f; ni[k] = 0.f; }
+            }
+            if constexpr (SPLIT) __syncthreads();
+            if (inv) {
+                const int slots = SPLIT ? ((wave & 1) ? SLOTS_B : SLOTS_A) : 0xF;
+                if (!SPLIT) subst_steps<0xF>(nr, ni, xrow, std::make_integer_sequence<int, 15>{});
+                else if (wave & 1) subst_steps<SLOTS_B>(nr, ni, xrow, std::make_integer_sequence<int, 15>{});
+                else subst_steps<SLOTS_A>(nr, ni, xrow, std::make_integer_sequence<int, 15>{});
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    if (((slots >> k) & 1) && 4 * k + cg < i)
+                        sm.g2[(p * 16 + i) * LDG + p * 16 + 4 * k + cg] = make_float2(nr[k], ni[k]);
+            }
         }
         __syncthreads();
         // off-diagonal blocks, block row by block row:
@@ -857,12 +873,13 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
     auto stage_G = [&](SM& sm) __attribute__((always_inline)) {
         stage_gram<P, C, true, false, SM, 4>(sm, rtid);
     };
-    // N = (I + D_beta L')^{-1} on the first preparing wave, written over L'; MODE 3: L'_kr
-    // and A_qr (not needed by the inverse) on the other three meanwhile
+    // N = (I + D_beta L')^{-1} into nn on the first two preparing waves (slots {0, 3} and
+    // {1, 2} of each row); MODE 3: L'_kr and A_qr (not needed by the inverse) on the other
+    // two meanwhile
     auto stage_S = [&](SM& sm) __attribute__((always_inline)) {
         if constexpr (MODE == 3)
-            if (pwave > 0) stage_gram<P, C, true, true, SM, 3>(sm, rtid - 64);
-        if (pwave == 0) {
+            if (pwave >= 2) stage_gram<P, C, true, true, SM, 2>(sm, rtid - 128);
+        if (pwave < 2) {
             const int i = lane & 15, cg = lane >> 4;
             const float bi = sm.beta[i];
             float2 xrow[16];
@@ -874,10 +891,12 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
             float nr[4], ni[4];
 #pragma unroll
             for (int k = 0; k < 4; ++k) { nr[k] = i == 4 * k + cg ? 1.f : 0.f; ni[k] = 0.f; }
-            subst_steps(nr, ni, xrow, std::make_integer_sequence<int, 15>{});
+            const int slots = pwave ? SLOTS_B : SLOTS_A;
+            if (pwave) subst_steps<SLOTS_B>(nr, ni, xrow, std::make_integer_sequence<int, 15>{});
+            else subst_steps<SLOTS_A>(nr, ni, xrow, std::make_integer_sequence<int, 15>{});
 #pragma unroll
             for (int k = 0; k < 4; ++k)
-                if (4 * k + cg < i) sm.g2[i * LDG + 4 * k + cg] = make_float2(nr[k], ni[k]);
+                if (((slots >> k) & 1) && 4 * k + cg < i) sm.nn[i * LDG + 4 * k + cg] = make_float2(nr[k], ni[k]);
         }
     };
     // A fragment of T = N D_beta (rows c, K = the chunk's tokens)
@@ -886,7 +905,7 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int j = 4 * g + r;
-            float2 nvv = sm.g2[c * LDG + j];
+            float2 nvv = sm.nn[c * LDG + j];
             nvv = j < c ? nvv : make_float2(j == c ? 1.f : 0.f, 0.f);
             const float bj = sm.beta[j];
             a.v[2 * r] = nvv.x * bj;
@@ -1157,7 +1176,8 @@ template <int C> constexpr int scan_waves() { return C == 64 ? 4 : 8; }
 template <int P, typename TIN, typename TOUT, int C, bool GATED, int MODE>
 __global__ __launch_bounds__(scan_waves<C>() * 64, 1) void chunk_kernel(ChunkArgs args)
 {
-    using SM = std::conditional_t<MODE == 3, ChunkSmemDec<C>, ChunkSmem<C>>;
+    using SM = std::conditional_t<MODE == 3, ChunkSmemDec<C>,
+                                  std::conditional_t<C == 16 && (MODE == 0 || MODE == 4), ChunkSmemPipe<C>, ChunkSmem<C>>>;
     if constexpr (C == 16 && (MODE == 0 || MODE == 3 || MODE == 4)) {
         __shared__ SM sms[2];
         chunk_scan_pipe<P, TIN, TOUT, GATED, MODE, SM>(sms, args, blockIdx.x, gridDim.x / args.n_slices);

@@ -90,10 +90,17 @@ struct ChunkSmem {
     float segp[4][MP];
 };
 
+// the role-split scans (16-token chunks) keep N = (I + D_beta L')^{-1} apart from L' (two
+// waves form it, so it cannot be written over L' while the other may still read L')
+template <int C>
+struct ChunkSmemPipe : ChunkSmem<C> {
+    float2 nn[C * ChunkSmem<C>::LDG];        // N, strict lower triangle
+};
+
 // the write-decoupled forward also keeps R / G, the k-r and q-r Gram blocks and the write
 // strengths
 template <int C>
-struct ChunkSmemDec : ChunkSmem<C> {
+struct ChunkSmemDec : ChunkSmemPipe<C> {
     float2 ri[C * LDX];                      // r_t / g_t
     float2 g3[C * ChunkSmem<C>::LDG];        // packed: L'_kr (strict lower), A_qr^T (strict upper), A_qr diag
     float wb[C];                             // write strengths beta_t
