@@ -83,6 +83,25 @@ __device__ __forceinline__ void subst_steps(float (&nr)[4], float (&ni)[4], cons
 }
 constexpr int SLOTS_A = 0x9, SLOTS_B = 0x6;     // the two halves of a shared inverse
 
+// Row i of X = -(D_beta L') for the substitution: the 16 entries of row i of the packed C x C
+// block at `row` (L' left of the diagonal, A to its right), taken on every lane and masked
+// afterwards -- read only where needed, each read would be issued and waited for on its own.
+// Eight at a time, to hold fewer registers.
+__device__ __forceinline__ void load_xrow(const float2* row, float bi, int i, float2 (&xrow)[16])
+{
+#pragma unroll
+    for (int h = 0; h < 16; h += 8) {
+        float2 l[8];
+#pragma unroll
+        for (int s2 = 0; s2 < 8; ++s2) l[s2] = row[h + s2];
+#pragma unroll
+        for (int s2 = 0; s2 < 8; ++s2) l[s2] = pin(l[s2]);
+#pragma unroll
+        for (int s2 = 0; s2 < 8; ++s2)
+            xrow[h + s2] = h + s2 < i ? make_float2(-bi * l[s2].x, -bi * l[s2].y) : make_float2(0.f, 0.f);
+    }
+}
+
 // a complex element as loaded (bf16 pair word or fp32 pair), converted where it is used
 template <typename T> struct RawC;
 template <> struct RawC<uint16_t> {
@@ -401,12 +420,7 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
             float2 xrow[16];
             float nr[4], ni[4];
             if (inv) {
-                const float bi = sm.beta[p * 16 + i];
-#pragma unroll
-                for (int s2 = 0; s2 < 16; ++s2) {
-                    const float2 l = sm.g2[(p * 16 + i) * LDG + p * 16 + s2];
-                    xrow[s2] = s2 < i ? make_float2(-bi * l.x, -bi * l.y) : make_float2(0.f, 0.f);
-                }
+                load_xrow(&sm.g2[(p * 16 + i) * LDG + p * 16], sm.beta[p * 16 + i], i, xrow);
 #pragma unroll
                 for (int k = 0; k < 4; ++k) { nr[k] = i == 4 * k + cg ? 1.f : 0.f; ni[k] = 0.f; }
             }
@@ -881,13 +895,8 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
             if (pwave >= 2) stage_gram<P, C, true, true, SM, 2>(sm, rtid - 128);
         if (pwave < 2) {
             const int i = lane & 15, cg = lane >> 4;
-            const float bi = sm.beta[i];
             float2 xrow[16];
-#pragma unroll
-            for (int s2 = 0; s2 < 16; ++s2) {
-                const float2 l = sm.g2[i * LDG + s2];
-                xrow[s2] = s2 < i ? make_float2(-bi * l.x, -bi * l.y) : make_float2(0.f, 0.f);
-            }
+            load_xrow(&sm.g2[i * LDG], sm.beta[i], i, xrow);
             float nr[4], ni[4];
 #pragma unroll
             for (int k = 0; k < 4; ++k) { nr[k] = i == 4 * k + cg ? 1.f : 0.f; ni[k] = 0.f; }
@@ -1318,13 +1327,10 @@ __global__ __launch_bounds__(NTHR) void solve_monitor_kernel(ChunkArgs args, flo
     float nr[4], ni[4];                              // row i of N
     float fro = 0.f;
     if (wave == 0) {
-        const float bi = sm.beta[i];
+        load_xrow(&sm.g2[i * LDG], sm.beta[i], i, xrow);
 #pragma unroll
-        for (int s2 = 0; s2 < 16; ++s2) {
-            const float2 l = sm.g2[i * LDG + s2];
-            xrow[s2] = s2 < i ? make_float2(-bi * l.x, -bi * l.y) : make_float2(0.f, 0.f);
+        for (int s2 = 0; s2 < 16; ++s2)
             fro = __builtin_fmaf(xrow[s2].x, xrow[s2].x, __builtin_fmaf(xrow[s2].y, xrow[s2].y, fro));
-        }
 #pragma unroll
         for (int k = 0; k < 4; ++k) { nr[k] = i == 4 * k + cg ? 1.f : 0.f; ni[k] = 0.f; }
         subst_steps(nr, ni, xrow, std::make_integer_sequence<int, 15>{});
