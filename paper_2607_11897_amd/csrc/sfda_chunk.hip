@@ -176,12 +176,13 @@ __device__ __forceinline__ void adjoint_chunk(ChunkSmem<C>& sm, const ChunkArgs&
 #pragma unroll
             for (int jb = rb; jb < NRB; ++jb) {
                 Frag8 a;
+                float2 xs[4];                                                        // A[jt][row]
+                lds_masked4([&](int r) { return sm.g2[row * LDG + jb * 16 + 4 * g + r]; },
+                            [&](int r) { return jb * 16 + 4 * g + r >= row; }, xs);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const int jt = jb * 16 + 4 * g + r;
-                    const float2 x = masked(jt >= row, pin(sm.g2[row * LDG + jt]));   // A[jt][row]
-                    a.v[2 * r] = x.x;
-                    a.v[2 * r + 1] = -x.y;
+                    a.v[2 * r] = xs[r].x;
+                    a.v[2 * r + 1] = -xs[r].y;
                 }
                 mma<P>(acc, a, br[jb]);
             }
@@ -199,11 +200,13 @@ __device__ __forceinline__ void adjoint_chunk(ChunkSmem<C>& sm, const ChunkArgs&
 #pragma unroll
             for (int kb = rb; kb < NRB; ++kb) {
                 Frag8 a;
+                float2 xs[4];                                                        // N[jt][row]
+                lds_masked4([&](int r) { return sm.g2[(kb * 16 + 4 * g + r) * LDG + row]; },
+                            [&](int r) { return kb * 16 + 4 * g + r > row; }, xs);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int jt = kb * 16 + 4 * g + r;
-                    float2 x = pin(sm.g2[jt * LDG + row]);                        // N[jt][row]
-                    x = jt > row ? x : make_float2(jt == row ? 1.f : 0.f, 0.f);
+                    const float2 x = jt == row ? make_float2(1.f, 0.f) : xs[r];
                     a.v[2 * r] = x.x;
                     a.v[2 * r + 1] = -x.y;
                 }
@@ -928,12 +931,12 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
         const Frag8 ta = tfrag(sm);
         Frag8 a3;
         if constexpr (MODE == 3) {
+            float2 xs[4];                                                     // L'_kr
+            lds_masked4([&](int r) { return sm.g3[c * LDG + 4 * g + r]; }, [&](int r) { return 4 * g + r < c; }, xs);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int jt = 4 * g + r;
-                const float2 x = masked(jt < c, pin(sm.g3[c * LDG + jt]));   // L'_kr
-                a3.v[2 * r] = x.x;
-                a3.v[2 * r + 1] = x.y;
+                a3.v[2 * r] = xs[r].x;
+                a3.v[2 * r + 1] = xs[r].y;
             }
         }
 #pragma unroll
@@ -1046,6 +1049,28 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
 
         // ---- O^* = conj(Q)G S + tril(A) Delta (column waves) | the next chunk's Gram products
         if (cols) {
+            // tril(A) row c (MODE 3: and tril(A_qr)), the same for every column block: A[c][jt]
+            // is stored transposed above the diagonal; read on every lane, then masked
+            auto tril_frag = [&](const float2* blk) __attribute__((always_inline)) {
+                float2 lo[4], dg = blk[c * LDG + c];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) lo[r] = blk[(4 * g + r) * LDG + c];
+                dg = pin(dg);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) lo[r] = pin(lo[r]);
+                Frag8 a;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int jt = 4 * g + r;
+                    const float2 x = jt < c ? lo[r] : jt == c ? dg : make_float2(0.f, 0.f);
+                    a.v[2 * r] = x.x;
+                    a.v[2 * r + 1] = x.y;
+                }
+                return a;
+            };
+            const Frag8 aA = tril_frag(cur.g2);
+            Frag8 aR;
+            if constexpr (MODE == 3) aR = tril_frag(cur.g3);
 #pragma unroll
             for (int w = 0; w < CBW; ++w) {
                 if (!active(w)) continue;
@@ -1062,27 +1087,8 @@ __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& a
                     }
                     mma<P>(acc, a, bfrag_from_acc(Sacc[w][kb], qp));
                 }
-                Frag8 a;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int jt = 4 * g + r;
-                    const float2 lo_p = pin(cur.g2[jt * LDG + c]), dg_p = pin(cur.g2[c * LDG + c]);
-                    const float2 x = masked(jt <= c, jt < c ? lo_p : dg_p);   // A[c][jt] (stored transposed)
-                    a.v[2 * r] = x.x;
-                    a.v[2 * r + 1] = x.y;
-                }
-                mma<P>(acc, a, bfrag_from_acc(U[w], qp));
-                if constexpr (MODE == 3) {            // + A_qr Delta_r
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int jt = 4 * g + r;
-                        const float2 lo_p = pin(cur.g3[jt * LDG + c]), dg_p = pin(cur.g3[c * LDG + c]);
-                        const float2 x = masked(jt <= c, jt < c ? lo_p : dg_p);
-                        a.v[2 * r] = x.x;
-                        a.v[2 * r + 1] = x.y;
-                    }
-                    mma<P>(acc, a, bvr[w]);
-                }
+                mma<P>(acc, aA, bfrag_from_acc(U[w], qp));
+                if constexpr (MODE == 3) mma<P>(acc, aR, bvr[w]);   // + A_qr Delta_r
                 if (!vset(w)) {                   // X_t = P_t^* q_t, [heads][T][m] complex fp32
                     if (j < m && args.xo != nullptr) {
 #pragma unroll

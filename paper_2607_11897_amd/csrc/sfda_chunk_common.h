@@ -77,6 +77,20 @@ struct ChunkArgs {
 
 __device__ __forceinline__ float sigmoid_acc(float x) { return 1.f / (1.f + expf(-x)); }
 
+// Four LDS entries at(r), r = 0..3, read on every lane -- each read issued before any is
+// waited for -- then kept where keep(r) and zero elsewhere.  (A read made conditional, or
+// pinned one at a time, is issued and waited for on its own.)
+template <typename AT, typename KEEP>
+__device__ __forceinline__ void lds_masked4(AT at, KEEP keep, float2 (&x)[4])
+{
+#pragma unroll
+    for (int r = 0; r < 4; ++r) x[r] = at(r);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) x[r] = pin(x[r]);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) x[r] = keep(r) ? x[r] : make_float2(0.f, 0.f);
+}
+
 template <int C>
 struct ChunkSmem {
     static constexpr int LDG = C + 1;

@@ -351,12 +351,13 @@ __global__ __launch_bounds__(GW * 64, C <= 16 ? 4 : 2) void grad_kernel(GradArgs
 #pragma unroll
                 for (int kb = 0; kb <= rb; ++kb) {
                     Frag8 a;
+                    float2 xs[4];
+                    lds_masked4([&](int r) { return sm.g2[row * LDG + kb * 16 + 4 * g + r]; },
+                                [&](int r) { return kb * 16 + 4 * g + r < row; }, xs);
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
-                        const int jt = kb * 16 + 4 * g + r;
-                        const float2 x = masked(jt < row, pin(sm.g2[row * LDG + jt]));
-                        a.v[2 * r] = x.x;
-                        a.v[2 * r + 1] = x.y;
+                        a.v[2 * r] = xs[r].x;
+                        a.v[2 * r + 1] = xs[r].y;
                     }
                     RC::mma(pw, RC::conv(a), dbf[kb]);
                 }
@@ -448,13 +449,19 @@ __global__ __launch_bounds__(GW * 64, C <= 16 ? 4 : 2) void grad_kernel(GradArgs
     auto cc_frag = [&](bool transposed_store, int row, int kb, int lo) {
         // lo: 0 -> jt < row, 1 -> jt <= row, 2 -> jt > row, 3 -> jt >= row
         Frag8 a;
+        float2 xs[4];
+        lds_masked4([&](int r) {
+                        const int jt = kb * 16 + 4 * g + r;
+                        return transposed_store ? sm.g2[jt * LDG + row] : sm.g2[row * LDG + jt];
+                    },
+                    [&](int r) {
+                        const int jt = kb * 16 + 4 * g + r;
+                        return lo == 0 ? jt < row : lo == 1 ? jt <= row : lo == 2 ? jt > row : jt >= row;
+                    }, xs);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const int jt = kb * 16 + 4 * g + r;
-            const bool ok = lo == 0 ? jt < row : lo == 1 ? jt <= row : lo == 2 ? jt > row : jt >= row;
-            const float2 x = masked(ok, pin(transposed_store ? sm.g2[jt * LDG + row] : sm.g2[row * LDG + jt]));
-            a.v[2 * r] = x.x;
-            a.v[2 * r + 1] = x.y;
+            a.v[2 * r] = xs[r].x;
+            a.v[2 * r + 1] = xs[r].y;
         }
         return RC::conv(a);
     };
