@@ -785,11 +785,13 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
 //   column waves:     -       | Delta   | O       | S update | U of c + 1 |  -
 //   preparing waves:  sums of c + 1 | operands | Gram | inverse | Wt tiles | Wt to LDS
 // (the column waves pass the load stage's inner barrier first, so the running sums of the
-// next chunk do not wait for Delta).  The stage functions take a thread index per role: the
-// preparing waves pass theirs less 256 (the first 256 "threads"), the column waves theirs
-// plus 256 (past the workers, so they only take part in the stages' barriers).  MODE 3 is
-// the write-decoupled forward (as in chunk_scan: R / G, the k-r and q-r Gram blocks and the
-// write rows Delta_r = D_beta conj(V) join the same stages).
+// next chunk do not wait for Delta; the inverse is shared by two preparing waves and kept
+// apart from L').  The stage functions take a thread index per role: the preparing waves pass
+// theirs less 256 (the first 256 "threads"), the column waves theirs plus 256 (past the
+// workers, so they only take part in the stages' barriers).  MODE 3 is the write-decoupled
+// forward (as in chunk_scan: R / G, the k-r and q-r Gram blocks -- formed beside the
+// inverse -- and the write rows Delta_r = D_beta conj(V) join the same stages); MODE 4 the
+// segment forward (two column sets per column wave, below).
 template <int P, typename TIN, typename TOUT, bool GATED, int MODE, typename SM>
 __device__ __forceinline__ void chunk_scan_pipe(SM (&sms)[2], const ChunkArgs& args, unsigned block, long heads)
 {
