@@ -338,10 +338,8 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
         lds_poison(&sm, sizeof(SM), tid, NW * 64);
         __syncthreads();
 #endif
-        // MODE 2: this wave's dL/do entries of the chunk, requested first so that they arrive
-        // during the load, Gram and inverse stages (tokens past T lie past the chunk's rows)
         typename RawC<TOUT>::W dor[CBW][NRB][4];
-        if constexpr (MODE == 2) {
+        auto load_dor = [&]() __attribute__((always_inline)) {
             const rsrc_t ro = buf(static_cast<const TOUT*>(args.dO) + 2 * (base_tn + static_cast<long>(t0) * n),
                                   static_cast<long>(min(C, T - t0)) * n * 2 * sizeof(TOUT));
 #pragma unroll
@@ -355,7 +353,7 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
                         dor[w][kb][r] = RawC<TOUT>::load(ro, j < n ? static_cast<uint32_t>((tl * n + j) * 2 * sizeof(TOUT)) : OOR);
                     }
             }
-        }
+        };
         if constexpr (MODE == 1 || MODE == 2) {
             // this wave's share of the chunk's [m][n] record: the state entering it (MODE 1)
             // or the adjoint of the state leaving it (MODE 2)
@@ -404,6 +402,10 @@ __device__ __forceinline__ void chunk_scan(SM& sm, const ChunkArgs& args, unsign
         if constexpr (PRE)
             if (it_ch + 1 < nchunks)
                 prefetch_inputs<TIN, C, true, MODE == 3>(args, bh, (MODE == 2 ? ch - 1 : ch + 1) * C, tid, pf);
+        // MODE 2: this wave's dL/do entries of the chunk, requested after the load stage (whose
+        // waits for the prefetched inputs would otherwise cover them too) and used by the
+        // adjoint two stages later (tokens past T lie past the chunk's rows)
+        if constexpr (MODE == 2) load_dor();
         __syncthreads();
 
         // ============================================================ G: L' and A
