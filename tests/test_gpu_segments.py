@@ -97,6 +97,27 @@ def test_segmented_f32_in_bf16_out(m, n, G):
     assert eo <= 2e-2 and es <= 1e-4
 
 
+@pytest.mark.parametrize("dtype,G", [("f32", 4), ("bf16", 8)])
+def test_segmented_strong_decay(dtype, G):
+    """alpha ~ U(0.02, 0.1): a segment's transfer decays to far below the float range (its
+    product P_g and the readouts X_t underflow to zero after a few chunks) and each 16-token
+    block stays inside it; o and S_T within the bars (float32: the segment forward and the
+    join; bfloat16: three passes)."""
+    import math
+    laws = I.Laws(alpha=("uniform", 0.02, 0.1), theta=("uniform", -math.pi, math.pi),
+                  beta=("uniform", 0.0, 1.0), s0_scale=0.1)
+    w = I.Workload("seg_strong", 1, 2, 512, 64, 48, 16, dtype, laws, 23, 1e-4)
+    x = I.make_chunk_inputs(w)
+    say(dtype, "strong decay, G", G)
+    o, S = run(x, 16, G)
+    o_ref, S_ref = run_oracle(x)
+    eo, es = rel_err(o, o_ref), rel_err(S, S_ref)
+    say("err(o)", eo, "err(S_T)", es)
+    tol = 1e-4 if dtype == "f32" else 2e-2
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(S))
+    assert eo <= tol and es <= tol
+
+
 def test_segmented_zero_state_and_in_place():
     x = make(1, 2, 128, 64, 64, 16, zero_state=True)
     o, S = run(x, 16, 4)
