@@ -767,7 +767,7 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                 const float es = s3 ? 1.f : ps;                                // exclusive suffix
                 tpk[k] = __builtin_amdgcn_fractf(pt3);
                 Pf[0][k] = em * m0; Pf[1][k] = em * m1; Pf[2][k] = em * m2; Pf[3][k] = em * m3;
-                Qb[0][k] = es * x0; Qb[1][k] = es * x1; Qb[2][k] = es * x2; Qb[3][k] = es;
+                if constexpr (!GATED) { Qb[0][k] = es * x0; Qb[1][k] = es * x1; Qb[2][k] = es * x2; Qb[3][k] = es; }
 #pragma unroll
                 for (int u = 0; u < 4; ++u) ph[u][k] = ep + lp[u];
                 dtot[k] = D;
@@ -844,7 +844,10 @@ __global__ __launch_bounds__(NTH, 1) void chunk_pipe_kernel(Args args)
                     const float qur = __builtin_fmaf(qr, cs, qi * sn), qui = __builtin_fmaf(qr, sn, -qi * cs);
                     const float kur = __builtin_fmaf(kr, cs, ki * sn), kui = __builtin_fmaf(kr, sn, -ki * cs);
                     const float P = Pf[u][k];
-                    const float Pk = P * kinv[u], Qk = Qb[u][k] * kinv[u];
+                    // gated: Q_t = D / P_t (alpha >= alpha_min keeps P_t a normal float), which
+                    // frees the suffix products' registers
+                    const float Qt = GATED ? dtot[k] * __builtin_amdgcn_rcpf(P) : Qb[u][k];
+                    const float Pk = P * kinv[u], Qk = Qt * kinv[u];
                     const float Dk = Qk * invd[k];             // 1 / P_t (= Q_t / D), times kinv
                     wq[k] = pack_bf16(qur * P, qui * P);
                     wk[k] = pack_bf16(kur * Pk, kui * Pk);
