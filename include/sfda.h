@@ -87,20 +87,22 @@ typedef void* sfda_stream_t;
  *   C in {16, 32, 64, 128} (SFDA_ERR_CHUNK otherwise).  The last chunk may be ragged
  *   (T mod C != 0).
  *   Chunk length: C fixes the paper's chunking; the result does not depend on it (Thm 6.1,
- *   up to rounding), and the kernels choose their own blocking.  bf16 inputs run 64-token
- *   steps of four 16-token blocks for every C (bitwise the same result for every C);
- *   float32 inputs run 16-token chunks for every C.
+ *   up to rounding), and the kernels choose their own blocking.  bf16 inputs with m > 4 run
+ *   64-token steps of four 16-token blocks for every C (bitwise the same result for every
+ *   C); float32 inputs, and bf16 inputs with m <= 4, run 16-token chunks for every C.
  *   Numerical range (App. C.4, local renormalisation): the decay is referenced to the start
  *   of each aligned 16-token block (tokens 16 j .. 16 j + 15), so the kernels divide by at
  *   most the decay over part of one block.  The result is exact to rounding for every
  *   alpha in (0, 1] whose product over each aligned 16-token block, per channel, is at
  *   least 2^-126 (e.g. any alpha >= 0.0043; alpha may be exactly 1 or vary per channel and
  *   token; the decay over longer stretches is unbounded).  Past that the outputs are NaN
- *   rather than wrong: with bf16 inputs from the 64-token step holding such a block on,
- *   with float32 inputs from the first token whose block decay so far is below 2^-126 (its
+ *   rather than wrong: with bf16 inputs (m > 4) from the 64-token step holding such a block
+ *   on, otherwise from the first token whose block decay so far is below 2^-126 (its
  *   16-token chunk's earlier rows may be NaN too); S_T is NaN in both cases.
- *   Accumulation and state are float32 for both dtypes; with in_dtype == SFDA_BF16 the
- *   matrix products take bfloat16 operands, and each head's share of q, k, v and o must
+ *   Accumulation and state are float32 for both dtypes; with in_dtype == SFDA_BF16 and
+ *   m > 4 the matrix products take bfloat16 operands (with m <= 4 they take float32 ones:
+ *   there 1 - beta |k|^2 can sit near 0, and the erase factor would amplify the operand
+ *   rounding of bfloat16 past its own precision); each head's share of q, k, v and o must
  *   stay below 2 GiB (T * max(m, n) * 2 * sizeof(out element) < 2^31; SFDA_ERR_SHAPE
  *   otherwise).
  */
@@ -309,7 +311,7 @@ const char* sfda_status_string(sfda_status_t s);
  * for every 16-token block of every head (the blocking of the chunk kernels), the
  * triangular solve that forms N = (I + D_beta L')^{-1} is repeated exactly as the float32
  * path's kernels do it (same load stage, Gram products and substitution; with bfloat16
- * inputs the Gram products take bfloat16 operands, as in the backward's scans), and
+ * inputs and m > 4 the Gram products take bfloat16 operands, as in the backward's scans), and
  *   residual[b, h, blk] = max_ij |((I + D_beta L') N - I)_ij|   (on the L' it used)
  *   lnorm[b, h, blk]    = ||D_beta L'||_F   (an upper bound of the spectral norm)
  * are written, float32, [B, H, ceil(T / 16)].  L'[t, j] = k_t^* diag(g_t / g_j) k_j for j < t

@@ -1251,7 +1251,10 @@ static hipError_t launch_chunk_t(const ChunkLaunch& L, hipStream_t st)
 
 hipError_t launch_chunk(const ChunkLaunch& L, hipStream_t st)
 {
-    if (L.in_bf16) return launch_chunk_bf16(L, st);
+    if (bf16_operands(L.in_bf16, L.m)) return launch_chunk_bf16(L, st);
+    if (L.in_bf16)              // a few key channels: this kernel with fp32 operands
+        return L.out_bf16 ? launch_chunk_t<PREC_F32, uint16_t, uint16_t>(L, st)
+                          : launch_chunk_t<PREC_F32, uint16_t, float>(L, st);
     return L.out_bf16 ? launch_chunk_t<PREC_F32, float, uint16_t>(L, st)
                       : launch_chunk_t<PREC_F32, float, float>(L, st);
 }
@@ -1284,9 +1287,12 @@ static hipError_t launch_dec_t(const ChunkLaunch& L, hipStream_t st)
 // the write-decoupled forward; bf16 inputs take bf16 matrix-core operands
 hipError_t launch_chunk_decoupled(const ChunkLaunch& L, hipStream_t st)
 {
-    if (L.in_bf16)
+    if (bf16_operands(L.in_bf16, L.m))
         return L.out_bf16 ? launch_dec_t<PREC_BF16, uint16_t, uint16_t>(L, st)
                           : launch_dec_t<PREC_BF16, uint16_t, float>(L, st);
+    if (L.in_bf16)
+        return L.out_bf16 ? launch_dec_t<PREC_F32, uint16_t, uint16_t>(L, st)
+                          : launch_dec_t<PREC_F32, uint16_t, float>(L, st);
     return L.out_bf16 ? launch_dec_t<PREC_F32, float, uint16_t>(L, st) : launch_dec_t<PREC_F32, float, float>(L, st);
 }
 
@@ -1393,15 +1399,19 @@ static hipError_t launch_monitor_t(const ChunkLaunch& L, float* residual, float*
 
 hipError_t launch_solve_monitor(const ChunkLaunch& L, float* residual, float* lnorm, hipStream_t st)
 {
-    return L.in_bf16 ? launch_monitor_t<PREC_BF16, uint16_t>(L, residual, lnorm, st)
+    if (bf16_operands(L.in_bf16, L.m)) return launch_monitor_t<PREC_BF16, uint16_t>(L, residual, lnorm, st);
+    return L.in_bf16 ? launch_monitor_t<PREC_F32, uint16_t>(L, residual, lnorm, st)
                      : launch_monitor_t<PREC_F32, float>(L, residual, lnorm, st);
 }
 
 hipError_t launch_bwd_scans(const ChunkLaunch& F, const ChunkLaunch& A, hipStream_t st)
 {
-    if (F.in_bf16)
+    if (bf16_operands(F.in_bf16, F.m))
         return A.out_bf16 ? launch_scans_t<PREC_BF16, uint16_t, uint16_t>(F, A, st)
                           : launch_scans_t<PREC_BF16, uint16_t, float>(F, A, st);
+    if (F.in_bf16)
+        return A.out_bf16 ? launch_scans_t<PREC_F32, uint16_t, uint16_t>(F, A, st)
+                          : launch_scans_t<PREC_F32, uint16_t, float>(F, A, st);
     return A.out_bf16 ? launch_scans_t<PREC_F32, float, uint16_t>(F, A, st)
                       : launch_scans_t<PREC_F32, float, float>(F, A, st);
 }

@@ -235,8 +235,13 @@ __global__ __launch_bounds__(GW * 64, C <= 16 ? 4 : 2) void grad_kernel(GradArgs
             for (int r = 0; r < 4; ++r) {
                 const uint32_t e = static_cast<uint32_t>((rb * 16 + 4 * g + r) * n + jv);
                 const uint32_t off = vok ? e * 2 * static_cast<uint32_t>(sizeof(TIN)) : OOR;
-                if constexpr (P == PREC_BF16) x.v[rb][r] = __builtin_amdgcn_raw_buffer_load_b32(rV, off, 0, 0);
-                else x.v[rb][r] = ld_c64(rV, off);
+                if constexpr (sizeof(TIN) == 2) {          // a complex bf16 pair
+                    const uint32_t w = __builtin_amdgcn_raw_buffer_load_b32(rV, off, 0, 0);
+                    if constexpr (P == PREC_BF16) x.v[rb][r] = w;
+                    else x.v[rb][r] = make_float2(__uint_as_float(w << 16), __uint_as_float(w & 0xFFFF0000u));
+                } else {
+                    x.v[rb][r] = ld_c64(rV, off);
+                }
             }
     };
     // put also adds the block's share of dL/dg_C's first part, rowsum(G * conj(S)) from the
@@ -711,9 +716,12 @@ static hipError_t launch_grad_t(const GradLaunch& L, hipStream_t st)
 hipError_t launch_chunk_grad(const GradLaunch& L, hipStream_t st)
 {
     // bf16 inputs take bf16 matrix-core operands (fp32 accumulation and records)
-    if (L.in_bf16)
+    if (bf16_operands(L.in_bf16, L.m))
         return L.out_bf16 ? launch_grad_t<PREC_BF16, uint16_t, uint16_t>(L, st)
                           : launch_grad_t<PREC_BF16, uint16_t, float>(L, st);
+    if (L.in_bf16)          // a few key channels: fp32 operands
+        return L.out_bf16 ? launch_grad_t<PREC_F32, uint16_t, uint16_t>(L, st)
+                          : launch_grad_t<PREC_F32, uint16_t, float>(L, st);
     return L.out_bf16 ? launch_grad_t<PREC_F32, float, uint16_t>(L, st) : launch_grad_t<PREC_F32, float, float>(L, st);
 }
 

@@ -57,6 +57,13 @@ struct GradLaunch {
     bool in_bf16, out_bf16;
 };
 
+// bfloat16 inputs with at most this many key channels take float32 matrix-core operands:
+// with one or two channels the erase factor (1 - beta |k|^2) can come close to zero, and the
+// cancellation in (I - beta k k^*) S then magnifies the rounding of bf16 operands past the
+// bf16 bar (fp32 operands keep it near the fp32 level); at these sizes the cost is nil
+constexpr int SMALL_M_FP32_OPERANDS = 4;
+inline bool bf16_operands(bool in_bf16, int m) { return in_bf16 && m > SMALL_M_FP32_OPERANDS; }
+
 struct GateParams {
     bool gated;
     float alpha_min, alpha_max, theta_max, eps;
