@@ -27,7 +27,8 @@ def _cases():
     return out
 
 
-CASES = _cases()
+# bfloat16 either side of the operand switch (at most four key channels: float32 operands)
+CASES = _cases() + [(4, 24, 65, 64, "bf16"), (5, 24, 65, 64, "bf16"), (4, 13, 33, 16, "bf16"), (5, 13, 33, 16, "bf16")]
 
 
 @pytest.fixture(scope="module", autouse=True)
